@@ -1,0 +1,107 @@
+/*
+ * fgq_oracle.h -- plain CPU oracle for Fine-Grained Quantization (FGQ)
+ * inference (Mellempudi et al., "Ternary Neural Networks with Fine-Grained
+ * Quantization", arXiv 1705.01462).
+ *
+ * TEST INFRASTRUCTURE ONLY.  Nothing in the product path may include, link or
+ * call this code; only the tests, the smoke check and the CPU-baseline leg of
+ * the benchmark use it.  It shares no code, header, table or helper with the
+ * HIP library.
+ *
+ * What it computes, each function citing the passage it follows:
+ *   orc_ternarize     Sec. 3 threshold rule + Eq. (1) objective, solved per
+ *                     group (Sec. 3.1, Eq. (2)) with the symmetric closed form
+ *                     of Eq. (5) by exhaustive search over the thresholds
+ *                     (the "brute-force" solve of Sec. 3.1 / Sec. 4); groups
+ *                     are N consecutive input channels at a fixed filter tap
+ *                     (Sec. 3.2, Fig. 2).  Method 1 is Lemma 1 (Delta = mean|W|).
+ *   orc_pack_codes    2-bit storage of ternary codes (4 per byte).
+ *   orc_quantize_act  activations quantized to 8 or 4 bits with one scale per
+ *                     tensor (Sec. 4, experimental setup).
+ *   orc_group_sums    exact integer partial sums P_g = sum_{i in g} t_i q_i
+ *                     (Sec. 4: 32-bit accumulation).
+ *   orc_conv2d        y = s_x * sum_g alpha_g * P_g for an implicit-GEMM conv
+ *   orc_gemm          (Sec. 3.1 Eq. (2) applied to a layer; one multiply per
+ *                     group, Sec. 4 Discussion).
+ *
+ * Parity status: ternarize, quantize, group sums, conv2d and gemm are pinned
+ * by the tests (brute-force enumeration, Lemma 1 statistics, closed forms,
+ * reduction to a library convolution); see tests/test_oracle_*.py.
+ *
+ * Conventions (shared with the library only by specification, not by code):
+ *   weights   fp32 [O][C][R][S]
+ *   codes     2-bit, reduction index k = (r*S + s)*C + c, row o holds
+ *             ceil(K/4) bytes; element k sits in bits [2(k%4), 2(k%4)+1] of
+ *             byte k/4; 00 -> 0, 01 -> +1, 11 -> -1 (10 never written)
+ *   alpha     fp32 [O][K/G], group g = k / G
+ *   acts      NHWC, u8 one per byte or u4 two per byte (even element in the
+ *             low nibble)
+ *   output    fp32 NHWC [B][Ho][Wo][O] (GEMM: [M][O])
+ */
+#ifndef FGQ_ORACLE_H
+#define FGQ_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+  ORC_OK = 0,
+  ORC_ERR_NULL = 1,
+  ORC_ERR_SHAPE = 2,
+  ORC_ERR_GROUP = 3,
+  ORC_ERR_BITS = 4,
+  ORC_ERR_NONFINITE = 5
+};
+
+enum { ORC_TERN_EXACT = 0, ORC_TERN_EXP_LEMMA = 1 };
+
+/* One group of n weights read at w[i*stride].  Writes t[i*tstride] in
+ * {-1,0,1}, *alpha, *delta.  Returns ORC_ERR_NONFINITE on NaN/Inf. */
+int orc_ternarize_group(const float* w, int64_t n, int64_t stride, int method,
+                        int8_t* t, int64_t tstride, float* alpha, float* delta);
+
+/* Whole layer.  t is [O][R][S][C] (unpacked codes), alpha/delta [O][K/G]. */
+int orc_ternarize(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
+                  int32_t G, int32_t method, int8_t* t, float* alpha,
+                  float* delta);
+
+/* 2-bit packing / unpacking of an [O][K] code matrix. */
+void orc_pack_codes(const int8_t* t, int64_t O, int64_t K, uint8_t* codes);
+void orc_unpack_codes(const uint8_t* codes, int64_t O, int64_t K, int8_t* t);
+
+/* Quantize n fp32 values to bits (8|4).  scale_in may be NULL (dynamic
+ * scale s = max(max x, 0)/qmax, or 1 if that is 0).  q holds n bytes (bits=8)
+ * or n/2 bytes (bits=4, n even).  *scale_out receives s. */
+int orc_quantize_act(const float* x, int64_t n, int32_t bits,
+                     const float* scale_in, uint8_t* q, float* scale_out);
+
+/* Exact group sums for output rows [row0, row0+nrows) of a conv:
+ * P[(row-row0)][o][g], int32. */
+int orc_group_sums_conv(const uint8_t* q, int32_t bits, int64_t B, int64_t H,
+                        int64_t W, int64_t C, const uint8_t* codes, int64_t O,
+                        int32_t R, int32_t S, int32_t sh, int32_t sw,
+                        int32_t ph, int32_t pw, int32_t G, int64_t row0,
+                        int64_t nrows, int32_t* P);
+
+/* y[m][o] = fp32( s_x * sum_g alpha[o][g] * P[m][o][g] ), fp64 sum.
+ * Rows [row0, row0+nrows) only (nrows < 0: all rows); y is indexed by the
+ * absolute row.  nthreads <= 0: OpenMP default. */
+int orc_conv2d(const uint8_t* q, int32_t bits, float sx, int64_t B, int64_t H,
+               int64_t W, int64_t C, const uint8_t* codes, const float* alpha,
+               int64_t O, int32_t R, int32_t S, int32_t sh, int32_t sw,
+               int32_t ph, int32_t pw, int32_t G, int64_t row0, int64_t nrows,
+               int32_t nthreads, float* y);
+
+int orc_gemm(const uint8_t* q, int32_t bits, float sx, int64_t M, int64_t K,
+             const uint8_t* codes, const float* alpha, int64_t O, int32_t G,
+             int32_t nthreads, float* y);
+
+int orc_max_threads(void);
+
+#ifdef __cplusplus
+}
+#endif
+#endif
