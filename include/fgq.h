@@ -1,0 +1,214 @@
+/*
+ * fgq.h -- C ABI of libfgq.so: Fine-Grained Quantization (FGQ) ternary
+ * inference on AMD Instinct MI355X (gfx950).
+ *
+ * Method: Mellempudi et al., "Ternary Neural Networks with Fine-Grained
+ * Quantization" (arXiv 1705.01462).  Weights are ternarized in groups of G
+ * consecutive input channels at each filter tap (Sec. 3.2, Fig. 2); every
+ * group carries its own fp32 scale alpha and ternary codes t in {-1,0,+1}
+ * (Sec. 3, Eq. (5)); activations are quantized to unsigned 8 or 4 bits with
+ * one scale s_x per tensor (Sec. 4); a layer computes
+ *
+ *     y[m][o] = s_x * sum_g alpha[o][g] * P[m][o][g],
+ *     P[m][o][g] = sum_{k in group g} t[o][k] * q[m][k]      (exact integer)
+ *
+ * (Eq. (2) applied to a convolution or fully-connected layer; one multiply
+ * per group of G accumulations, Sec. 4 Discussion).
+ *
+ * General conventions
+ *  - Every tensor pointer is a DEVICE pointer owned by the caller; the
+ *    library never allocates, frees or keeps device memory of its own.
+ *  - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *    Calls enqueue work on it and return without waiting, except
+ *    fgq_ternarize, which synchronizes the stream (offline preparation that
+ *    must report non-finite weights).
+ *  - Arguments are validated on the host before anything is enqueued; on
+ *    any error nothing is launched and the outputs are untouched.
+ *  - No C++ exception crosses this interface.  Calls on distinct streams
+ *    with distinct buffers are thread-safe.
+ *  - Shapes are int64 and must be positive unless stated otherwise.
+ *
+ * Layouts
+ *  - Weights (input of fgq_ternarize): fp32 [O][C][R][S].
+ *  - Reduction index k = (r*S + s)*C + c, K = R*S*C (a GEMM is a 1x1 conv,
+ *    K = C).  Group g = k / G; G must divide C, so a group never straddles
+ *    two taps.
+ *  - Codes: 2 bits per weight, row o holds fgq_codes_bytes(1, K) bytes;
+ *    weight k sits in bits [2(k%4), 2(k%4)+1] of byte k/4 of its row;
+ *    00 = 0, 01 = +1, 11 = -1; 10 is never written.  Bits past K in the
+ *    last byte of a row are zero.
+ *  - alpha (and delta): fp32 [O][K/G].
+ *  - Activations q: NHWC.  bits=8: one uint8 per value.  bits=4: two values
+ *    per byte, element 2j in the low nibble, 2j+1 in the high nibble; C must
+ *    then be even.  Real value = s_x * q, with no zero point.
+ *  - Output y: fp32 NHWC [B][Ho][Wo][O] (GEMM: [M][O]),
+ *    Ho = (H + 2*pad_h - R)/stride_h + 1, Wo likewise; out-of-image taps
+ *    read q = 0.
+ *  - s_x is a device fp32 scalar so that quantize -> conv needs no host sync.
+ */
+#ifndef FGQ_H
+#define FGQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t fgq_status;
+enum {
+  FGQ_OK = 0,
+  FGQ_ERR_NULL = 1,        /* a required pointer is NULL */
+  FGQ_ERR_SHAPE = 2,       /* non-positive or inconsistent sizes */
+  FGQ_ERR_GROUP = 3,       /* G < 1 or G does not divide C (or K) */
+  FGQ_ERR_BITS = 4,        /* bits not 8|4, or odd C / n with bits=4 */
+  FGQ_ERR_NONFINITE = 5,   /* fgq_ternarize met NaN or Inf weights */
+  FGQ_ERR_HIP = 6,         /* HIP runtime error (also: no device) */
+  FGQ_ERR_UNSUPPORTED = 7, /* method or path not available for the shape */
+  FGQ_ERR_WORKSPACE = 8    /* workspace missing or too small */
+};
+
+/* Ternarization methods of fgq_ternarize. */
+enum {
+  FGQ_TERN_EXACT = 0,     /* Eq. (5) solved exactly by exhaustive threshold
+                             search (the brute-force solve of Sec. 3.1/4) */
+  FGQ_TERN_EXP_LEMMA = 1  /* Lemma 1: Delta = mean |w| of the group */
+};
+
+/* Human-readable name of a status code (static string, never NULL). */
+const char* fgq_status_string(fgq_status s);
+
+/* Interface version; bumped on any incompatible change of this header. */
+int32_t fgq_abi_version(void);
+
+/* Number of visible HIP devices (0 when none or on runtime error). */
+int32_t fgq_device_count(void);
+
+/* Bytes of the 2-bit code array of an [O][K] weight matrix: O*ceil(K/4). */
+size_t fgq_codes_bytes(int64_t O, int64_t K);
+
+/* Number of groups O*K/G, or -1 when G does not divide K. */
+int64_t fgq_group_count(int64_t O, int64_t K, int32_t G);
+
+/*
+ * fgq_ternarize -- per-group threshold Delta and scale alpha (Sec. 3, Eq. (1);
+ * Sec. 3.1, Eq. (2) and Eq. (5); Lemma 1 for method 1), packed to codes.
+ *
+ * For each group of G weights w (G consecutive input channels at one (o,r,s),
+ * Sec. 3.2): with magnitudes sorted in decreasing order (ties by channel),
+ * S_j the fp64 sum of the j largest non-zero magnitudes and f_j = S_j^2 / j,
+ * the kept count J is the first j maximising f_j; alpha = fp32(S_J / J),
+ * Delta = the (J+1)-th largest magnitude (0 if all are kept), t = sign(w) on
+ * the J largest and 0 elsewhere.  An all-zero group gets alpha = Delta = 0.
+ * Method FGQ_TERN_EXP_LEMMA: Delta = fp32(mean |w|), kept iff |w| > Delta,
+ * alpha = fp32(mean of the kept magnitudes) (0 if none).
+ *
+ * w      [in]  fp32 [O][C][R][S]
+ * codes  [out] fgq_codes_bytes(O, R*S*C) bytes, layout above
+ * alpha  [out] fp32 [O][R*S*C/G]
+ * delta  [out] fp32 [O][R*S*C/G], or NULL if not wanted
+ * Synchronizes `stream`.  Returns FGQ_ERR_NONFINITE if any weight is NaN or
+ * Inf (outputs are then unspecified).
+ */
+fgq_status fgq_ternarize(const float* w, int64_t O, int64_t C, int32_t R,
+                         int32_t S, int32_t G, int32_t method, uint8_t* codes,
+                         float* alpha, float* delta, void* stream);
+
+/*
+ * fgq_quantize_act -- activations to unsigned `bits` (8 or 4) with one scale
+ * per tensor (Sec. 4: activations quantized before each convolution).
+ *
+ * s = *scale_in if scale_in is not NULL (it must hold a positive finite
+ * value), else s = max(max_i x_i, 0) / qmax in fp32 (s = 1 when that max is
+ * 0), qmax = 255 or 15.  q_i = min(max(rint(x_i / s), 0), qmax) with IEEE
+ * division and round-half-even; NaN maps to 0.  s is written to *scale_out.
+ *
+ * x         [in]  fp32, n values (for a conv input: NHWC, n = B*H*W*C)
+ * q         [out] n bytes (bits=8) or n/2 bytes (bits=4, n even)
+ * scale_out [out] device fp32 scalar
+ * ws        [tmp] device workspace of fgq_quantize_ws_bytes(n) bytes, needed
+ *                 only when scale_in is NULL (dynamic scale); not kept.
+ */
+size_t fgq_quantize_ws_bytes(int64_t n);
+fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits,
+                            const float* scale_in, uint8_t* q,
+                            float* scale_out, void* ws, size_t ws_bytes,
+                            void* stream);
+
+/*
+ * fgq_prepare_weights -- per-layer constants for the folded-scale kernels
+ * (built once per layer, like the ternarization itself).
+ *
+ * The group scales are brought to one fixed-point grid per output channel:
+ * A[o][g] = rint(alpha[o][g] * 2^E_o), with E_o the largest exponent keeping
+ * every A of the channel within 127*(1 + 255 + 255^2), written as three
+ * balanced base-255 digits in [-127, 127].  The folded weights t*digit are
+ * int8, so the layer runs as three exact int8 products whose integer sums
+ * are combined exactly; only the rounding of alpha to the grid (relative
+ * step below 1.21e-7 of the channel's largest alpha) and one final
+ * fp32 rounding differ from the exact formula.
+ *
+ * codes, alpha  [in]  as produced by fgq_ternarize for an [O][K] layer
+ * prepared      [out] device buffer of fgq_prepared_bytes(O, K, G) bytes,
+ *                     256-byte aligned; opaque; read by fgq_conv2d/fgq_gemm.
+ */
+size_t fgq_prepared_bytes(int64_t O, int64_t K, int32_t G);
+fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha,
+                               int64_t O, int64_t K, int32_t G, void* prepared,
+                               size_t prepared_bytes, void* stream);
+
+/*
+ * fgq_conv2d -- FGQ convolution as an implicit GEMM (Sec. 3.2 grouping;
+ * Sec. 4 low-precision pipeline with 32-bit integer accumulation):
+ * y[b][ho][wo][o] = s_x * sum_g alpha[o][g] * P_g with the group sums P_g
+ * taken over the input window of output pixel (b, ho, wo).
+ *
+ * q        [in]  activations NHWC [B][H][W][C], bits 8 or 4 (layout above)
+ * sx       [in]  device fp32 scalar s_x (e.g. fgq_quantize_act's scale_out)
+ * codes    [in]  2-bit codes of the [O][R][S][C] weights
+ * alpha    [in]  fp32 [O][K/G]
+ * prepared [in]  NULL, or the output of fgq_prepare_weights for these
+ *                codes/alpha/O/K/G.  NULL selects the direct per-group
+ *                kernels: exact int32 group sums and an fp32 (G >= 64 with
+ *                K a multiple of 64: int8 matrix cores) or fp64 (otherwise)
+ *                alpha epilogue.  Non-NULL selects the folded-scale int8
+ *                matrix-core kernel (any G).
+ * y        [out] fp32 [B][Ho][Wo][O]
+ */
+fgq_status fgq_conv2d(const uint8_t* q, int32_t bits, const float* sx,
+                      int64_t B, int64_t H, int64_t W, int64_t C,
+                      const uint8_t* codes, const float* alpha,
+                      const void* prepared, int64_t O, int32_t R, int32_t S,
+                      int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                      int32_t pad_w, int32_t G, float* y, void* stream);
+
+/*
+ * fgq_gemm -- FGQ fully-connected layer, y[m][o] = s_x * sum_g alpha[o][g] *
+ * sum_{k in g} t[o][k] q[m][k]; identical to fgq_conv2d with B=1, H=M, W=1,
+ * C=K, R=S=1.  q is [M][K] (bits=4: K even); y is [M][O].
+ */
+fgq_status fgq_gemm(const uint8_t* q, int32_t bits, const float* sx,
+                    int64_t M, int64_t K, const uint8_t* codes,
+                    const float* alpha, const void* prepared, int64_t O,
+                    int32_t G, float* y, void* stream);
+
+/*
+ * fgq_group_sums -- the exact integer group sums P[m][o][g] (Sec. 4: 32-bit
+ * accumulation) of fgq_conv2d's geometry for output rows m in
+ * [row0, row0 + nrows), m = (b*Ho + ho)*Wo + wo.
+ *
+ * P [out] int32 [nrows][O][K/G]
+ */
+fgq_status fgq_group_sums(const uint8_t* q, int32_t bits, int64_t B,
+                          int64_t H, int64_t W, int64_t C,
+                          const uint8_t* codes, int64_t O, int32_t R,
+                          int32_t S, int32_t stride_h, int32_t stride_w,
+                          int32_t pad_h, int32_t pad_w, int32_t G,
+                          int64_t row0, int64_t nrows, int32_t* P,
+                          void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* FGQ_H */

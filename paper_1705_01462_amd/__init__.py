@@ -1,0 +1,200 @@
+"""Python binding of libfgq.so (FGQ ternary inference on MI355X / gfx950).
+
+Thin ctypes marshalling over the C ABI declared in include/fgq.h: every
+function below has the name of the C entry point it calls, checks device,
+dtype and contiguity, allocates outputs with torch (device memory only) and
+passes raw pointers plus torch's current HIP stream.  No arithmetic of the
+method happens here; there is no CPU fallback -- if the library is missing,
+importing the call raises.
+"""
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libfgq.so")
+
+FGQ_TERN_EXACT = 0
+FGQ_TERN_EXP_LEMMA = 1
+
+_STATUS = {0: "FGQ_OK", 1: "FGQ_ERR_NULL", 2: "FGQ_ERR_SHAPE", 3: "FGQ_ERR_GROUP",
+           4: "FGQ_ERR_BITS", 5: "FGQ_ERR_NONFINITE", 6: "FGQ_ERR_HIP",
+           7: "FGQ_ERR_UNSUPPORTED", 8: "FGQ_ERR_WORKSPACE"}
+
+
+class FgqError(RuntimeError):
+    def __init__(self, code, where):
+        super().__init__(f"{where}: {_STATUS.get(code, code)}")
+        self.code = code
+
+
+_lib = None
+_P = ctypes.c_void_p
+_I32 = ctypes.c_int32
+_I64 = ctypes.c_int64
+_SZ = ctypes.c_size_t
+
+_SIGS = {
+    "fgq_status_string": ([_I32], ctypes.c_char_p),
+    "fgq_abi_version": ([], _I32),
+    "fgq_device_count": ([], _I32),
+    "fgq_codes_bytes": ([_I64, _I64], _SZ),
+    "fgq_group_count": ([_I64, _I64, _I32], _I64),
+    "fgq_ternarize": ([_P, _I64, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P], _I32),
+    "fgq_quantize_ws_bytes": ([_I64], _SZ),
+    "fgq_quantize_act": ([_P, _I64, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
+    "fgq_prepared_bytes": ([_I64, _I64, _I32], _SZ),
+    "fgq_prepare_weights": ([_P, _P, _I64, _I64, _I32, _P, _SZ, _P], _I32),
+    "fgq_conv2d": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
+                    _I32, _I32, _I32, _I32, _I32, _P, _P], _I32),
+    "fgq_gemm": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _P, _P], _I32),
+    "fgq_group_sums": ([_P, _I32, _I64, _I64, _I64, _I64, _P, _I64, _I32, _I32, _I32, _I32,
+                        _I32, _I32, _I32, _I64, _I64, _P, _P], _I32),
+}
+
+
+def lib():
+    """The loaded libfgq.so (raises if it has not been built)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"libfgq.so not found at {LIB_PATH}; run __graft_entry__.build() "
+                               "(hipcc --offload-arch=gfx950) first")
+        L = ctypes.CDLL(LIB_PATH)
+        for name, (args, res) in _SIGS.items():
+            f = getattr(L, name)
+            f.argtypes = args
+            f.restype = res
+        _lib = L
+    return _lib
+
+
+def _check(rc, where):
+    if rc != 0:
+        raise FgqError(rc, where)
+
+
+def _stream():
+    return ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+
+
+def _dev(t, dtype, name):
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a torch tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if t.dtype != dtype:
+        raise TypeError(f"{name} must be {dtype}, got {t.dtype}")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def conv_out_hw(H, W, R, S, stride, pad):
+    return (H + 2 * pad[0] - R) // stride[0] + 1, (W + 2 * pad[1] - S) // stride[1] + 1
+
+
+def _pair(v):
+    return (v, v) if isinstance(v, int) else tuple(v)
+
+
+def fgq_ternarize(w, G, method=FGQ_TERN_EXACT, want_delta=True):
+    """w: fp32 [O][C][R][S] (or [O][K]).  Returns (codes uint8 [O][ceil(K/4)],
+    alpha fp32 [O][K/G], delta fp32 [O][K/G] or None)."""
+    w4 = w if w.dim() == 4 else w.reshape(w.shape[0], w.shape[1], 1, 1)
+    O, C, R, S = w4.shape
+    K = C * R * S
+    pw = _dev(w4, torch.float32, "w")
+    codes = torch.empty((O, (K + 3) // 4), dtype=torch.uint8, device=w.device)
+    ng = K // G if G > 0 and K % G == 0 else 1
+    alpha = torch.empty((O, ng), dtype=torch.float32, device=w.device)
+    delta = torch.empty_like(alpha) if want_delta else None
+    rc = lib().fgq_ternarize(pw, O, C, R, S, G, method, codes.data_ptr(), alpha.data_ptr(),
+                             delta.data_ptr() if delta is not None else None, _stream())
+    _check(rc, "fgq_ternarize")
+    return codes, alpha, delta
+
+
+def fgq_quantize_ws_bytes(n):
+    return int(lib().fgq_quantize_ws_bytes(n))
+
+
+def fgq_quantize_act(x, bits, scale_in=None, q=None, scale_out=None, ws=None):
+    """x: fp32 tensor (any shape, contiguous).  Returns (q uint8 packed, scale fp32[1])."""
+    n = x.numel()
+    px = _dev(x, torch.float32, "x")
+    nbytes = n if bits == 8 else n // 2
+    if q is None:
+        q = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=x.device)[:nbytes]
+    if scale_out is None:
+        scale_out = torch.empty(1, dtype=torch.float32, device=x.device)
+    if scale_in is None and ws is None:
+        ws = torch.empty(max(fgq_quantize_ws_bytes(n), 4), dtype=torch.uint8, device=x.device)
+    rc = lib().fgq_quantize_act(px, n, bits,
+                                None if scale_in is None else _dev(scale_in, torch.float32, "scale_in"),
+                                _dev(q, torch.uint8, "q"), _dev(scale_out, torch.float32, "scale_out"),
+                                None if ws is None else ctypes.c_void_p(ws.data_ptr()),
+                                0 if ws is None else ws.numel() * ws.element_size(), _stream())
+    _check(rc, "fgq_quantize_act")
+    return q, scale_out
+
+
+def fgq_prepared_bytes(O, K, G):
+    return int(lib().fgq_prepared_bytes(O, K, G))
+
+
+def fgq_prepare_weights(codes, alpha, O, K, G, prepared=None):
+    """Per-layer constants of the folded-scale kernel (opaque uint8 buffer)."""
+    nb = fgq_prepared_bytes(O, K, G)
+    if nb == 0:
+        raise FgqError(3, "fgq_prepare_weights")
+    if prepared is None:
+        prepared = torch.empty(nb, dtype=torch.uint8, device=codes.device)
+    if prepared.data_ptr() % 256:
+        raise ValueError("prepared buffer must be 256-byte aligned")
+    rc = lib().fgq_prepare_weights(_dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                                   O, K, G, ctypes.c_void_p(prepared.data_ptr()), nb, _stream())
+    _check(rc, "fgq_prepare_weights")
+    return prepared
+
+
+def fgq_conv2d(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, G, prepared=None, y=None):
+    """q: NHWC activations (packed uint8); shape = (B, H, W, C); sx: fp32[1]
+    device scalar.  Returns y fp32 [B][Ho][Wo][O]."""
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv_out_hw(H, W, R, S, (sh, sw), (ph, pw))
+    if y is None:
+        y = torch.empty((B, Ho, Wo, O), dtype=torch.float32, device=q.device)
+    rc = lib().fgq_conv2d(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), B, H, W, C,
+                          _dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                          None if prepared is None else _dev(prepared, torch.uint8, "prepared"),
+                          O, R, S, sh, sw, ph, pw, G, _dev(y, torch.float32, "y"), _stream())
+    _check(rc, "fgq_conv2d")
+    return y
+
+
+def fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=None, y=None):
+    if y is None:
+        y = torch.empty((M, O), dtype=torch.float32, device=q.device)
+    rc = lib().fgq_gemm(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), M, K,
+                        _dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                        None if prepared is None else _dev(prepared, torch.uint8, "prepared"),
+                        O, G, _dev(y, torch.float32, "y"), _stream())
+    _check(rc, "fgq_gemm")
+    return y
+
+
+def fgq_group_sums(q, bits, shape, codes, O, R, S, stride, pad, G, row0, nrows, P=None):
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    K = R * S * C
+    if P is None:
+        P = torch.empty((nrows, O, K // G), dtype=torch.int32, device=q.device)
+    rc = lib().fgq_group_sums(_dev(q, torch.uint8, "q"), bits, B, H, W, C, _dev(codes, torch.uint8, "codes"),
+                              O, R, S, sh, sw, ph, pw, G, row0, nrows, _dev(P, torch.int32, "P"), _stream())
+    _check(rc, "fgq_group_sums")
+    return P

@@ -1,0 +1,190 @@
+// api.hip -- the extern "C" boundary of libfgq.so (declared in include/fgq.h):
+// host-side validation, then kernel selection and launch on the caller's
+// stream.  No allocation, no hidden device state.
+#include <stdlib.h>
+
+#include <vector>
+
+#include "fgq_internal.h"
+
+using namespace fgq;
+
+namespace {
+
+bool conv_geom(int64_t B, int64_t H, int64_t W, int64_t C, int64_t O, int32_t R, int32_t S,
+               int32_t sh, int32_t sw, int32_t ph, int32_t pw, int32_t G, int32_t bits,
+               ConvGeom* g, fgq_status* err) {
+  *err = FGQ_OK;
+  if (bits != 8 && bits != 4) {
+    *err = FGQ_ERR_BITS;
+    return false;
+  }
+  if (B < 1 || H < 1 || W < 1 || C < 1 || O < 1 || R < 1 || S < 1 || sh < 1 || sw < 1 ||
+      ph < 0 || pw < 0 || H + 2LL * ph < R || W + 2LL * pw < S) {
+    *err = FGQ_ERR_SHAPE;
+    return false;
+  }
+  if (G < 1 || C % G != 0) {
+    *err = FGQ_ERR_GROUP;
+    return false;
+  }
+  if (bits == 4 && C % 2 != 0) {
+    *err = FGQ_ERR_BITS;
+    return false;
+  }
+  g->B = B; g->H = H; g->W = W; g->C = C; g->O = O;
+  g->R = R; g->S = S; g->sh = sh; g->sw = sw; g->ph = ph; g->pw = pw;
+  g->G = G; g->bits = bits;
+  g->Ho = (H + 2LL * ph - R) / sh + 1;
+  g->Wo = (W + 2LL * pw - S) / sw + 1;
+  g->M = B * g->Ho * g->Wo;
+  g->K = static_cast<int64_t>(R) * S * C;
+  if (g->M > (1LL << 40) || g->K > (1LL << 31) || O > (1LL << 31)) {
+    *err = FGQ_ERR_SHAPE;
+    return false;
+  }
+  return true;
+}
+
+fgq_status run_layer(const uint8_t* q, const float* sx, const uint8_t* codes,
+                     const float* alpha, const void* prepared, const ConvGeom& g, float* y,
+                     void* stream) {
+  hipStream_t st = as_stream(stream);
+  if (prepared && fold_supported(g, q)) return launch_fold_conv(q, sx, prepared, g, y, st);
+  if (group64_supported(g, q)) return launch_group64_conv(q, sx, codes, alpha, g, y, st);
+  return launch_exact_conv(q, sx, codes, alpha, g, y, st);
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* fgq_status_string(fgq_status s) {
+  switch (s) {
+    case FGQ_OK: return "FGQ_OK";
+    case FGQ_ERR_NULL: return "FGQ_ERR_NULL: a required pointer is NULL";
+    case FGQ_ERR_SHAPE: return "FGQ_ERR_SHAPE: invalid or inconsistent sizes";
+    case FGQ_ERR_GROUP: return "FGQ_ERR_GROUP: group size must be >= 1 and divide C";
+    case FGQ_ERR_BITS: return "FGQ_ERR_BITS: bits must be 8 or 4 (4 needs an even C or n)";
+    case FGQ_ERR_NONFINITE: return "FGQ_ERR_NONFINITE: weights contain NaN or Inf";
+    case FGQ_ERR_HIP: return "FGQ_ERR_HIP: HIP runtime error or no device";
+    case FGQ_ERR_UNSUPPORTED: return "FGQ_ERR_UNSUPPORTED: method or shape not supported";
+    case FGQ_ERR_WORKSPACE: return "FGQ_ERR_WORKSPACE: workspace missing or too small";
+    default: return "FGQ: unknown status";
+  }
+}
+
+int32_t fgq_abi_version(void) { return 1; }
+
+int32_t fgq_device_count(void) {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess) return 0;
+  return n;
+}
+
+size_t fgq_codes_bytes(int64_t O, int64_t K) {
+  if (O < 0 || K < 0) return 0;
+  return static_cast<size_t>(O * ceil_div(K, 4));
+}
+
+int64_t fgq_group_count(int64_t O, int64_t K, int32_t G) {
+  if (O < 0 || K < 0 || G < 1 || K % G != 0) return -1;
+  return O * (K / G);
+}
+
+fgq_status fgq_ternarize(const float* w, int64_t O, int64_t C, int32_t R, int32_t S, int32_t G,
+                         int32_t method, uint8_t* codes, float* alpha, float* delta,
+                         void* stream) {
+  if (!w || !codes || !alpha) return FGQ_ERR_NULL;
+  if (O < 1 || C < 1 || R < 1 || S < 1) return FGQ_ERR_SHAPE;
+  if (G < 1 || C % G != 0) return FGQ_ERR_GROUP;
+  if (method != FGQ_TERN_EXACT && method != FGQ_TERN_EXP_LEMMA) return FGQ_ERR_UNSUPPORTED;
+  const int64_t K = static_cast<int64_t>(R) * S * C;
+  hipStream_t st = as_stream(stream);
+  fgq_status rc = launch_ternarize(w, O, C, R, S, G, method, codes, alpha, delta, st);
+  if (rc != FGQ_OK) return rc;
+  // Offline step: wait, then report non-finite weights (their groups carry
+  // alpha = NaN).
+  const int64_t ng = O * (K / G);
+  std::vector<float> host(static_cast<size_t>(ng));
+  FGQ_TRY_HIP(hipMemcpyAsync(host.data(), alpha, sizeof(float) * ng, hipMemcpyDeviceToHost, st));
+  FGQ_TRY_HIP(hipStreamSynchronize(st));
+  for (int64_t i = 0; i < ng; ++i)
+    if (host[i] != host[i]) return FGQ_ERR_NONFINITE;
+  return FGQ_OK;
+}
+
+size_t fgq_quantize_ws_bytes(int64_t n) {
+  if (n < 0) return 0;
+  return sizeof(float) * static_cast<size_t>(quantize_partials(n));
+}
+
+fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits, const float* scale_in,
+                            uint8_t* q, float* scale_out, void* ws, size_t ws_bytes,
+                            void* stream) {
+  if (!x || !q || !scale_out) return FGQ_ERR_NULL;
+  if (bits != 8 && bits != 4) return FGQ_ERR_BITS;
+  if (n < 1) return FGQ_ERR_SHAPE;
+  if (bits == 4 && n % 2 != 0) return FGQ_ERR_BITS;
+  const int32_t np = quantize_partials(n);
+  if (!scale_in && (!ws || ws_bytes < sizeof(float) * static_cast<size_t>(np)))
+    return FGQ_ERR_WORKSPACE;
+  return launch_quantize(x, n, bits, scale_in, q, scale_out, static_cast<float*>(ws), np,
+                         as_stream(stream));
+}
+
+size_t fgq_prepared_bytes(int64_t O, int64_t K, int32_t G) {
+  if (O < 1 || K < 1 || G < 1 || K % G != 0) return 0;
+  return static_cast<size_t>(prepared_layout(O, K).total);
+}
+
+fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha, int64_t O, int64_t K,
+                               int32_t G, void* prepared, size_t prepared_bytes, void* stream) {
+  if (!codes || !alpha || !prepared) return FGQ_ERR_NULL;
+  if (O < 1 || K < 1) return FGQ_ERR_SHAPE;
+  if (G < 1 || K % G != 0) return FGQ_ERR_GROUP;
+  if (O > (1LL << 31) || K > (1LL << 31)) return FGQ_ERR_SHAPE;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  if (prepared_bytes < static_cast<size_t>(prepared_layout(O, K).total)) return FGQ_ERR_WORKSPACE;
+  return launch_prepare(codes, alpha, O, K, G, prepared, as_stream(stream));
+}
+
+fgq_status fgq_conv2d(const uint8_t* q, int32_t bits, const float* sx, int64_t B, int64_t H,
+                      int64_t W, int64_t C, const uint8_t* codes, const float* alpha,
+                      const void* prepared, int64_t O, int32_t R, int32_t S, int32_t stride_h,
+                      int32_t stride_w, int32_t pad_h, int32_t pad_w, int32_t G, float* y,
+                      void* stream) {
+  if (!q || !sx || !codes || !alpha || !y) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(B, H, W, C, O, R, S, stride_h, stride_w, pad_h, pad_w, G, bits, &g, &err))
+    return err;
+  if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  return run_layer(q, sx, codes, alpha, prepared, g, y, stream);
+}
+
+fgq_status fgq_gemm(const uint8_t* q, int32_t bits, const float* sx, int64_t M, int64_t K,
+                    const uint8_t* codes, const float* alpha, const void* prepared, int64_t O,
+                    int32_t G, float* y, void* stream) {
+  if (!q || !sx || !codes || !alpha || !y) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(1, M, 1, K, O, 1, 1, 1, 1, 0, 0, G, bits, &g, &err)) return err;
+  if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  return run_layer(q, sx, codes, alpha, prepared, g, y, stream);
+}
+
+fgq_status fgq_group_sums(const uint8_t* q, int32_t bits, int64_t B, int64_t H, int64_t W,
+                          int64_t C, const uint8_t* codes, int64_t O, int32_t R, int32_t S,
+                          int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                          int32_t G, int64_t row0, int64_t nrows, int32_t* P, void* stream) {
+  if (!q || !codes || !P) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(B, H, W, C, O, R, S, stride_h, stride_w, pad_h, pad_w, G, bits, &g, &err))
+    return err;
+  if (row0 < 0 || nrows < 0 || row0 + nrows > g.M) return FGQ_ERR_SHAPE;
+  return launch_group_sums(q, codes, g, row0, nrows, P, as_stream(stream));
+}
+
+}  // extern "C"

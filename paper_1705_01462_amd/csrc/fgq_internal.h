@@ -1,0 +1,74 @@
+// fgq_internal.h -- internal declarations shared by the libfgq sources.
+// Not installed; the public interface is include/fgq.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "fgq.h"
+
+#define FGQ_TRY_HIP(expr)                      \
+  do {                                         \
+    hipError_t fgq_e_ = (expr);                \
+    if (fgq_e_ != hipSuccess) return FGQ_ERR_HIP; \
+  } while (0)
+
+namespace fgq {
+
+// Geometry of an implicit-GEMM convolution (a GEMM is B=1, H=M, W=1, R=S=1).
+struct ConvGeom {
+  int64_t B, H, W, C, O, Ho, Wo, M, K;
+  int32_t R, S, sh, sw, ph, pw, G, bits;
+};
+
+inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
+
+inline fgq_status last_launch() {
+  return hipGetLastError() == hipSuccess ? FGQ_OK : FGQ_ERR_HIP;
+}
+
+__host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+__host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
+
+// Layout of the buffer written by fgq_prepare_weights (offsets in bytes).
+// planes : int8  [3][O][Kp]  folded digits t*d_j (j = 0 least significant)
+// bias   : int32 [3][O]      128 * sum_k plane_j[o][k] (uint8 offset term)
+// scale  : fp32  [O]         2^-E_o
+struct PreparedLayout {
+  int64_t Kp, planes_off, bias_off, scale_off, total;
+};
+constexpr int64_t kFoldKPad = 128;
+PreparedLayout prepared_layout(int64_t O, int64_t K);
+
+// Launchers (return FGQ_OK or FGQ_ERR_HIP); arguments already validated.
+fgq_status launch_ternarize(const float* w, int64_t O, int64_t C, int32_t R,
+                            int32_t S, int32_t G, int32_t method,
+                            uint8_t* codes, float* alpha, float* delta,
+                            hipStream_t st);
+fgq_status launch_quantize(const float* x, int64_t n, int32_t bits,
+                           const float* scale_in, uint8_t* q, float* scale_out,
+                           float* partials, int32_t npart, hipStream_t st);
+int32_t quantize_partials(int64_t n);
+fgq_status launch_exact_conv(const uint8_t* q, const float* sx,
+                             const uint8_t* codes, const float* alpha,
+                             const ConvGeom& g, float* y, hipStream_t st);
+fgq_status launch_group_sums(const uint8_t* q, const uint8_t* codes,
+                             const ConvGeom& g, int64_t row0, int64_t nrows,
+                             int32_t* P, hipStream_t st);
+fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O,
+                          int64_t K, int32_t G, void* prepared,
+                          hipStream_t st);
+// Folded-scale int8 MFMA kernel; returns FGQ_ERR_UNSUPPORTED when the
+// geometry does not meet its alignment needs.
+bool fold_supported(const ConvGeom& g, const uint8_t* q);
+fgq_status launch_fold_conv(const uint8_t* q, const float* sx,
+                            const void* prepared, const ConvGeom& g, float* y,
+                            hipStream_t st);
+// Direct per-group int8 MFMA kernel (G a multiple of 64).
+bool group64_supported(const ConvGeom& g, const uint8_t* q);
+fgq_status launch_group64_conv(const uint8_t* q, const float* sx,
+                               const uint8_t* codes, const float* alpha,
+                               const ConvGeom& g, float* y, hipStream_t st);
+
+}  // namespace fgq

@@ -1,0 +1,126 @@
+// prepare.hip -- per-layer constants of the folded-scale kernel.
+//
+// y[m][o] = s_x * sum_k q[m][k] * alpha[o][g(k)] * t[o][k] is a dense GEMM
+// with real weights.  Putting every alpha of channel o on one fixed-point
+// grid, A[o][g] = rint(alpha[o][g] * 2^E_o) <= 127*(1+255+255^2), and writing
+// A in three balanced base-255 digits d_j in [-127, 127] gives int8 weights
+// t*d_j, so the layer becomes three exact int8 products combined as
+//   y = s_x * 2^-E_o * sum_j 255^j * (S_j + bias_j[o]),
+// S_j = sum_k q'[m][k] * t[o][k] * d_j[o][g(k)] over offset activations
+// q' = q - 128 (uint8) and bias_j = 128 * sum_k t*d_j (zero for uint4).
+// The only departures from the exact value are the rounding of alpha to the
+// grid (step 2^-E_o < alpha_max(o) / 4145343) and the final fp32 rounding.
+//
+// One block per output channel: max alpha -> E_o, then digits, planes and
+// the per-plane sums.
+#include "fgq_internal.h"
+
+// Every floating-point expression here is evaluated exactly as written.
+#pragma clang fp contract(off)
+
+namespace fgq {
+
+PreparedLayout prepared_layout(int64_t O, int64_t K) {
+  PreparedLayout L;
+  L.Kp = round_up(K, kFoldKPad);
+  L.planes_off = 0;
+  L.bias_off = round_up(3 * O * L.Kp, 256);
+  L.scale_off = round_up(L.bias_off + 12 * O, 256);
+  L.total = round_up(L.scale_off + 4 * O, 256);
+  return L;
+}
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int64_t kAmax = 127LL * (1 + 255 + 255 * 255);  // 8290687
+
+__device__ inline void digits_of(int64_t A, int d[3]) {
+  for (int j = 0; j < 3; ++j) {
+    int64_t r = A % 255;  // A >= 0
+    if (r > 127) r -= 255;
+    d[j] = static_cast<int>(r);
+    A = (A - r) / 255;
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void prepare_kernel(
+    const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O,
+    int64_t K, int32_t G, int64_t Kp, int8_t* __restrict__ planes,
+    int32_t* __restrict__ bias, float* __restrict__ scale) {
+  __shared__ float redf[kThreads / 64];
+  __shared__ int64_t redi[3][kThreads / 64];
+  const int64_t o = blockIdx.x;
+  const int64_t ng = K / G;
+  const int64_t rb = ceil_div(K, 4);
+  const int lane = threadIdx.x % 64, wid = threadIdx.x / 64;
+
+  float amax = 0.0f;
+  for (int64_t gi = threadIdx.x; gi < ng; gi += kThreads) amax = fmaxf(amax, alpha[o * ng + gi]);
+  for (int off = 32; off > 0; off >>= 1) amax = fmaxf(amax, __shfl_xor(amax, off));
+  if (lane == 0) redf[wid] = amax;
+  __syncthreads();
+  amax = redf[0];
+  for (int i = 1; i < kThreads / 64; ++i) amax = fmaxf(amax, redf[i]);
+
+  // Largest E with rint(amax * 2^E) <= kAmax (E = 0 for an all-zero row).
+  int E = 0;
+  if (amax > 0.0f) {
+    int e2;
+    frexpf(amax, &e2);  // amax = f * 2^e2, f in [0.5, 1)
+    E = 23 - e2;
+    if (rint(ldexp(static_cast<double>(amax), E)) > static_cast<double>(kAmax)) E -= 1;
+    if (E > 126) E = 126;
+    if (E < -126) E = -126;
+  }
+  const double two_e = ldexp(1.0, E);
+
+  int64_t s[3] = {0, 0, 0};
+  for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
+    int d[3] = {0, 0, 0};
+    int t = 0;
+    if (k < K) {
+      const uint32_t c = (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u;
+      t = c == 1 ? 1 : (c == 3 ? -1 : 0);
+      const int64_t A = static_cast<int64_t>(rint(static_cast<double>(alpha[o * ng + k / G]) * two_e));
+      digits_of(A, d);
+    }
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      const int v = t * d[j];
+      planes[(static_cast<int64_t>(j) * O + o) * Kp + k] = static_cast<int8_t>(v);
+      s[j] += v;
+    }
+  }
+#pragma unroll
+  for (int j = 0; j < 3; ++j) {
+    int64_t v = s[j];
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off);
+    if (lane == 0) redi[j][wid] = v;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int j = 0; j < 3; ++j) {
+      int64_t v = 0;
+      for (int i = 0; i < kThreads / 64; ++i) v += redi[j][i];
+      bias[j * O + o] = static_cast<int32_t>(128 * v);
+    }
+    scale[o] = static_cast<float>(ldexp(1.0, -E));
+  }
+}
+
+}  // namespace
+
+fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O, int64_t K,
+                          int32_t G, void* prepared, hipStream_t st) {
+  const PreparedLayout L = prepared_layout(O, K);
+  char* base = static_cast<char*>(prepared);
+  if (O > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  hipLaunchKernelGGL(prepare_kernel, dim3(static_cast<uint32_t>(O)), dim3(kThreads), 0, st, codes,
+                     alpha, O, K, G, L.Kp, reinterpret_cast<int8_t*>(base + L.planes_off),
+                     reinterpret_cast<int32_t*>(base + L.bias_off),
+                     reinterpret_cast<float*>(base + L.scale_off));
+  return last_launch();
+}
+
+}  // namespace fgq

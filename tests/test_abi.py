@@ -1,0 +1,108 @@
+"""The C ABI of libfgq.so, checked without a GPU: the library loads, exports
+every entry point include/fgq.h declares, and rejects invalid arguments on
+the host before anything is enqueued."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_1705_01462_amd as fgq
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "fgq.h")
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(fgq_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    names = declared_functions()
+    assert "fgq_conv2d" in names and "fgq_ternarize" in names and len(names) >= 13
+    L = ctypes.CDLL(fgq.LIB_PATH)
+    for n in names:
+        assert hasattr(L, n), n
+    # the binding wraps every entry point under the same name
+    for n in ("fgq_ternarize", "fgq_quantize_act", "fgq_prepare_weights", "fgq_conv2d",
+              "fgq_gemm", "fgq_group_sums"):
+        assert callable(getattr(fgq, n))
+
+
+def test_host_helpers():
+    L = fgq.lib()
+    assert L.fgq_abi_version() == 1
+    assert L.fgq_codes_bytes(128, 1152) == 128 * 288
+    assert L.fgq_codes_bytes(3, 5) == 3 * 2
+    assert L.fgq_group_count(128, 1152, 4) == 128 * 288
+    assert L.fgq_group_count(128, 1152, 5) == -1
+    assert L.fgq_prepared_bytes(128, 1152, 4) >= 3 * 128 * 1152
+    assert L.fgq_prepared_bytes(128, 1152, 5) == 0
+    assert L.fgq_prepared_bytes(128, 1152, 4) % 256 == 0
+    assert L.fgq_quantize_ws_bytes(32 * 28 * 28 * 128) >= 4
+    for code in range(9):
+        assert L.fgq_status_string(code).startswith(b"FGQ")
+
+
+# Arguments that fail validation are rejected before any HIP call, so these
+# use placeholder pointers.  Skip them where a device exists, so that a
+# validation bug could never launch a kernel on bogus addresses.
+no_device = pytest.mark.skipif(fgq.lib().fgq_device_count() > 0,
+                               reason="placeholder pointers are only passed on a host without a GPU")
+P = ctypes.c_void_p(0x1000)
+N = None
+
+
+@no_device
+def test_ternarize_validation():
+    L = fgq.lib()
+    assert L.fgq_ternarize(N, 4, 8, 3, 3, 4, 0, P, P, P, N) == 1
+    assert L.fgq_ternarize(P, 0, 8, 3, 3, 4, 0, P, P, P, N) == 2
+    assert L.fgq_ternarize(P, 4, 8, 3, 3, 3, 0, P, P, P, N) == 3
+    assert L.fgq_ternarize(P, 4, 8, 3, 3, 4, 7, P, P, P, N) == 7
+
+
+@no_device
+def test_quantize_validation():
+    L = fgq.lib()
+    assert L.fgq_quantize_act(N, 16, 8, N, P, P, P, 4096, N) == 1
+    assert L.fgq_quantize_act(P, 16, 6, N, P, P, P, 4096, N) == 4
+    assert L.fgq_quantize_act(P, 15, 4, N, P, P, P, 4096, N) == 4
+    assert L.fgq_quantize_act(P, 0, 8, N, P, P, P, 4096, N) == 2
+    assert L.fgq_quantize_act(P, 16, 8, N, P, P, N, 0, N) == 8   # dynamic scale needs ws
+
+
+@no_device
+def test_layer_validation():
+    L = fgq.lib()
+    conv = L.fgq_conv2d
+    ok = dict(B=2, H=8, W=8, C=16, O=8, R=3, S=3, sh=1, sw=1, ph=1, pw=1, G=4)
+
+    def call(bits=8, q=P, prepared=N, **kw):
+        a = dict(ok, **kw)
+        return conv(q, bits, P, a["B"], a["H"], a["W"], a["C"], P, P, prepared, a["O"], a["R"],
+                    a["S"], a["sh"], a["sw"], a["ph"], a["pw"], a["G"], P, N)
+
+    assert call(q=N) == 1
+    assert call(bits=5) == 4
+    assert call(bits=4, C=15, G=5) == 4
+    assert call(G=3) == 3
+    assert call(G=0) == 3
+    assert call(B=0) == 2
+    assert call(sh=0) == 2
+    assert call(ph=-1) == 2
+    assert call(H=1, ph=0) == 2                    # kernel larger than the padded image
+    assert call(prepared=ctypes.c_void_p(0x1001)) == 8   # misaligned prepared buffer
+    assert L.fgq_gemm(P, 8, P, 4, 64, P, P, N, 8, 3, P, N) == 3
+    assert L.fgq_group_sums(P, 8, 2, 8, 8, 16, P, 8, 3, 3, 1, 1, 1, 1, 4, 0, 129, P, N) == 2
+    assert L.fgq_group_sums(P, 8, 2, 8, 8, 16, P, 8, 3, 3, 1, 1, 1, 1, 4, -1, 1, P, N) == 2
+    assert L.fgq_prepare_weights(P, P, 8, 64, 4, ctypes.c_void_p(0x1010), 1 << 20, N) == 8
+    assert L.fgq_prepare_weights(P, P, 8, 64, 4, P, 16, N) == 8
+    assert L.fgq_prepare_weights(P, P, 8, 64, 3, P, 1 << 20, N) == 3
+
+
+@no_device
+def test_no_device_reports_hip_error():
+    assert fgq.lib().fgq_device_count() == 0
