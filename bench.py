@@ -206,6 +206,10 @@ def main():
     ap.add_argument("--sets", type=int, default=40, help="rotating buffer sets (~29 MB each)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--direct", action="store_true", help="time the direct per-group kernels")
+    ap.add_argument("--profile-steps", type=int, default=0,
+                    help="for profilers: run this many eager steps per group size (no graphs, "
+                         "no timing) and exit")
+    ap.add_argument("--groups", default="4,64", help="group sizes for --profile-steps")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FGQ layer is "
@@ -223,6 +227,16 @@ def main():
     bits = 8
     M, K, Ho, Wo = layer_dims(LAYER)
     ops = 2.0 * M * LAYER["O"] * K
+
+    if args.profile_steps:
+        for G in [int(g) for g in args.groups.split(",")]:
+            st = Setup(torch, fgq, fi, LAYER, G, bits, 4, folded=not args.direct)
+            for i in range(args.profile_steps):
+                st.step(i % 4)
+            torch.cuda.synchronize()
+            log(f"[bench] profile G={G}: {args.profile_steps} eager steps done")
+            del st
+        return
 
     log(f"[bench] setting up G=4 ({args.sets} buffer sets)")
     st4 = Setup(torch, fgq, fi, LAYER, 4, bits, args.sets, folded=not args.direct)

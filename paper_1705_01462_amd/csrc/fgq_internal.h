@@ -32,13 +32,19 @@ __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
 // Layout of the buffer written by fgq_prepare_weights (offsets in bytes).
-// planes : int8  [3][O][Kp]  folded digits t*d_j (j = 0 least significant)
+// planes : int8 folded digits t*d_j (j = 0 least significant) in the order
+//          the matrix-core kernel consumes them:
+//          [O32/32][Kp/64][3 planes][2 K halves][64 lanes][16 bytes], where
+//          lane l of (channel tile, K step, plane, half) holds channel
+//          32*tile + l%32, k = 64*step + 32*half + 16*(l/32) + [0, 16);
+//          channels >= O and k >= K are zero.
 // bias   : int32 [3][O]      128 * sum_k plane_j[o][k] (uint8 offset term)
 // scale  : fp32  [O]         2^-E_o
 struct PreparedLayout {
-  int64_t Kp, planes_off, bias_off, scale_off, total;
+  int64_t O32, Kp, nks, planes_off, bias_off, scale_off, total;
 };
-constexpr int64_t kFoldKPad = 128;
+constexpr int64_t kFoldKStep = 64;
+constexpr int64_t kFoldTileBytes = 3 * 2 * 64 * 16;  // one channel tile, one K step
 PreparedLayout prepared_layout(int64_t O, int64_t K);
 
 // Launchers (return FGQ_OK or FGQ_ERR_HIP); arguments already validated.

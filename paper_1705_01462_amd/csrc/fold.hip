@@ -12,19 +12,29 @@
 // piece of k (C % 16 == 0) is 16 consecutive channels of one input pixel.
 //
 // Work split.  A 256-thread workgroup owns a tile of output rows x output
-// channels and walks K in steps of 64 (one v_mfma_i32_16x16x64_i8 K).  Its
-// four waves are kNWO (channels) x 4/kNWO (rows); each wave owns 32
-// channels x kMB*16 rows, i.e. 2 x kMB 16x16 blocks per digit plane.
-//  * Weights (the 16-row MFMA operand) go straight from memory (L2: every
-//    workgroup reads the same few hundred KB) into registers, one step
-//    ahead; no two waves of a workgroup share them.
-//  * Activations (the 16-column operand) are gathered into LDS once per
-//    workgroup per step (double-buffered) and read by every wave that
-//    shares those rows.
-// A lane's four accumulators are four consecutive channels of one output
-// row, so each fp32 result leaves as one 16-byte store.  Workgroups are
-// numbered so that consecutive row tiles land on one XCD (shared halos in
-// that XCD's L2).  All in-loop index arithmetic is 32-bit and incremental.
+// channels and walks K in steps of 64 (two K halves of the
+// v_mfma_i32_32x32x32_i8 instruction, which runs at twice the rate of the
+// 16x16x64 form on gfx950).  Its four waves are kNWO (channels) x 4/kNWO
+// (rows); each wave owns 32 channels x kNB*32 rows, i.e. kNB 32x32 blocks
+// per digit plane.
+//  * Activations are the 32-row MFMA operand: gathered into LDS once per
+//    workgroup per step (double-buffered, 64-byte rows with the 16-byte
+//    slot XOR-swizzled by row/4 so that both the 16-row writes and the
+//    32-row fragment reads hit every bank once per pass) and read by every
+//    wave that shares those rows.
+//  * Weights are the 32-column operand: raw buffer loads straight into
+//    registers (every workgroup reads the same few hundred KB, so they come
+//    from L2).  They are stored in fragment order, so each wave-wide load is
+//    one contiguous kilobyte; a lane's offset is fixed and the K step is the
+//    scalar offset, so the loop spends no vector instructions on them.
+//  * Out-of-image activation pieces are loaded with an offset past the
+//    buffer end, which the hardware returns as zeros (q = 0, then q' = -128
+//    for uint8), so padding needs no select.
+// A lane's 16 accumulators of a block are 16 rows of one channel; for each
+// row the wave stores 32 consecutive channels (128 contiguous bytes).
+// Workgroups are numbered so that consecutive row tiles land on one XCD
+// (shared halos in that XCD's L2).  In-loop index arithmetic is 32-bit and
+// incremental.
 #include <type_traits>
 
 #include "fgq_internal.h"
@@ -33,11 +43,14 @@ namespace fgq {
 namespace {
 
 typedef int v4i __attribute__((ext_vector_type(4)));
-typedef float v4f __attribute__((ext_vector_type(4)));
+typedef int v16i __attribute__((ext_vector_type(16)));
+typedef int v2i __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
-constexpr int kKT = 64;            // K per step
-constexpr int kLdsRow = kKT + 16;  // bytes per LDS row; 80 spreads 16-byte reads over the banks
+constexpr int kKT = 64;      // K per step
+constexpr int kRowB = 64;    // LDS bytes per activation row (one step of K)
+constexpr int kBufFlags = 0x00020000;  // raw buffer descriptor word 3 (gfx9)
+constexpr uint32_t kOutOfRange = 0x80000000u;
 
 struct FoldArgs {
   const uint8_t* q;
@@ -46,16 +59,17 @@ struct FoldArgs {
   const int32_t* bias;
   const float* scale;
   float* y;
-  int32_t M, K, O, Kp;
+  int32_t M, K, O, nks;
   int32_t H, W, C, R, S, Ho, Wo, sh, sw, ph, pw;
+  int32_t q_bytes, planes_bytes;
   int32_t n_otiles, n_mtiles;
 };
 
 // Unpack 16 four-bit values (8 bytes, element 2i in the low nibble) to 16
 // bytes in element order.
-__device__ inline v4i unpack_u4x16(uint2 v) {
-  const uint32_t lo0 = v.x & 0x0F0F0F0Fu, hi0 = (v.x >> 4) & 0x0F0F0F0Fu;
-  const uint32_t lo1 = v.y & 0x0F0F0F0Fu, hi1 = (v.y >> 4) & 0x0F0F0F0Fu;
+__device__ inline v4i unpack_u4x16(uint32_t x0, uint32_t x1) {
+  const uint32_t lo0 = x0 & 0x0F0F0F0Fu, hi0 = (x0 >> 4) & 0x0F0F0F0Fu;
+  const uint32_t lo1 = x1 & 0x0F0F0F0Fu, hi1 = (x1 >> 4) & 0x0F0F0F0Fu;
   v4i r;
   r.x = static_cast<int>(__builtin_amdgcn_perm(hi0, lo0, 0x05010400u));
   r.y = static_cast<int>(__builtin_amdgcn_perm(hi0, lo0, 0x07030602u));
@@ -71,16 +85,21 @@ __device__ inline int xcd_swizzle(int bid, int n) {
   return x * qn + (x < rn ? x : rn) + bid / 8;
 }
 
-template <int kBits, int kNWO, int kMB, bool kSmallC>
+// Byte offset of the 16-byte k-slot `slot` of activation row `row` in LDS.
+__device__ inline int lds_off(int row, int slot) {
+  return row * kRowB + 16 * (slot ^ ((row >> 2) & 3));
+}
+
+template <int kBits, int kNWO, int kNB, bool kSmallC>
 __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
-  constexpr int kTM = kNWM * kMB * 16;
-  constexpr int kPieces = kTM * 4;  // 16-byte pieces of one activation step
+  constexpr int kTM = kNWM * kNB * 32;
+  constexpr int kPieces = kTM * 4;  // 16-element pieces of one activation step
   constexpr int kXP = (kPieces + kThreads - 1) / kThreads;
-  // Pieces past the tile (when kTM*4 is not a multiple of 256) are written
-  // to spare rows after the tile so that every store is unconditional.
-  constexpr int kStage = (kTM + (kXP * kThreads - kPieces) / 4) * kLdsRow;
+  // Pieces past the tile (when kTM*4 is not a multiple of 256) go to spare
+  // rows after the tile so that every store is unconditional.
+  constexpr int kStage = (kTM + (kXP * kThreads - kPieces) / 4) * kRowB;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kStage];
 
   const int tid = threadIdx.x;
@@ -90,18 +109,15 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
   const int o0 = (tile % a.n_otiles) * kTO + 32 * wo;  // this wave's first channel
   const int m0 = (tile / a.n_otiles) * kTM;             // workgroup's first row
 
-  // ---- weight fragment pointers: lane supplies channel o0+16b+lane%16,
-  // k-slot 16*(lane/16) of each step.  Channels past O read channel O-1
-  // (their results are never stored).
-  const int8_t* wp[3][2];
-#pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    int o = o0 + 16 * b + lane % 16;
-    o = o < a.O ? o : a.O - 1;
-#pragma unroll
-    for (int j = 0; j < 3; ++j)
-      wp[j][b] = a.planes + (static_cast<int64_t>(j) * a.O + o) * a.Kp + 16 * (lane / 16);
-  }
+  const __amdgpu_buffer_rsrc_t qrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
+  const __amdgpu_buffer_rsrc_t wrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.planes), 0, a.planes_bytes, kBufFlags);
+
+  // ---- weight fragments: lane supplies channel o0 + lane%32, k-slot
+  // 16*(lane/32) of K half h; the fragment-ordered planes put the wave's
+  // 64 lanes x 16 bytes of (tile, step, plane, half) in one kilobyte.
+  const int wbase = (o0 / 32) * a.nks * static_cast<int>(kFoldTileBytes) + 16 * lane;
 
   // ---- activation pieces owned by this thread: piece p = tid + 256*i is
   // row p/4 of the tile, k-slot 16*(p%4) = 16*(tid%4) of each step.
@@ -121,6 +137,12 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
     hi0[i] = ho * a.sh - a.ph;
     wi0[i] = wo_ * a.sw - a.pw;
     rowbase[i] = (b * a.H + hi0[i]) * a.W + wi0[i];
+  }
+  int xlds[kXP];
+#pragma unroll
+  for (int i = 0; i < kXP; ++i) {
+    const int p = tid + kThreads * i;
+    xlds[i] = lds_off(p / 4, p % 4);
   }
   // tap state (r, s, c) of k = step*64 + 16*sub, advanced incrementally
   int tr, ts, tc, tk = 16 * sub;
@@ -148,210 +170,189 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
     }
   };
 
-  // Loads are unconditional (out-of-range pieces read the tensor's first
-  // bytes); the zero select, the uint8 offset and the uint4 unpack happen
-  // when the piece is written to LDS, so nothing waits on a load before the
-  // matrix-core work of the step has been issued.
-  typedef typename std::conditional<kBits == 8, v4i, uint2>::type raw_t;
-  raw_t xraw[3][kXP];
-  bool xok[3][kXP];
-  auto load_x = [&](auto U) {
-    constexpr int u = decltype(U)::value;
+  typedef typename std::conditional<kBits == 8, v4i, v2i>::type raw_t;
+  raw_t xraw[kXP];
+  auto load_x = [&]() {
 #pragma unroll
     for (int i = 0; i < kXP; ++i) {
+      // Branch-free bounds test (bitwise, no short-circuit) so that the
+      // whole step stays one basic block for the scheduler.
       const int hi = hi0[i] + tr, wi = wi0[i] + ts;
-      const bool ok = rowok[i] && tk < a.K && hi >= 0 && hi < a.H && wi >= 0 && wi < a.W;
-      const int64_t e = ok ? static_cast<int64_t>(rowbase[i] + tr * a.W + ts) * a.C + tc : 0;
-      xraw[u][i] = *reinterpret_cast<const raw_t*>(a.q + (kBits == 8 ? e : e / 2));
-      xok[u][i] = ok;
+      const bool ok = rowok[i] & (tk < a.K) & (static_cast<unsigned>(hi) < static_cast<unsigned>(a.H)) &
+                      (static_cast<unsigned>(wi) < static_cast<unsigned>(a.W));
+      const int e = (rowbase[i] + tr * a.W + ts) * a.C + tc;  // element offset
+      if constexpr (kBits == 8) {
+        const uint32_t off = ok ? static_cast<uint32_t>(e) : kOutOfRange;
+        xraw[i] = __builtin_amdgcn_raw_buffer_load_b128(qrs, off, 0, 0);
+      } else {
+        const uint32_t off = ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange;
+        xraw[i] = __builtin_amdgcn_raw_buffer_load_b64(qrs, off, 0, 0);
+      }
     }
   };
-  auto store_x = [&](auto U, int stage) {
-    constexpr int u = decltype(U)::value;
+  auto store_x = [&](int stage) {
     unsigned char* base = lds + stage * kStage;
 #pragma unroll
     for (int i = 0; i < kXP; ++i) {
-      const int p = tid + kThreads * i;
       v4i v;
       if constexpr (kBits == 8) {
         const int x = static_cast<int>(0x80808080u);
-        v = xraw[u][i];
-        if (!xok[u][i]) v = v4i{0, 0, 0, 0};
-        v.x ^= x; v.y ^= x; v.z ^= x; v.w ^= x;  // q - 128; padding reads -128
+        v = xraw[i];
+        v.x ^= x; v.y ^= x; v.z ^= x; v.w ^= x;  // q - 128 (padding read 0 -> -128)
       } else {
-        v = xok[u][i] ? unpack_u4x16(xraw[u][i]) : v4i{0, 0, 0, 0};
+        v = unpack_u4x16(static_cast<uint32_t>(xraw[i].x), static_cast<uint32_t>(xraw[i].y));
       }
-      *reinterpret_cast<v4i*>(base + (p / 4) * kLdsRow + 16 * (p % 4)) = v;
+      *reinterpret_cast<v4i*>(base + xlds[i]) = v;
     }
   };
 
-  v4i acc[3][2][kMB];
-#pragma unroll
-  for (int j = 0; j < 3; ++j)
-#pragma unroll
-    for (int b = 0; b < 2; ++b)
-#pragma unroll
-      for (int c = 0; c < kMB; ++c) acc[j][b][c] = v4i{0, 0, 0, 0};
-
-  const int nk = (a.K + kKT - 1) / kKT;
-  const int xrow0 = wm * kMB * 16 + lane % 16, xslot = 16 * (lane / 16);
-  const unsigned char* xfrag = lds + xrow0 * kLdsRow + xslot;
-  auto compute = [&](int stage, const v4i (&w)[3][2]) {
-    const unsigned char* base = xfrag + stage * kStage;
-    v4i xf[kMB];
-#pragma unroll
-    for (int c = 0; c < kMB; ++c) xf[c] = *reinterpret_cast<const v4i*>(base + 16 * c * kLdsRow);
-#pragma unroll
-    for (int c = 0; c < kMB; ++c)
-#pragma unroll
-      for (int b = 0; b < 2; ++b)
-#pragma unroll
-        for (int j = 0; j < 3; ++j)
-          acc[j][b][c] = __builtin_amdgcn_mfma_i32_16x16x64_i8(w[j][b], xf[c], acc[j][b][c], 0, 0, 0);
-    // Issue every fragment read first (distinct registers), then the
-    // matrix instructions, so LDS latency is paid once per step.
-#pragma unroll
-    for (int c = 0; c < kMB; ++c) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-    __builtin_amdgcn_sched_group_barrier(0x008, 6 * kMB, 0);
-  };
-
-  // Software pipeline, two steps deep: step ks issues the loads of step
-  // ks+2 (weights into ring slot (ks+2)%3, activations into registers),
-  // feeds the matrix cores with LDS stage ks%2 and ring slot ks%3, then
-  // publishes the activations of step ks+1 (loaded a step earlier) to the
-  // other LDS stage.  Prefetches past the last step reload the last step's
-  // weights and read no activations, so no load needs a branch.  The loop
-  // is unrolled by 3 so that every ring index is a compile-time constant.
-  using I0 = std::integral_constant<int, 0>;
-  using I1 = std::integral_constant<int, 1>;
-  using I2 = std::integral_constant<int, 2>;
-  v4i wring[3][3][2];
-  const int klast = (nk - 1) * kKT;
-  auto load_w_step = [&](auto U, int ks) {
+  v4i wring[2][3][2];
+  auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
-    const int kc = ks * kKT < klast ? ks * kKT : klast;
+    const int kso = (ks < a.nks ? ks : a.nks - 1) * static_cast<int>(kFoldTileBytes);
 #pragma unroll
     for (int j = 0; j < 3; ++j)
 #pragma unroll
-      for (int b = 0; b < 2; ++b) wring[u][j][b] = *reinterpret_cast<const v4i*>(wp[j][b] + kc);
+      for (int h = 0; h < 2; ++h)
+        wring[u][j][h] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, kso, 0);
   };
+
+  v16i acc[3][kNB];
+#pragma unroll
+  for (int j = 0; j < 3; ++j)
+#pragma unroll
+    for (int c = 0; c < kNB; ++c) acc[j][c] = v16i{};
+
+  // A-operand fragment addresses (row = wave rows + 32c + lane%32, slot 2h + lane/32)
+  int afrag[kNB][2];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c)
+#pragma unroll
+    for (int h = 0; h < 2; ++h) afrag[c][h] = lds_off(wm * kNB * 32 + 32 * c + lane % 32, 2 * h + lane / 32);
+
+  auto compute = [&](int stage, const v4i (&w)[3][2]) {
+    const unsigned char* base = lds + stage * kStage;
+    v4i xf[kNB][2];
+#pragma unroll
+    for (int c = 0; c < kNB; ++c)
+#pragma unroll
+      for (int h = 0; h < 2; ++h) xf[c][h] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+#pragma unroll
+    for (int h = 0; h < 2; ++h)
+#pragma unroll
+      for (int c = 0; c < kNB; ++c)
+#pragma unroll
+        for (int j = 0; j < 3; ++j)
+          acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][h], w[j][h], acc[j][c], 0, 0, 0);
+  };
+
+  // Step ks: prefetch step ks+1 (weights into ring slot (ks+1)%2,
+  // activations into registers), feed the matrix cores from LDS stage ks%2
+  // and ring slot ks%2, then publish the prefetched activations to the
+  // other LDS stage.  Loads past the last step are clamped (weights) or
+  // read nothing (activations), so the step has no data-dependent branch;
+  // the loop is unrolled by 2 so that ring indices are constants.
+  const int nk = (a.K + kKT - 1) / kKT;
   auto step = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
-    constexpr int u2 = (u + 2) % 3, u1 = (u + 1) % 3;
-    load_w_step(std::integral_constant<int, u2>{}, ks + 2);
+    load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
     advance_tap();
-    load_x(std::integral_constant<int, u2>{});
-    __builtin_amdgcn_sched_barrier(0);  // prefetch issued before the matrix work
-    compute(ks & 1, wring[u]);
-    __builtin_amdgcn_sched_barrier(0);  // publish (which waits) after it
-    store_x(std::integral_constant<int, u1>{}, (ks + 1) & 1);
+    load_x();
+    compute(u, wring[u]);
+    // Schedule: every fragment read first (distinct registers, LDS latency
+    // paid once), then the matrix instructions with the prefetch loads and
+    // their address arithmetic slotted between them, so the per-CU load
+    // path works while the matrix cores do.
+#pragma unroll
+    for (int i = 0; i < 2 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+    for (int i = 0; i < 6 + kXP; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, 6 * kNB - 2 * (6 + kXP) > 0 ? 6 * kNB - 2 * (6 + kXP) : 0, 0);
+    __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
+    store_x(1 - u);
     __syncthreads();
   };
-
-  load_w_step(I0{}, 0);
-  load_x(I0{});
-  load_w_step(I1{}, 1);
-  advance_tap();
-  load_x(I1{});
-  store_x(I0{}, 0);
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  load_w(I0{}, 0);
+  load_x();
+  store_x(0);
   __syncthreads();
   int ks = 0;
-  for (; ks + 3 <= nk; ks += 3) {
+  for (; ks + 2 <= nk; ks += 2) {
     step(I0{}, ks);
     step(I1{}, ks + 1);
-    step(I2{}, ks + 2);
   }
   if (ks < nk) step(I0{}, ks);
-  if (ks + 1 < nk) step(I1{}, ks + 1);
 
-  // ---- epilogue: lane holds channels ob..ob+3 of row m.
+  // ---- epilogue: lane holds rows m of channel o.
+  const int o = o0 + lane % 32;
+  if (o >= a.O) return;
   const float sx = *a.sx;
+  const float c0 = sx * a.scale[o];
+  const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
+  int32_t b0 = 0, b1 = 0, b2 = 0;
+  if constexpr (kBits == 8) {
+    b0 = a.bias[o];
+    b1 = a.bias[a.O + o];
+    b2 = a.bias[2 * a.O + o];
+  }
 #pragma unroll
-  for (int b = 0; b < 2; ++b) {
-    const int ob = o0 + 16 * b + 4 * (lane / 16);
-    float c0[4], c1[4], c2[4];
-    int32_t b0[4], b1[4], b2[4];
+  for (int c = 0; c < kNB; ++c) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int o = ob + r;
-      const bool ok = o < a.O;
-      const float s0 = ok ? sx * a.scale[o] : 0.0f;
-      c0[r] = s0;
-      c1[r] = s0 * 255.0f;
-      c2[r] = s0 * 65025.0f;
-      if (kBits == 8 && ok) {
-        b0[r] = a.bias[o];
-        b1[r] = a.bias[a.O + o];
-        b2[r] = a.bias[2 * a.O + o];
-      } else {
-        b0[r] = b1[r] = b2[r] = 0;
-      }
-    }
-#pragma unroll
-    for (int c = 0; c < kMB; ++c) {
-      const int m = m0 + wm * kMB * 16 + 16 * c + lane % 16;
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + wm * kNB * 32 + 32 * c + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
       if (m >= a.M) continue;
-      float out[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        const float f2 = static_cast<float>(acc[2][b][c][r] + b2[r]);
-        const float f1 = static_cast<float>(acc[1][b][c][r] + b1[r]);
-        const float f0 = static_cast<float>(acc[0][b][c][r] + b0[r]);
-        out[r] = fmaf(f2, c2[r], fmaf(f1, c1[r], f0 * c0[r]));
-      }
-      float* dst = a.y + static_cast<int64_t>(m) * a.O + ob;
-      if (ob + 3 < a.O && (a.O % 4) == 0) {
-        const v4f v = {out[0], out[1], out[2], out[3]};
-        __builtin_nontemporal_store(v, reinterpret_cast<v4f*>(dst));
-      } else {
-#pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (ob + r < a.O) dst[r] = out[r];
-      }
+      const float f2 = static_cast<float>(acc[2][c][r] + b2);
+      const float f1 = static_cast<float>(acc[1][c][r] + b1);
+      const float f0 = static_cast<float>(acc[0][c][r] + b0);
+      __builtin_nontemporal_store(fmaf(f2, c2, fmaf(f1, c1, f0 * c0)),
+                                  a.y + static_cast<int64_t>(m) * a.O + o);
     }
   }
 }
 
-template <int kBits, int kNWO, int kMB>
+template <int kBits, int kNWO, int kNB>
 fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
-  const bool small_c = a0.C < kKT;
-  constexpr int kTO = 32 * kNWO, kTM = (4 / kNWO) * kMB * 16;
+  constexpr int kTO = 32 * kNWO, kTM = (4 / kNWO) * kNB * 32;
   FoldArgs a = a0;
   a.n_otiles = (a.O + kTO - 1) / kTO;
   a.n_mtiles = (a.M + kTM - 1) / kTM;
   const int64_t n = static_cast<int64_t>(a.n_otiles) * a.n_mtiles;
   if (n > 0x7fffffffLL) return FGQ_ERR_SHAPE;
-  if (small_c)
-    hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kMB, true>), dim3(static_cast<uint32_t>(n)),
+  if (a.C < kKT)
+    hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, true>), dim3(static_cast<uint32_t>(n)),
                        dim3(kThreads), 0, st, a);
   else
-    hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kMB, false>), dim3(static_cast<uint32_t>(n)),
+    hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, false>), dim3(static_cast<uint32_t>(n)),
                        dim3(kThreads), 0, st, a);
   return last_launch();
 }
 
-// Rows per wave (kMB blocks of 16) are chosen so that the workgroups fill
-// the 256 compute units in as few rounds as possible: cost = rounds * kMB.
+// Rows per wave (kNB blocks of 32) are chosen so that the workgroups fill
+// the 256 compute units in as few rounds as possible: cost = rounds * kNB.
 template <int kBits, int kNWO>
 fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
   constexpr int kNWM = 4 / kNWO;
   const int64_t otiles = ceil_div(a.O, 32 * kNWO);
-  int best = 8;
+  int best = 4;
   int64_t best_cost = -1;
-  for (int mb = 8; mb >= 4; --mb) {
-    const int64_t tiles = otiles * ceil_div(a.M, kNWM * mb * 16);
-    const int64_t cost = ceil_div(tiles, 256) * mb;
+  for (int nb = 4; nb >= 2; --nb) {
+    const int64_t tiles = otiles * ceil_div(a.M, kNWM * nb * 32);
+    const int64_t cost = ceil_div(tiles, 256) * nb;
     if (best_cost < 0 || cost < best_cost) {
       best_cost = cost;
-      best = mb;
+      best = nb;
     }
   }
   switch (best) {
-    case 4: return launch_cfg<kBits, kNWO, 4>(a, st);
-    case 5: return launch_cfg<kBits, kNWO, 5>(a, st);
-    case 6: return launch_cfg<kBits, kNWO, 6>(a, st);
-    case 7: return launch_cfg<kBits, kNWO, 7>(a, st);
-    default: return launch_cfg<kBits, kNWO, 8>(a, st);
+    case 2: return launch_cfg<kBits, kNWO, 2>(a, st);
+    case 3: return launch_cfg<kBits, kNWO, 3>(a, st);
+    default: return launch_cfg<kBits, kNWO, 4>(a, st);
   }
 }
 
@@ -367,9 +368,10 @@ fgq_status launch_bits(const FoldArgs& a, hipStream_t st) {
 bool fold_supported(const ConvGeom& g, const uint8_t* q) {
   const uintptr_t qa = reinterpret_cast<uintptr_t>(q);
   const int64_t in_elems = g.B * g.H * g.W * g.C;
+  const PreparedLayout L = prepared_layout(g.O, g.K);
+  const int64_t plane_bytes = 3 * L.O32 * L.Kp;
   return g.C % 16 == 0 && g.K < (1LL << 17) && qa % (g.bits == 8 ? 16 : 8) == 0 &&
-         in_elems < (1LL << 31) && g.M < (1LL << 31) && g.O < (1LL << 24) &&
-         g.H * g.W < (1LL << 30);
+         in_elems < (1LL << 31) && g.M < (1LL << 31) && plane_bytes < (1LL << 31);
 }
 
 fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepared,
@@ -386,7 +388,7 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.M = static_cast<int32_t>(g.M);
   a.K = static_cast<int32_t>(g.K);
   a.O = static_cast<int32_t>(g.O);
-  a.Kp = static_cast<int32_t>(L.Kp);
+  a.nks = static_cast<int32_t>(L.nks);
   a.H = static_cast<int32_t>(g.H);
   a.W = static_cast<int32_t>(g.W);
   a.C = static_cast<int32_t>(g.C);
@@ -398,6 +400,9 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.sw = g.sw;
   a.ph = g.ph;
   a.pw = g.pw;
+  const int64_t in_elems = g.B * g.H * g.W * g.C;
+  a.q_bytes = static_cast<int32_t>(g.bits == 8 ? in_elems : in_elems / 2);
+  a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
   a.n_otiles = a.n_mtiles = 0;
   return g.bits == 8 ? launch_bits<8>(a, st) : launch_bits<4>(a, st);
 }

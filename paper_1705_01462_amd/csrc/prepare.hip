@@ -11,8 +11,9 @@
 // The only departures from the exact value are the rounding of alpha to the
 // grid (step 2^-E_o < alpha_max(o) / 4145343) and the final fp32 rounding.
 //
-// One block per output channel: max alpha -> E_o, then digits, planes and
-// the per-plane sums.
+// One block per output channel (channels padded to a multiple of 32 get
+// zero planes): max alpha -> E_o, then digits, planes (written in the
+// fragment order of the matrix-core kernel) and the per-plane sums.
 #include "fgq_internal.h"
 
 // Every floating-point expression here is evaluated exactly as written.
@@ -22,9 +23,11 @@ namespace fgq {
 
 PreparedLayout prepared_layout(int64_t O, int64_t K) {
   PreparedLayout L;
-  L.Kp = round_up(K, kFoldKPad);
+  L.O32 = round_up(O, 32);
+  L.Kp = round_up(K, kFoldKStep);
+  L.nks = L.Kp / kFoldKStep;
   L.planes_off = 0;
-  L.bias_off = round_up(3 * O * L.Kp, 256);
+  L.bias_off = round_up(3 * L.O32 * L.Kp, 256);
   L.scale_off = round_up(L.bias_off + 12 * O, 256);
   L.total = round_up(L.scale_off + 4 * O, 256);
   return L;
@@ -44,6 +47,14 @@ __device__ inline void digits_of(int64_t A, int d[3]) {
   }
 }
 
+// Byte offset of plane j, channel o, reduction index k in the fragment order.
+__device__ inline int64_t frag_offset(int64_t nks, int j, int64_t o, int64_t k) {
+  const int64_t tile = o / 32, ks = k / kFoldKStep;
+  const int kk = static_cast<int>(k % kFoldKStep);
+  const int half = kk / 32, lane = static_cast<int>(o % 32) + 32 * ((kk % 32) / 16);
+  return (((tile * nks + ks) * 3 + j) * 2 + half) * 1024 + lane * 16 + (kk % 16);
+}
+
 __global__ __launch_bounds__(kThreads) void prepare_kernel(
     const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O,
     int64_t K, int32_t G, int64_t Kp, int8_t* __restrict__ planes,
@@ -51,6 +62,12 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
   __shared__ float redf[kThreads / 64];
   __shared__ int64_t redi[3][kThreads / 64];
   const int64_t o = blockIdx.x;
+  const int64_t nks = Kp / kFoldKStep;
+  if (o >= O) {  // padding channel of the last 32-channel tile
+    for (int64_t k = threadIdx.x; k < Kp; k += kThreads)
+      for (int j = 0; j < 3; ++j) planes[frag_offset(nks, j, o, k)] = 0;
+    return;
+  }
   const int64_t ng = K / G;
   const int64_t rb = ceil_div(K, 4);
   const int lane = threadIdx.x % 64, wid = threadIdx.x / 64;
@@ -88,7 +105,7 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
       const int v = t * d[j];
-      planes[(static_cast<int64_t>(j) * O + o) * Kp + k] = static_cast<int8_t>(v);
+      planes[frag_offset(nks, j, o, k)] = static_cast<int8_t>(v);
       s[j] += v;
     }
   }
@@ -116,7 +133,7 @@ fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O, i
   const PreparedLayout L = prepared_layout(O, K);
   char* base = static_cast<char*>(prepared);
   if (O > 0x7fffffffLL) return FGQ_ERR_SHAPE;
-  hipLaunchKernelGGL(prepare_kernel, dim3(static_cast<uint32_t>(O)), dim3(kThreads), 0, st, codes,
+  hipLaunchKernelGGL(prepare_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0, st, codes,
                      alpha, O, K, G, L.Kp, reinterpret_cast<int8_t*>(base + L.planes_off),
                      reinterpret_cast<int32_t*>(base + L.bias_off),
                      reinterpret_cast<float*>(base + L.scale_off));
