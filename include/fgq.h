@@ -145,9 +145,10 @@ fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits,
  * every A of the channel within 127*(1 + 255 + 255^2), written as three
  * balanced base-255 digits in [-127, 127].  The folded weights t*digit are
  * int8, so the layer runs as three exact int8 products whose integer sums
- * are combined exactly; only the rounding of alpha to the grid (relative
- * step below 1.21e-7 of the channel's largest alpha) and one final
- * fp32 rounding differ from the exact formula.
+ * are combined exactly; only the rounding of alpha to the grid (an error
+ * of at most 1.21e-7 times the channel's largest alpha) and the fp32
+ * conversions and fused multiply-adds of the final combination differ from
+ * the exact formula.
  *
  * codes, alpha  [in]  as produced by fgq_ternarize for an [O][K] layer
  * prepared      [out] device buffer of fgq_prepared_bytes(O, K, G) bytes,
@@ -170,10 +171,13 @@ fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha,
  * alpha    [in]  fp32 [O][K/G]
  * prepared [in]  NULL, or the output of fgq_prepare_weights for these
  *                codes/alpha/O/K/G.  NULL selects the direct per-group
- *                kernels: exact int32 group sums and an fp32 (G >= 64 with
- *                K a multiple of 64: int8 matrix cores) or fp64 (otherwise)
- *                alpha epilogue.  Non-NULL selects the folded-scale int8
- *                matrix-core kernel (any G).
+ *                kernel: exact int32 group sums (packed 4-way dot products)
+ *                and an fp64 alpha epilogue, bit-identical to evaluating the
+ *                formula in fp64 in group order and rounding once to fp32.
+ *                Non-NULL selects the folded-scale int8 matrix-core kernel
+ *                (any G) when C is a multiple of 16, K < 2^17, q is 16-byte
+ *                (bits 8) or 8-byte (bits 4) aligned and every buffer is
+ *                below 2^31 bytes; otherwise the direct kernel runs.
  * y        [out] fp32 [B][Ho][Wo][O]
  */
 fgq_status fgq_conv2d(const uint8_t* q, int32_t bits, const float* sx,

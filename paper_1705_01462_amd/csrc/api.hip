@@ -51,7 +51,6 @@ fgq_status run_layer(const uint8_t* q, const float* sx, const uint8_t* codes,
                      void* stream) {
   hipStream_t st = as_stream(stream);
   if (prepared && fold_supported(g, q)) return launch_fold_conv(q, sx, prepared, g, y, st);
-  if (group64_supported(g, q)) return launch_group64_conv(q, sx, codes, alpha, g, y, st);
   return launch_exact_conv(q, sx, codes, alpha, g, y, st);
 }
 

@@ -37,7 +37,7 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 //          [O32/32][Kp/64][3 planes][2 K halves][64 lanes][16 bytes], where
 //          lane l of (channel tile, K step, plane, half) holds channel
 //          32*tile + l%32, k = 64*step + 32*half + 16*(l/32) + [0, 16);
-//          channels >= O and k >= K are zero.
+//          channels >= O and k >= K are zero; Kp is a multiple of 128.
 // bias   : int32 [3][O]      128 * sum_k plane_j[o][k] (uint8 offset term)
 // scale  : fp32  [O]         2^-E_o
 struct PreparedLayout {
@@ -71,10 +71,5 @@ bool fold_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_fold_conv(const uint8_t* q, const float* sx,
                             const void* prepared, const ConvGeom& g, float* y,
                             hipStream_t st);
-// Direct per-group int8 MFMA kernel (G a multiple of 64).
-bool group64_supported(const ConvGeom& g, const uint8_t* q);
-fgq_status launch_group64_conv(const uint8_t* q, const float* sx,
-                               const uint8_t* codes, const float* alpha,
-                               const ConvGeom& g, float* y, hipStream_t st);
 
 }  // namespace fgq

@@ -12,14 +12,15 @@
 // piece of k (C % 16 == 0) is 16 consecutive channels of one input pixel.
 //
 // Work split.  A 256-thread workgroup owns a tile of output rows x output
-// channels and walks K in steps of 64 (two K halves of the
+// channels and walks K in steps of 128 (four 32-wide K slices of the
 // v_mfma_i32_32x32x32_i8 instruction, which runs at twice the rate of the
-// 16x16x64 form on gfx950).  Its four waves are kNWO (channels) x 4/kNWO
+// 16x16x64 form on gfx950; the prepared K is padded to a multiple of 128
+// with zero weights).  Its four waves are kNWO (channels) x 4/kNWO
 // (rows); each wave owns 32 channels x kNB*32 rows, i.e. kNB 32x32 blocks
 // per digit plane.
 //  * Activations are the 32-row MFMA operand: gathered into LDS once per
-//    workgroup per step (double-buffered, 64-byte rows with the 16-byte
-//    slot XOR-swizzled by row/4 so that both the 16-row writes and the
+//    workgroup per step (double-buffered, 128-byte rows with the 16-byte
+//    slot XOR-swizzled by (row/2) % 8 so that both the row writes and the
 //    32-row fragment reads hit every bank once per pass) and read by every
 //    wave that shares those rows.
 //  * Weights are the 32-column operand: raw buffer loads straight into
@@ -30,6 +31,8 @@
 //  * Out-of-image activation pieces are loaded with an offset past the
 //    buffer end, which the hardware returns as zeros (q = 0, then q' = -128
 //    for uint8), so padding needs no select.
+// The accumulators start at the per-plane bias (uint8), and the loads of
+// step ks+1 are interleaved between the matrix instructions of step ks.
 // A lane's 16 accumulators of a block are 16 rows of one channel; for each
 // row the wave stores 32 consecutive channels (128 contiguous bytes).
 // Workgroups are numbered so that consecutive row tiles land on one XCD
@@ -47,8 +50,9 @@ typedef int v16i __attribute__((ext_vector_type(16)));
 typedef int v2i __attribute__((ext_vector_type(2)));
 
 constexpr int kThreads = 256;
-constexpr int kKT = 64;      // K per step
-constexpr int kRowB = 64;    // LDS bytes per activation row (one step of K)
+constexpr int kKT = 128;     // K per step (two fragment-ordered 64-wide blocks)
+constexpr int kRowB = kKT;   // LDS bytes per activation row (one step of K)
+constexpr int kSlots = kKT / 16;  // 16-byte k-slots per row
 constexpr int kBufFlags = 0x00020000;  // raw buffer descriptor word 3 (gfx9)
 constexpr uint32_t kOutOfRange = 0x80000000u;
 
@@ -86,8 +90,11 @@ __device__ inline int xcd_swizzle(int bid, int n) {
 }
 
 // Byte offset of the 16-byte k-slot `slot` of activation row `row` in LDS.
+// The slot is XOR-swizzled by row/2 so that 16 consecutive rows at one slot
+// (a fragment read) and 2 rows x 8 slots (a publish) each cover all 64
+// banks once.
 __device__ inline int lds_off(int row, int slot) {
-  return row * kRowB + 16 * (slot ^ ((row >> 2) & 3));
+  return row * kRowB + 16 * (slot ^ ((row >> 1) & (kSlots - 1)));
 }
 
 template <int kBits, int kNWO, int kNB, bool kSmallC>
@@ -95,11 +102,11 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
   constexpr int kTM = kNWM * kNB * 32;
-  constexpr int kPieces = kTM * 4;  // 16-element pieces of one activation step
+  constexpr int kPieces = kTM * kSlots;  // 16-element pieces of one activation step
   constexpr int kXP = (kPieces + kThreads - 1) / kThreads;
   // Pieces past the tile (when kTM*4 is not a multiple of 256) go to spare
   // rows after the tile so that every store is unconditional.
-  constexpr int kStage = (kTM + (kXP * kThreads - kPieces) / 4) * kRowB;
+  constexpr int kStage = (kTM + (kXP * kThreads - kPieces) / kSlots) * kRowB;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kStage];
 
   const int tid = threadIdx.x;
@@ -120,14 +127,15 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
   const int wbase = (o0 / 32) * a.nks * static_cast<int>(kFoldTileBytes) + 16 * lane;
 
   // ---- activation pieces owned by this thread: piece p = tid + 256*i is
-  // row p/4 of the tile, k-slot 16*(p%4) = 16*(tid%4) of each step.
-  const int sub = tid % 4;
+  // row p/kSlots of the tile, k-slot 16*(p%kSlots) = 16*(tid%kSlots) of each
+  // step.
+  const int sub = tid % kSlots;
   int rowbase[kXP], hi0[kXP], wi0[kXP];
   bool rowok[kXP];
 #pragma unroll
   for (int i = 0; i < kXP; ++i) {
     const int p = tid + kThreads * i;
-    const int m = m0 + p / 4;
+    const int m = m0 + p / kSlots;
     rowok[i] = (p < kPieces) && (m < a.M);
     const int mm = rowok[i] ? m : 0;
     const int wo_ = mm % a.Wo;
@@ -142,7 +150,7 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
 #pragma unroll
   for (int i = 0; i < kXP; ++i) {
     const int p = tid + kThreads * i;
-    xlds[i] = lds_off(p / 4, p % 4);
+    xlds[i] = lds_off(p / kSlots, p % kSlots);
   }
   // tap state (r, s, c) of k = step*64 + 16*sub, advanced incrementally
   int tr, ts, tc, tk = 16 * sub;
@@ -154,12 +162,12 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
   }
   auto advance_tap = [&]() {
     tk += kKT;
-    if constexpr (kSmallC) {  // C in {16, 32, 48}: several taps per step
+    if constexpr (kSmallC) {  // C < 128: several taps per step
       const int t = ts + (tc + kKT) / a.C;
       tc = (tc + kKT) % a.C;
       tr += t / a.S;
       ts = t % a.S;
-    } else {                  // C >= 64: at most one tap boundary per step
+    } else {                  // C >= 128: at most one tap boundary per step
       tc += kKT;
       const bool wrap = tc >= a.C;
       tc = wrap ? tc - a.C : tc;
@@ -206,39 +214,57 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
     }
   };
 
-  v4i wring[2][3][2];
+  // A step covers two 64-wide fragment blocks (K quarters hq = 2*blk + h).
+  // Loads past the last block read zeros or another tile's weights; they
+  // are never used.
+  v4i wring[2][3][4];
   auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
-    const int kso = (ks < a.nks ? ks : a.nks - 1) * static_cast<int>(kFoldTileBytes);
 #pragma unroll
-    for (int j = 0; j < 3; ++j)
+    for (int blk = 0; blk < 2; ++blk) {
+      const int kso = (2 * ks + blk) * static_cast<int>(kFoldTileBytes);
 #pragma unroll
-      for (int h = 0; h < 2; ++h)
-        wring[u][j][h] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, kso, 0);
+      for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          wring[u][j][2 * blk + h] =
+              __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, kso, 0);
+    }
   };
 
+  // Accumulators start at the uint8 offset term 128 * sum_k plane_j[o][k]
+  // of the lane's channel, so the epilogue needs no integer additions.
   v16i acc[3][kNB];
+  {
+    const int oc = o0 + lane % 32;
 #pragma unroll
-  for (int j = 0; j < 3; ++j)
+    for (int j = 0; j < 3; ++j) {
+      const int bj = (kBits == 8 && oc < a.O) ? a.bias[j * a.O + oc] : 0;
+      v16i init;
 #pragma unroll
-    for (int c = 0; c < kNB; ++c) acc[j][c] = v16i{};
+      for (int r = 0; r < 16; ++r) init[r] = bj;
+#pragma unroll
+      for (int c = 0; c < kNB; ++c) acc[j][c] = init;
+    }
+  }
 
-  // A-operand fragment addresses (row = wave rows + 32c + lane%32, slot 2h + lane/32)
-  int afrag[kNB][2];
+  // A-operand fragment addresses (row = wave rows + 32c + lane%32, slot
+  // 2*quarter + lane/32)
+  int afrag[kNB][4];
 #pragma unroll
   for (int c = 0; c < kNB; ++c)
 #pragma unroll
-    for (int h = 0; h < 2; ++h) afrag[c][h] = lds_off(wm * kNB * 32 + 32 * c + lane % 32, 2 * h + lane / 32);
+    for (int h = 0; h < 4; ++h) afrag[c][h] = lds_off(wm * kNB * 32 + 32 * c + lane % 32, 2 * h + lane / 32);
 
-  auto compute = [&](int stage, const v4i (&w)[3][2]) {
+  auto compute = [&](int stage, const v4i (&w)[3][4]) {
     const unsigned char* base = lds + stage * kStage;
-    v4i xf[kNB][2];
+    v4i xf[kNB][4];
 #pragma unroll
     for (int c = 0; c < kNB; ++c)
 #pragma unroll
-      for (int h = 0; h < 2; ++h) xf[c][h] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+      for (int h = 0; h < 4; ++h) xf[c][h] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
 #pragma unroll
-    for (int h = 0; h < 2; ++h)
+    for (int h = 0; h < 4; ++h)
 #pragma unroll
       for (int c = 0; c < kNB; ++c)
 #pragma unroll
@@ -264,14 +290,14 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
     // their address arithmetic slotted between them, so the per-CU load
     // path works while the matrix cores do.
 #pragma unroll
-    for (int i = 0; i < 2 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    for (int i = 0; i < 4 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-    for (int i = 0; i < 6 + kXP; ++i) {
+    for (int i = 0; i < 12 + kXP; ++i) {
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 6 * kNB - 2 * (6 + kXP) > 0 ? 6 * kNB - 2 * (6 + kXP) : 0, 0);
+    __builtin_amdgcn_sched_group_barrier(0x008, 12 * kNB - 2 * (12 + kXP) > 0 ? 12 * kNB - 2 * (12 + kXP) : 0, 0);
     __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
     store_x(1 - u);
     __syncthreads();
@@ -295,21 +321,15 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
   const float sx = *a.sx;
   const float c0 = sx * a.scale[o];
   const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
-  int32_t b0 = 0, b1 = 0, b2 = 0;
-  if constexpr (kBits == 8) {
-    b0 = a.bias[o];
-    b1 = a.bias[a.O + o];
-    b2 = a.bias[2 * a.O + o];
-  }
 #pragma unroll
   for (int c = 0; c < kNB; ++c) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int m = m0 + wm * kNB * 32 + 32 * c + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
       if (m >= a.M) continue;
-      const float f2 = static_cast<float>(acc[2][c][r] + b2);
-      const float f1 = static_cast<float>(acc[1][c][r] + b1);
-      const float f0 = static_cast<float>(acc[0][c][r] + b0);
+      const float f2 = static_cast<float>(acc[2][c][r]);
+      const float f1 = static_cast<float>(acc[1][c][r]);
+      const float f0 = static_cast<float>(acc[0][c][r]);
       __builtin_nontemporal_store(fmaf(f2, c2, fmaf(f1, c1, f0 * c0)),
                                   a.y + static_cast<int64_t>(m) * a.O + o);
     }
@@ -405,13 +425,6 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
   a.n_otiles = a.n_mtiles = 0;
   return g.bits == 8 ? launch_bits<8>(a, st) : launch_bits<4>(a, st);
-}
-
-// Direct G%64 matrix-core path: not built yet.
-bool group64_supported(const ConvGeom&, const uint8_t*) { return false; }
-fgq_status launch_group64_conv(const uint8_t*, const float*, const uint8_t*, const float*,
-                               const ConvGeom&, float*, hipStream_t) {
-  return FGQ_ERR_UNSUPPORTED;
 }
 
 }  // namespace fgq

@@ -24,7 +24,7 @@ namespace fgq {
 PreparedLayout prepared_layout(int64_t O, int64_t K) {
   PreparedLayout L;
   L.O32 = round_up(O, 32);
-  L.Kp = round_up(K, kFoldKStep);
+  L.Kp = round_up(K, 2 * kFoldKStep);  // whole 128-wide kernel steps; k >= K is zero
   L.nks = L.Kp / kFoldKStep;
   L.planes_off = 0;
   L.bias_off = round_up(3 * L.O32 * L.Kp, 256);

@@ -3,12 +3,15 @@
 // convolution).  Streaming, HBM-bound.
 //
 // Dynamic scale: pass 1 writes one partial maximum per block to the caller's
-// workspace; pass 2 has every block reduce those partials (a few KB from L2)
-// to the same s = max/qmax before quantizing its slice, so no atomics, no
-// zero-initialised state and no host synchronisation are needed.
-// Each pass-2 thread converts 16 (u8) or 32 (u4) values into one 16-byte
-// store; the division x/s is IEEE (correctly rounded) and rint rounds half
-// to even, so the codes are reproducible bit for bit.
+// workspace; pass 2 has every block reduce those partials (at most a few KB
+// from L2) to the same s = max/qmax before quantizing its slice, so there
+// are no atomics, no zero-initialised state and no host synchronisation.
+// Both passes issue all of a thread's loads before using any of them (pass
+// 2 also before the partials are reduced), so each costs about one memory
+// round trip plus its bytes.  Each pass-2 thread turns 16 (u8) or 32 (u4)
+// values into one 16-byte store; the division x/s is IEEE (correctly
+// rounded) and rint rounds half to even, so the codes are reproducible bit
+// for bit.
 #include "fgq_internal.h"
 
 namespace fgq {
@@ -17,34 +20,38 @@ namespace {
 typedef float v4f __attribute__((ext_vector_type(4)));
 constexpr int kThreads = 256;
 constexpr int kMaxPartials = 1024;
+constexpr int kP1Vec = 4;  // float4 loads per pass-1 thread and iteration
 
 __device__ inline float block_max(float v, float* red) {
   for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off));
   const int wid = threadIdx.x / 64, lane = threadIdx.x % 64;
   if (lane == 0) red[wid] = v;
   __syncthreads();
-  if (threadIdx.x == 0) {
-    float m = red[0];
-    for (int i = 1; i < kThreads / 64; ++i) m = fmaxf(m, red[i]);
-    red[kThreads / 64] = m;
-  }
-  __syncthreads();
-  return red[kThreads / 64];
+  float m = red[0];
+#pragma unroll
+  for (int i = 1; i < kThreads / 64; ++i) m = fmaxf(m, red[i]);
+  return m;
 }
 
 template <bool kAligned>
 __global__ __launch_bounds__(kThreads) void absmax_partial_kernel(
     const float* __restrict__ x, int64_t n, float* __restrict__ partials) {
-  __shared__ float red[kThreads / 64 + 1];
+  __shared__ float red[kThreads / 64];
   float m = 0.0f;  // max(max x, 0); fmaxf ignores NaN
   const int64_t tid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
   const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
   if (kAligned) {
     const v4f* x4 = reinterpret_cast<const v4f*>(x);
     const int64_t n4 = n / 4;
-    for (int64_t i = tid; i < n4; i += stride) {
-      const v4f v = __builtin_nontemporal_load(&x4[i]);
-      m = fmaxf(m, fmaxf(fmaxf(v.x, v.y), fmaxf(v.z, v.w)));
+    for (int64_t base = tid; base < n4; base += stride * kP1Vec) {
+      v4f v[kP1Vec];
+#pragma unroll
+      for (int u = 0; u < kP1Vec; ++u) {
+        const int64_t i = base + u * stride;
+        v[u] = i < n4 ? x4[i] : v4f{0.0f, 0.0f, 0.0f, 0.0f};
+      }
+#pragma unroll
+      for (int u = 0; u < kP1Vec; ++u) m = fmaxf(m, fmaxf(fmaxf(v[u].x, v[u].y), fmaxf(v[u].z, v[u].w)));
     }
     for (int64_t i = n4 * 4 + tid; i < n; i += stride) m = fmaxf(m, x[i]);
   } else {
@@ -65,25 +72,16 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const float* __restrict__ x, int64_t n, const float* __restrict__ scale_in,
     const float* __restrict__ partials, int32_t npart, uint8_t* __restrict__ q,
     float* __restrict__ scale_out) {
-  __shared__ float red[kThreads / 64 + 1];
+  __shared__ float red[kThreads / 64];
   constexpr float qmax = kBits == 8 ? 255.0f : 15.0f;
-  float s;
-  if (scale_in) {
-    s = *scale_in;
-  } else {
-    float m = 0.0f;
-    for (int i = threadIdx.x; i < npart; i += kThreads) m = fmaxf(m, partials[i]);
-    m = block_max(m, red);
-    s = m > 0.0f ? m / qmax : 1.0f;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = s;
-
   constexpr int kPer = kBits == 8 ? 16 : 32;  // values per 16-byte store
   const int64_t nchunks = n / kPer;
-  const int64_t tid = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
-  const int64_t stride = static_cast<int64_t>(gridDim.x) * kThreads;
-  for (int64_t ch = tid; ch < nchunks; ch += stride) {
-    float v[kPer];
+  const int64_t ch = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x;
+
+  // 1. issue this thread's loads
+  float v[kPer];
+  const bool have = ch < nchunks;
+  if (have) {
     if (kAligned) {
       const v4f* x4 = reinterpret_cast<const v4f*>(x + ch * kPer);
 #pragma unroll
@@ -98,6 +96,21 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
 #pragma unroll
       for (int i = 0; i < kPer; ++i) v[i] = x[ch * kPer + i];
     }
+  }
+  // 2. the scale, while those loads are in flight
+  float s;
+  if (scale_in) {
+    s = *scale_in;
+  } else {
+    float m = 0.0f;
+    for (int i = threadIdx.x; i < npart; i += kThreads) m = fmaxf(m, partials[i]);
+    m = block_max(m, red);
+    s = m > 0.0f ? m / qmax : 1.0f;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = s;
+
+  // 3. quantize and store
+  if (have) {
     uint32_t out[4];
 #pragma unroll
     for (int wd = 0; wd < 4; ++wd) {
@@ -119,31 +132,30 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
       for (int i = 0; i < 16; ++i) dst[i] = static_cast<uint8_t>(out[i / 4] >> (8 * (i % 4)));
     }
   }
-  // tail (fewer than kPer values), one byte per thread
+  // 4. the tail (fewer than kPer values), one byte per thread of the grid
   const int64_t done = nchunks * kPer;
   const int64_t tail_bytes = kBits == 8 ? (n - done) : (n - done) / 2;
-  for (int64_t b = tid; b < tail_bytes; b += stride) {
+  if (ch < tail_bytes) {
     if (kBits == 8) {
-      q[done + b] = static_cast<uint8_t>(qval(x[done + b], s, qmax));
+      q[done + ch] = static_cast<uint8_t>(qval(x[done + ch], s, qmax));
     } else {
-      const int64_t e = done + 2 * b;
+      const int64_t e = done + 2 * ch;
       q[e / 2] = static_cast<uint8_t>(qval(x[e], s, qmax) | (qval(x[e + 1], s, qmax) << 4));
     }
   }
 }
 
-int32_t pass2_blocks(int64_t n, int32_t bits) {
+int64_t pass2_blocks(int64_t n, int32_t bits) {
   const int64_t per = bits == 8 ? 16 : 32;
-  int64_t b = ceil_div(ceil_div(n, per), kThreads);
-  if (b < 1) b = 1;
-  if (b > 8192) b = 8192;
-  return static_cast<int32_t>(b);
+  int64_t b = ceil_div(n / per, kThreads);
+  if (b < 1) b = 1;  // the tail (< per values) needs at least one block
+  return b;
 }
 
 }  // namespace
 
 int32_t quantize_partials(int64_t n) {
-  int64_t b = ceil_div(n, static_cast<int64_t>(kThreads) * 16);
+  int64_t b = ceil_div(ceil_div(n, 4), static_cast<int64_t>(kThreads) * kP1Vec);
   if (b < 1) b = 1;
   if (b > kMaxPartials) b = kMaxPartials;
   return static_cast<int32_t>(b);
@@ -161,7 +173,9 @@ fgq_status launch_quantize(const float* x, int64_t n, int32_t bits,
       hipLaunchKernelGGL(absmax_partial_kernel<false>, dim3(npart), dim3(kThreads), 0, st, x, n, partials);
     if (last_launch() != FGQ_OK) return FGQ_ERR_HIP;
   }
-  const dim3 grid(pass2_blocks(n, bits));
+  const int64_t blocks = pass2_blocks(n, bits);
+  if (blocks > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  const dim3 grid(static_cast<uint32_t>(blocks));
   if (bits == 8) {
     if (aligned)
       hipLaunchKernelGGL((quantize_kernel<8, true>), grid, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q, scale_out);
