@@ -35,10 +35,18 @@ HBM_PEAK_GBS = 8000.0
 INT8_PEAK_TOPS = 5000.0
 
 LAYER = dict(B=32, H=28, W=28, C=128, O=128, R=3, S=3, stride=1, pad=1)
+LAYER_1X1 = dict(B=32, H=56, W=56, C=256, O=64, R=1, S=1, stride=1, pad=0)
 CALIB_COPY_BYTES = 64 << 20  # plain device copy used to calibrate FETCH_SIZE / WRITE_SIZE
-TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_fold_conv3x_b32.json")
-KERNEL_SOURCES = ["paper_1705_01462_amd/csrc/fold.hip", "paper_1705_01462_amd/csrc/prepare.hip",
-                  "paper_1705_01462_amd/csrc/fgq_internal.h"]
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_conv_b32.json")
+_CSRC = "paper_1705_01462_amd/csrc/"
+# Sources of the convolution kernel that runs at each group size.
+KERNEL_SOURCES = {
+    4: [_CSRC + f for f in ("fold.hip", "igemm.h", "prepare.hip", "fgq_internal.h")],
+    64: [_CSRC + f for f in ("group.hip", "igemm.h", "prepare.hip", "fgq_internal.h")],
+}
+
+
+CONFIGS = {"conv3x_g4": (LAYER, 4), "conv3x_g64": (LAYER, 64), "1x1_g64": (LAYER_1X1, 64)}
 
 
 def log(*a):
@@ -189,11 +197,11 @@ def cpu_baseline(fi, L, G, bits, budget_s=15.0):
             "seconds": round(t_total, 3)}
 
 
-def kernel_source_hash():
+def kernel_source_hash(G):
     """sha256 of the conv kernel's sources with // comments and blank lines
     removed, so that a comment edit does not invalidate the counters."""
     h = hashlib.sha256()
-    for f in KERNEL_SOURCES:
+    for f in KERNEL_SOURCES[4 if G % 64 else 64]:
         for line in open(os.path.join(ROOT, f), encoding="utf-8"):
             code = line.split("//", 1)[0].rstrip()
             if code:
@@ -201,17 +209,21 @@ def kernel_source_hash():
     return h.hexdigest()
 
 
-def measured_traffic(G):
+def layer_key(L, G):
+    return f"{L['R']}x{L['S']}_{L['C']}to{L['O']}_{L['H']}x{L['W']}_b{L['B']}_G{G}"
+
+
+def measured_traffic(L, G):
     """HBM bytes per launch from the committed counter summary, if it was
     taken on the current kernel sources (else None)."""
     try:
         t = json.load(open(TRAFFIC_FILE))
     except (OSError, ValueError):
         return None
-    if t.get("kernel_source_sha256") != kernel_source_hash():
+    e = t.get("per_launch", {}).get(layer_key(L, G))
+    if e is None or e.get("kernel_source_sha256") != kernel_source_hash(G):
         return None
-    e = t.get("per_launch", {}).get(f"G{G}")
-    return None if e is None else int(e["fetch_bytes"] + e["write_bytes"])
+    return int(e["fetch_bytes"] + e["write_bytes"])
 
 
 def roofline(L, G, bits, conv_us):
@@ -223,12 +235,12 @@ def roofline(L, G, bits, conv_us):
     if t_hbm >= t_mfma:
         achieved = nbytes / (conv_us * 1e-6) / 1e9
         return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(G),
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(L, G),
                 "kernel": "fgq_conv2d", "kernel_us": round(conv_us, 3),
                 "algorithmic_bytes": int(nbytes)}
     achieved = ops / (conv_us * 1e-6) / 1e12
     return {"bound": "mfma", "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": measured_traffic(G),
+            "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": measured_traffic(L, G),
             "kernel": "fgq_conv2d", "kernel_us": round(conv_us, 3), "algorithmic_ops": ops}
 
 
@@ -243,7 +255,8 @@ def main():
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="for profilers: run this many eager steps per group size (no graphs, "
                          "no timing) and exit")
-    ap.add_argument("--groups", default="4,64", help="group sizes for --profile-steps")
+    ap.add_argument("--layers", default="conv3x_g4,conv3x_g64,1x1_g64",
+                    help="layer configurations for --profile-steps")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FGQ layer is "
@@ -263,12 +276,13 @@ def main():
     ops = 2.0 * M * LAYER["O"] * K
 
     if args.profile_steps:
-        for G in [int(g) for g in args.groups.split(",")]:
-            st = Setup(torch, fgq, fi, LAYER, G, bits, 4, folded=not args.direct)
+        for name in args.layers.split(","):
+            L, G = CONFIGS[name]
+            st = Setup(torch, fgq, fi, L, G, bits, 4, folded=not args.direct)
             for i in range(args.profile_steps):
                 st.step(i % 4)
             torch.cuda.synchronize()
-            log(f"[bench] profile G={G}: {args.profile_steps} eager steps done")
+            log(f"[bench] profile {name} ({layer_key(L, G)}): {args.profile_steps} eager steps done")
             del st
         # calibration: one plain device copy of known size (FETCH_SIZE and
         # WRITE_SIZE of this dispatch give the counter-to-bytes factor)
@@ -296,6 +310,15 @@ def main():
     del st64
     torch.cuda.empty_cache()
 
+    log("[bench] setting up the 1x1 layer, G=64")
+    st11 = Setup(torch, fgq, fi, LAYER_1X1, 64, bits, args.sets, folded=not args.direct)
+    r11 = measure(torch, st11, steps64, args.sets)
+    log(f"[bench] 1x1 G=64: {r11}")
+    del st11
+    torch.cuda.empty_cache()
+    M11, K11, _, _ = layer_dims(LAYER_1X1)
+    ops11 = 2.0 * M11 * LAYER_1X1["O"] * K11
+
     out = {
         "metric": METRIC,
         "value": round(ops / (ms_per_step * 1e-3) / 1e12, 2),
@@ -314,7 +337,7 @@ def main():
                                "(dynamic per-tensor scale); fp32 NHWC output",
                    "B": LAYER["B"], "H": LAYER["H"], "W": LAYER["W"], "C": LAYER["C"], "O": LAYER["O"],
                    "R": 3, "S": 3, "G": 4, "bits": bits, "M": M, "K": K,
-                   "kernel": "direct" if args.direct else "folded-scale int8 MFMA",
+                   "kernel": "direct" if args.direct else "folded-scale int8 MFMA (G=4); per-group int8 MFMA + fp32 epilogue (G=64)",
                    "step": "fgq_quantize_act + fgq_conv2d"},
         "roofline": roofline(LAYER, 4, bits, r4["conv_us"]),
         "step_detail": {"conv_us": round(r4["conv_us"], 3), "quantize_us": round(r4["quant_us"], 3),
@@ -326,6 +349,12 @@ def main():
                 "conv_us": round(r64["conv_us"], 3),
                 "conv_only_tops": round(ops / (r64["conv_us"] * 1e-6) / 1e12, 1),
                 "roofline": roofline(LAYER, 64, bits, r64["conv_us"])},
+        "g64_1x1": {"workload": "ResNet-50 1x1 conv 256->64, 56x56, batch 32, G=64", "steps": steps64,
+                    "value": round(ops11 / (r11["wall_ms"] / steps64 * 1e-3) / 1e12, 2),
+                    "ms_per_step": round(r11["wall_ms"] / steps64, 5),
+                    "conv_us": round(r11["conv_us"], 3), "quantize_us": round(r11["quant_us"], 3),
+                    "conv_only_tops": round(ops11 / (r11["conv_us"] * 1e-6) / 1e12, 1),
+                    "roofline": roofline(LAYER_1X1, 64, bits, r11["conv_us"])},
     }
     if not args.no_cpu:
         log("[bench] CPU oracle baseline")

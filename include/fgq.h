@@ -137,22 +137,30 @@ fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits,
                             void* stream);
 
 /*
- * fgq_prepare_weights -- per-layer constants for the folded-scale kernels
- * (built once per layer, like the ternarization itself).
+ * fgq_prepare_weights -- per-layer constants for the matrix-core kernels
+ * (built once per layer, like the ternarization itself).  The layout
+ * depends on G alone:
  *
- * The group scales are brought to one fixed-point grid per output channel:
- * A[o][g] = rint(alpha[o][g] * 2^E_o), with E_o the largest exponent keeping
- * every A of the channel within 127*(1 + 255 + 255^2), written as three
- * balanced base-255 digits in [-127, 127].  The folded weights t*digit are
- * int8, so the layer runs as three exact int8 products whose integer sums
- * are combined exactly; only the rounding of alpha to the grid (an error
- * of at most 1.21e-7 times the channel's largest alpha) and the fp32
- * conversions and fused multiply-adds of the final combination differ from
- * the exact formula.
+ * G = 64 with K/64 <= 160 (per-group kernel, Sec. 4: 32-bit group sums,
+ * then one multiplication by the group scale per group): the ternary
+ * weights as int8 in the kernel's operand order and alpha transposed per
+ * group; 1 byte per weight plus 4 bytes per group.
+ *
+ * Any other G (folded-scale kernel): the group scales are brought to one
+ * fixed-point grid per output channel: A[o][g] = rint(alpha[o][g] * 2^E_o),
+ * with E_o the largest exponent keeping every A of the channel within
+ * 127*(1 + 255 + 255^2), written as three balanced base-255 digits in
+ * [-127, 127].  The folded weights t*digit are int8, so the layer runs as
+ * three exact int8 products whose integer sums are combined exactly; only
+ * the rounding of alpha to the grid (an error of at most 1.21e-7 times the
+ * channel's largest alpha) and the fp32 conversions and fused multiply-adds
+ * of the final combination differ from the exact formula.  3 bytes per
+ * weight.
  *
  * codes, alpha  [in]  as produced by fgq_ternarize for an [O][K] layer
  * prepared      [out] device buffer of fgq_prepared_bytes(O, K, G) bytes,
- *                     256-byte aligned; opaque; read by fgq_conv2d/fgq_gemm.
+ *                     256-byte aligned; opaque; read by fgq_conv2d/fgq_gemm
+ *                     with the same O, K, G.
  */
 size_t fgq_prepared_bytes(int64_t O, int64_t K, int32_t G);
 fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha,
@@ -174,10 +182,13 @@ fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha,
  *                kernel: exact int32 group sums (packed 4-way dot products)
  *                and an fp64 alpha epilogue, bit-identical to evaluating the
  *                formula in fp64 in group order and rounding once to fp32.
- *                Non-NULL selects the folded-scale int8 matrix-core kernel
- *                (any G) when C is a multiple of 16, K < 2^17, q is 16-byte
- *                (bits 8) or 8-byte (bits 4) aligned and every buffer is
- *                below 2^31 bytes; otherwise the direct kernel runs.
+ *                Non-NULL selects a matrix-core kernel when C is a multiple
+ *                of 16, q is 16-byte (bits 8) or 8-byte (bits 4) aligned and
+ *                every buffer is below 2^31 bytes: the per-group kernel for
+ *                G = 64 (int32 group sums, fp32 alpha epilogue, at most
+ *                K/64 + 1 fp32 roundings relative to s_x*sum_g alpha_g|P_g|)
+ *                and the folded-scale kernel for other G (K < 2^17);
+ *                otherwise the direct kernel runs.
  * y        [out] fp32 [B][Ho][Wo][O]
  */
 fgq_status fgq_conv2d(const uint8_t* q, int32_t bits, const float* sx,

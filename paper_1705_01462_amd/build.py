@@ -25,13 +25,21 @@ FLAGS = [
 ]
 
 
+# Per-source flags.  group.hip converts every matrix-core result on the
+# vector ALU, so its results must be allocated in ordinary VGPRs (otherwise
+# each value is first copied out of an accumulation register).
+EXTRA = {
+    "group.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+}
+
+
 def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
 def _compile(src, verbose):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = ["hipcc", *FLAGS, "-c", src, "-o", obj]
+    cmd = ["hipcc", *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -50,7 +50,13 @@ fgq_status run_layer(const uint8_t* q, const float* sx, const uint8_t* codes,
                      const float* alpha, const void* prepared, const ConvGeom& g, float* y,
                      void* stream) {
   hipStream_t st = as_stream(stream);
-  if (prepared && fold_supported(g, q)) return launch_fold_conv(q, sx, prepared, g, y, st);
+  if (prepared) {
+    if (prepared_layout(g.O, g.K, g.G).kind == kPrepGroup) {
+      if (group_supported(g, q)) return launch_group_conv(q, sx, prepared, g, y, st);
+    } else if (fold_supported(g, q)) {
+      return launch_fold_conv(q, sx, prepared, g, y, st);
+    }
+  }
   return launch_exact_conv(q, sx, codes, alpha, g, y, st);
 }
 
@@ -134,7 +140,7 @@ fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits, const float
 
 size_t fgq_prepared_bytes(int64_t O, int64_t K, int32_t G) {
   if (O < 1 || K < 1 || G < 1 || K % G != 0) return 0;
-  return static_cast<size_t>(prepared_layout(O, K).total);
+  return static_cast<size_t>(prepared_layout(O, K, G).total);
 }
 
 fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha, int64_t O, int64_t K,
@@ -144,7 +150,7 @@ fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha, int64_t
   if (G < 1 || K % G != 0) return FGQ_ERR_GROUP;
   if (O > (1LL << 31) || K > (1LL << 31)) return FGQ_ERR_SHAPE;
   if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
-  if (prepared_bytes < static_cast<size_t>(prepared_layout(O, K).total)) return FGQ_ERR_WORKSPACE;
+  if (prepared_bytes < static_cast<size_t>(prepared_layout(O, K, G).total)) return FGQ_ERR_WORKSPACE;
   return launch_prepare(codes, alpha, O, K, G, prepared, as_stream(stream));
 }
 

@@ -32,20 +32,32 @@ __host__ __device__ inline int64_t ceil_div(int64_t a, int64_t b) { return (a + 
 __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_div(a, b) * b; }
 
 // Layout of the buffer written by fgq_prepare_weights (offsets in bytes).
-// planes : int8 folded digits t*d_j (j = 0 least significant) in the order
-//          the matrix-core kernel consumes them:
-//          [O32/32][Kp/64][3 planes][2 K halves][64 lanes][16 bytes], where
-//          lane l of (channel tile, K step, plane, half) holds channel
-//          32*tile + l%32, k = 64*step + 32*half + 16*(l/32) + [0, 16);
-//          channels >= O and k >= K are zero; Kp is a multiple of 128.
-// bias   : int32 [3][O]      128 * sum_k plane_j[o][k] (uint8 offset term)
-// scale  : fp32  [O]         2^-E_o
+// Two kinds, chosen by G alone:
+//  * group (G = 64 and at most kGroupMaxGroups groups per channel): the
+//    per-group kernel.
+//      planes : int8 ternary weights t in fragment order
+//               [O32/32][Kp/64][2 K halves][64 lanes][16 bytes]
+//      alpha  : fp32 [Kp/64][O32], alpha of group k/64 of channel o
+//  * fold (every other G): the folded-scale kernel.
+//      planes : int8 folded digits t*d_j (j = 0 least significant),
+//               [O32/32][Kp/64][3 planes][2 K halves][64 lanes][16 bytes]
+//      bias   : int32 [3][O]  128 * sum_k plane_j[o][k] (uint8 offset term)
+//      scale  : fp32  [O]     2^-E_o
+// In the fragment order, lane l of (channel tile, 64-wide K block, plane,
+// half) holds channel 32*tile + l%32, k = 64*block + 32*half + 16*(l/32) +
+// [0, 16), so each wave-wide 16-byte load is one contiguous kilobyte.
+// Channels >= O, k >= K (and their alpha) are zero; Kp is a multiple of 128.
+enum PrepKind { kPrepFold = 0, kPrepGroup = 1 };
 struct PreparedLayout {
-  int64_t O32, Kp, nks, planes_off, bias_off, scale_off, total;
+  int kind;
+  int64_t O32, Kp, nks, planes_off, bias_off, scale_off, alpha_off, total;
 };
 constexpr int64_t kFoldKStep = 64;
-constexpr int64_t kFoldTileBytes = 3 * 2 * 64 * 16;  // one channel tile, one K step
-PreparedLayout prepared_layout(int64_t O, int64_t K);
+constexpr int64_t kFoldTileBytes = 3 * 2 * 64 * 16;  // one channel tile, one K block
+// The per-group kernel accumulates one fp32 product per group; with at most
+// 160 groups its rounding error stays below 1e-5 of the summand magnitude.
+constexpr int64_t kGroupMaxGroups = 160;
+PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G);
 
 // Launchers (return FGQ_OK or FGQ_ERR_HIP); arguments already validated.
 fgq_status launch_ternarize(const float* w, int64_t O, int64_t C, int32_t R,
@@ -65,11 +77,16 @@ fgq_status launch_group_sums(const uint8_t* q, const uint8_t* codes,
 fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O,
                           int64_t K, int32_t G, void* prepared,
                           hipStream_t st);
-// Folded-scale int8 MFMA kernel; returns FGQ_ERR_UNSUPPORTED when the
-// geometry does not meet its alignment needs.
+// Folded-scale int8 MFMA kernel (prepared layout of kind fold); callers
+// check fold_supported first.
 bool fold_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_fold_conv(const uint8_t* q, const float* sx,
                             const void* prepared, const ConvGeom& g, float* y,
                             hipStream_t st);
+// Per-group int8 MFMA kernel with an fp32 alpha epilogue (G = 64).
+bool group_supported(const ConvGeom& g, const uint8_t* q);
+fgq_status launch_group_conv(const uint8_t* q, const float* sx,
+                             const void* prepared, const ConvGeom& g, float* y,
+                             hipStream_t st);
 
 }  // namespace fgq

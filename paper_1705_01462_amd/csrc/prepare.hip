@@ -1,5 +1,11 @@
-// prepare.hip -- per-layer constants of the folded-scale kernel.
+// prepare.hip -- per-layer constants of the matrix-core kernels.
 //
+// Group size 64 (a group is two K slices of the 32x32x32 int8 instruction):
+// the per-group kernel takes the ternary weights as int8 in fragment order
+// and alpha transposed to [K/64][O32], so that one wave reads the alphas of
+// its 32 channels for one group as 128 contiguous bytes.
+//
+// Other group sizes: the folded-scale kernel.
 // y[m][o] = s_x * sum_k q[m][k] * alpha[o][g(k)] * t[o][k] is a dense GEMM
 // with real weights.  Putting every alpha of channel o on one fixed-point
 // grid, A[o][g] = rint(alpha[o][g] * 2^E_o) <= 127*(1+255+255^2), and writing
@@ -21,15 +27,24 @@
 
 namespace fgq {
 
-PreparedLayout prepared_layout(int64_t O, int64_t K) {
+PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G) {
   PreparedLayout L;
   L.O32 = round_up(O, 32);
   L.Kp = round_up(K, 2 * kFoldKStep);  // whole 128-wide kernel steps; k >= K is zero
   L.nks = L.Kp / kFoldKStep;
   L.planes_off = 0;
-  L.bias_off = round_up(3 * L.O32 * L.Kp, 256);
-  L.scale_off = round_up(L.bias_off + 12 * O, 256);
-  L.total = round_up(L.scale_off + 4 * O, 256);
+  if (G == 64 && K / 64 <= kGroupMaxGroups) {
+    L.kind = kPrepGroup;
+    L.alpha_off = round_up(L.O32 * L.Kp, 256);
+    L.total = round_up(L.alpha_off + 4 * L.nks * L.O32, 256);
+    L.bias_off = L.scale_off = L.total;
+  } else {
+    L.kind = kPrepFold;
+    L.bias_off = round_up(3 * L.O32 * L.Kp, 256);
+    L.scale_off = round_up(L.bias_off + 12 * O, 256);
+    L.total = round_up(L.scale_off + 4 * O, 256);
+    L.alpha_off = L.total;
+  }
   return L;
 }
 
@@ -126,13 +141,42 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
   }
 }
 
+// Group kind: one block per channel of the padded channel range.
+__global__ __launch_bounds__(kThreads) void prepare_group_kernel(
+    const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O,
+    int64_t K, int64_t Kp, int64_t O32, int8_t* __restrict__ planes,
+    float* __restrict__ alpha_t) {
+  const int64_t o = blockIdx.x;
+  const int64_t nks = Kp / kFoldKStep, ng = K / 64, rb = ceil_div(K, 4);
+  for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
+    int t = 0;
+    if (o < O && k < K) {
+      const uint32_t c = (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u;
+      t = c == 1 ? 1 : (c == 3 ? -1 : 0);
+    }
+    const int64_t tile = o / 32, ks = k / kFoldKStep;
+    const int kk = static_cast<int>(k % kFoldKStep);
+    const int half = kk / 32, lane = static_cast<int>(o % 32) + 32 * ((kk % 32) / 16);
+    planes[((tile * nks + ks) * 2 + half) * 1024 + lane * 16 + (kk % 16)] = static_cast<int8_t>(t);
+  }
+  for (int64_t gi = threadIdx.x; gi < nks; gi += kThreads)
+    alpha_t[gi * O32 + o] = (o < O && gi < ng) ? alpha[o * ng + gi] : 0.0f;
+}
+
 }  // namespace
 
 fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O, int64_t K,
                           int32_t G, void* prepared, hipStream_t st) {
-  const PreparedLayout L = prepared_layout(O, K);
+  const PreparedLayout L = prepared_layout(O, K, G);
   char* base = static_cast<char*>(prepared);
-  if (O > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  if (L.O32 > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  if (L.kind == kPrepGroup) {
+    hipLaunchKernelGGL(prepare_group_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0,
+                       st, codes, alpha, O, K, L.Kp, L.O32,
+                       reinterpret_cast<int8_t*>(base + L.planes_off),
+                       reinterpret_cast<float*>(base + L.alpha_off));
+    return last_launch();
+  }
   hipLaunchKernelGGL(prepare_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0, st, codes,
                      alpha, O, K, G, L.Kp, reinterpret_cast<int8_t*>(base + L.planes_off),
                      reinterpret_cast<int32_t*>(base + L.bias_off),

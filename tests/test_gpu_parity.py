@@ -3,9 +3,10 @@ same seeded inputs.
 
 Bars: ternary codes, alpha, Delta, quantized activations,
 the scale and int32 group sums are bit-exact; the direct per-group layer
-kernel (fp64 alpha epilogue) is bit-exact too; the folded-scale kernel is
-within 1e-5 of the summand magnitude s_x * sum_g alpha_g |P_g| element-wise
-and within 1e-5 normwise.
+kernel (fp64 alpha epilogue) is bit-exact too; the matrix-core kernels
+(folded-scale for G != 64, per-group for G = 64) are within 1e-5 of the
+summand magnitude s_x * sum_g alpha_g |P_g| element-wise and within 1e-5
+normwise.
 """
 import numpy as np
 import pytest
@@ -233,6 +234,28 @@ def test_gemm_single_layer(bits, folded):
         np.testing.assert_array_equal(y.view(np.uint32), y_ref.view(np.uint32))
 
 
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("M,K,O", [(64, 256, 128), (77, 640, 40), (40, 64 * 161, 40)])
+def test_gemm_group64(bits, M, K, O):
+    """G=64 GEMMs with prepared weights: the per-group kernel (K/64 <= 160
+    groups, incl. an odd group count and ragged M, O) and the folded-scale
+    kernel beyond that (161 groups)."""
+    G = 64
+    w = fi.gauss_weights(O, K, 0.05, "gemm64", M, K)
+    x = fi.relu_gauss((M, K), "gemm64", M, K)
+    t, a, _ = oracle.ternarize(w, G)
+    codes_ref = oracle.pack_codes(t)
+    q_ref, s_ref = oracle.quantize_act(x, bits)
+    y_ref = oracle.gemm(q_ref, bits, s_ref, M, K, codes_ref, a, O, G)
+    codes, alpha, _ = fgq.fgq_ternarize(dev(w), G)
+    q, sx = fgq.fgq_quantize_act(dev(x), bits)
+    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+    y = host(fgq.fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
+    P = oracle.group_sums_conv(q_ref, bits, (1, M, 1, K), codes_ref, O, 1, 1, (1, 1), (0, 0), G)
+    mag = float(s_ref) * np.einsum("mog,og->mo", np.abs(P.astype(np.float64)), a.astype(np.float64))
+    assert_fold_close(y, y_ref, mag)
+
+
 FULL = [
     # conv3_x 3x3 128->128 on 28x28, batch 32, G=4 and G=64; 1x1 256->64 on 56x56, G=64
     (32, 28, 28, 128, 128, 3, 3, 1, 1, 4, 8),
@@ -273,11 +296,13 @@ def test_full_size_layers_sampled_rows(case):
             np.testing.assert_array_equal(y_dir[row0:row0 + 200], y_ref)
 
 
+@pytest.mark.parametrize("G", [4, 64])
 @pytest.mark.parametrize("bits", [8, 4])
-def test_degenerate_activations(bits):
+def test_degenerate_activations(bits, G):
     """All-zero activations give exactly 0; all-qmax activations give
     s_x * qmax * sum_g alpha_g T_g on both paths."""
-    B, H, W, C, O, R, S, G = 2, 6, 6, 32, 48, 3, 3, 4
+    B, H, W, O, R, S = 2, 6, 6, 48, 3, 3
+    C = 32 if G == 4 else 64
     w = fi.he_weights(O, C, R, S, "degen")
     codes, alpha, _ = fgq.fgq_ternarize(dev(w), G)
     K = R * S * C

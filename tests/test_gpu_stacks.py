@@ -1,0 +1,84 @@
+"""GPU parity on every distinct layer shape of the two network-shaped stacks
+(ResNet-50: batch 64, G=4, uint8; ResNet-101: batch 64, G=64, uint4), each
+run at its full size through the C ABI exactly as a stack would launch it
+(prepared weights), with the oracle computing sampled output rows.
+
+Layers are tested one by one on seeded ReLU-Gaussian inputs of the layer's
+own shape rather than chained, so that each comparison starts from the
+same bytes on both sides (a chained run would have to feed the oracle the
+GPU's own quantized input anyway).  conv1 has its 3 input channels padded to
+4 and uses groups of 4 in both stacks, since 64 does not divide 4.
+"""
+import numpy as np
+import pytest
+import torch
+
+import fgq_inputs as fi
+import oracle
+
+fgq = pytest.importorskip("paper_1705_01462_amd")
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+TOL = 1e-5
+ROWS = 128  # rows per sampled range (first, middle, last)
+
+
+def unique_layers(depth, batch=64):
+    seen, out = set(), []
+    for L in fi.resnet_convs(depth, batch):
+        key = tuple(L[k] for k in ("H", "W", "C", "O", "R", "S", "stride", "pad"))
+        if key not in seen:
+            seen.add(key)
+            out.append(L)
+    return out
+
+
+CASES = [(depth, G, bits, L) for depth, G, bits in ((50, 4, 8), (101, 64, 4))
+         for L in unique_layers(depth)]
+
+
+@pytest.mark.parametrize("depth,G,bits,L", CASES,
+                         ids=[f"r{d}-G{g}-u{b}-{L['name']}" for d, g, b, L in CASES])
+def test_stack_layer_sampled_rows(depth, G, bits, L):
+    B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+    st, pd = L["stride"], L["pad"]
+    g = G if C % G == 0 else 4
+    print(f"[stack] r{depth} {L['name']} B={B} {H}x{W} C={C} O={O} {R}x{S}/{st} G={g} u{bits}",
+          flush=True)
+    w = fi.he_weights(O, C, R, S, "stack", depth, L["name"])
+    if L["name"] == "conv1":
+        w[:, 3:] = 0.0  # the padded input channel carries no weight
+    x = fi.relu_gauss((B, H, W, C), "stack", depth, L["name"])
+    if L["name"] == "conv1":
+        x[..., 3:] = 0.0
+
+    codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), g)
+    q, sx = fgq.fgq_quantize_act(torch.from_numpy(x).cuda(), bits)
+    K = R * S * C
+    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, g)
+    y = fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, prepared=prep)
+    torch.cuda.synchronize()
+
+    t, a, _ = oracle.ternarize(w, g)
+    codes_ref = oracle.pack_codes(t)
+    q_ref, s_ref = oracle.quantize_act(x, bits)
+    np.testing.assert_array_equal(codes.cpu().numpy(), codes_ref)
+    np.testing.assert_array_equal(alpha.cpu().numpy(), a)
+    np.testing.assert_array_equal(q.cpu().numpy(), q_ref)
+    assert sx.item() == s_ref
+    yh = y.cpu().numpy().reshape(-1, O)
+    M = yh.shape[0]
+    n = min(ROWS, M)
+    for row0 in sorted({0, max(0, M // 2 - n // 2), M - n}):
+        y_ref = oracle.conv2d(q_ref, bits, s_ref, x.shape, codes_ref, a, O, R, S, (st, st), (pd, pd), g,
+                              rows=(row0, n))[row0:row0 + n]
+        P = oracle.group_sums_conv(q_ref, bits, x.shape, codes_ref, O, R, S, (st, st), (pd, pd), g,
+                                   row0, n).astype(np.float64)
+        mag = float(s_ref) * np.einsum("mog,og->mo", np.abs(P), a.astype(np.float64))
+        err = np.abs(yh[row0:row0 + n].astype(np.float64) - y_ref.astype(np.float64))
+        bad = err > TOL * mag
+        assert not bad.any(), (f"rows [{row0}, {row0 + n}): {bad.sum()} outputs beyond 1e-5 of the "
+                               f"summand magnitude, worst {np.max(err / np.maximum(mag, 1e-300)):.3e}")
+        assert np.linalg.norm(err) <= TOL * np.linalg.norm(y_ref.astype(np.float64)) + 1e-30
