@@ -130,6 +130,32 @@ def test_quantize_bit_exact(bits, n, given_scale):
     np.testing.assert_array_equal(host(q), q_ref)
 
 
+@pytest.mark.parametrize("bits", [8, 4])
+@pytest.mark.parametrize("scale", [0.5, 1.0 / 3.0, 0.0173, 7.0e-30, 3.0e38, 1.0e-39])
+def test_quantize_rounding_ties_and_extremes(bits, scale):
+    """Quotients at and next to half-integers (round half to even), values
+    far beyond the range, +-inf, NaN, zeros and subnormal inputs, for
+    scales whose reciprocal is normal (the reciprocal-and-correction path)
+    and for a subnormal scale and one with a subnormal reciprocal (the
+    ordinary division path)."""
+    s32 = np.float32(scale)
+    qmax = 255 if bits == 8 else 15
+    k = np.arange(0, qmax + 2, dtype=np.float32)
+    ties = (k + np.float32(0.5)) * s32                      # float32 products: at or next to ties
+    near = np.concatenate([np.nextafter(ties, np.float32(np.inf)), np.nextafter(ties, np.float32(0))])
+    r = fi.rng("quant-ties", bits, scale)
+    rand = (r.random(4000).astype(np.float32) * np.float32(qmax + 3)) * s32
+    special = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1e-45, -1e-45, 1e-40, 3.4e38, -3.4e38,
+                        s32 * np.float32(1e6), s32], np.float32)
+    x = np.concatenate([ties, near, rand, special]).astype(np.float32)
+    if x.size % 2:
+        x = np.append(x, np.float32(1.0))
+    q_ref, s_ref = oracle.quantize_act(x, bits, s32)
+    q, sq = fgq.fgq_quantize_act(dev(x), bits, scale_in=dev(np.array([s32], np.float32)))
+    assert host(sq)[0] == s_ref
+    np.testing.assert_array_equal(host(q), q_ref)
+
+
 def test_quantize_unaligned_views():
     """Pointers that are not 16-byte aligned take the scalar path."""
     x = fi.relu_gauss((1003 * 2,), "unal")
@@ -235,11 +261,13 @@ def test_gemm_single_layer(bits, folded):
 
 
 @pytest.mark.parametrize("bits", [8, 4])
-@pytest.mark.parametrize("M,K,O", [(64, 256, 128), (77, 640, 40), (40, 64 * 161, 40)])
+@pytest.mark.parametrize("M,K,O", [(64, 256, 128), (77, 640, 40), (40, 64 * 161, 40), (300, 1280, 96),
+                                   (70, 1344, 33)])
 def test_gemm_group64(bits, M, K, O):
-    """G=64 GEMMs with prepared weights: the per-group kernel (K/64 <= 160
-    groups, incl. an odd group count and ragged M, O) and the folded-scale
-    kernel beyond that (161 groups)."""
+    """G=64 GEMMs with prepared weights: the per-group kernels (K/64 <= 160
+    groups, incl. odd group counts, ragged M and O, the largest reduction
+    of the persistent kernel (1280) and the next one up) and the
+    folded-scale kernel beyond 160 groups."""
     G = 64
     w = fi.gauss_weights(O, K, 0.05, "gemm64", M, K)
     x = fi.relu_gauss((M, K), "gemm64", M, K)
@@ -326,3 +354,4 @@ def test_degenerate_activations(bits, G):
                 np.testing.assert_array_equal(y, y_ref)
             else:
                 assert_fold_close(y, y_ref, mag)
+
