@@ -115,9 +115,10 @@ def test_ternarize_reports_nonfinite():
 
 
 @pytest.mark.parametrize("bits", [8, 4])
-@pytest.mark.parametrize("n", [2, 4096 * 16 + 2, 3 * 7 * 5 * 16, 32 * 28 * 28 * 128])
+@pytest.mark.parametrize("n", [2, 4096 * 16 + 2, 3 * 7 * 5 * 16, 32 * 28 * 28 * 128, 4 * 5_000_003])
 @pytest.mark.parametrize("given_scale", [False, True])
 def test_quantize_bit_exact(bits, n, given_scale):
+    """Odd sizes (tails), the benchmark size and a 20M-value tensor."""
     x = fi.relu_gauss((n,), "quant", bits)
     x[::97] *= -1.0           # some negative inputs
     if n > 100:
@@ -141,12 +142,13 @@ def test_quantize_rounding_ties_and_extremes(bits, scale):
     s32 = np.float32(scale)
     qmax = 255 if bits == 8 else 15
     k = np.arange(0, qmax + 2, dtype=np.float32)
-    ties = (k + np.float32(0.5)) * s32                      # float32 products: at or next to ties
-    near = np.concatenate([np.nextafter(ties, np.float32(np.inf)), np.nextafter(ties, np.float32(0))])
-    r = fi.rng("quant-ties", bits, scale)
-    rand = (r.random(4000).astype(np.float32) * np.float32(qmax + 3)) * s32
-    special = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1e-45, -1e-45, 1e-40, 3.4e38, -3.4e38,
-                        s32 * np.float32(1e6), s32], np.float32)
+    with np.errstate(over="ignore"):  # the 3e38 scale overflows to inf on purpose
+        ties = (k + np.float32(0.5)) * s32                  # float32 products: at or next to ties
+        near = np.concatenate([np.nextafter(ties, np.float32(np.inf)), np.nextafter(ties, np.float32(0))])
+        r = fi.rng("quant-ties", bits, scale)
+        rand = (r.random(4000).astype(np.float32) * np.float32(qmax + 3)) * s32
+        special = np.array([0.0, -0.0, np.inf, -np.inf, np.nan, 1e-45, -1e-45, 1e-40, 3.4e38, -3.4e38,
+                            s32 * np.float32(1e6), s32], np.float32)
     x = np.concatenate([ties, near, rand, special]).astype(np.float32)
     if x.size % 2:
         x = np.append(x, np.float32(1.0))
