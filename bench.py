@@ -197,6 +197,103 @@ def cpu_baseline(fi, L, G, bits, budget_s=15.0):
             "seconds": round(t_total, 3)}
 
 
+def stack_layers(fi, depth, batch):
+    """Distinct layer shapes of the ResNet stack with their multiplicities."""
+    out, index = [], {}
+    for L in fi.resnet_convs(depth, batch):
+        key = tuple(L[k] for k in ("H", "W", "C", "O", "R", "S", "stride", "pad"))
+        if key in index:
+            out[index[key]][1] += 1
+        else:
+            index[key] = len(out)
+            out.append([L, 1])
+    return out
+
+
+def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
+    """Per-layer kernel times of a batch-`batch` ResNet-`depth` stack, every
+    distinct layer timed at its full shape (graph replays over `nsets`
+    rotating buffer sets) and counted with its multiplicity.  Inputs are
+    seeded ReLU-Gaussian activations of each layer's shape (the layers are
+    not chained); conv1 has its 3 input channels padded to 4 and uses
+    groups of 4.  Effective ops use the unpadded conv1 reduction (147)."""
+    layers = []
+    tot = dict(conv_us=0.0, quant_us=0.0, ops=0.0, roof_us=0.0, bytes=0.0)
+    gen = torch.Generator(device="cuda")
+    for li, (L, count) in enumerate(stack_layers(fi, depth, batch)):
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        st, pd = L["stride"], L["pad"]
+        g = G if C % G == 0 else 4
+        w = fi.he_weights(O, C, R, S, "stack-bench", depth, L["name"])
+        if L["name"] == "conv1":
+            w[:, 3:] = 0.0
+        codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), g)
+        K = R * S * C
+        prep = fgq.fgq_prepare_weights(codes, alpha, O, K, g)
+        n = B * H * W * C
+        Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
+        M = B * Ho * Wo
+        gen.manual_seed(fi.SEED + 1000 * depth + li)
+        sets = []
+        for _ in range(nsets):
+            x = torch.randn(n, generator=gen, device="cuda").clamp_(min=0.0)
+            if L["name"] == "conv1":
+                x.view(B, H, W, C)[..., 3:] = 0.0
+            q = torch.empty(n * bits // 8, dtype=torch.uint8, device="cuda")
+            sx = torch.empty(1, dtype=torch.float32, device="cuda")
+            ws = torch.empty(fgq.fgq_quantize_ws_bytes(n), dtype=torch.uint8, device="cuda")
+            y = torch.empty((B, Ho, Wo, O), dtype=torch.float32, device="cuda")
+            sets.append((x, q, sx, ws, y))
+
+        def quant(i):
+            x, q, sx, ws, y = sets[i]
+            fgq.fgq_quantize_act(x, bits, q=q, scale_out=sx, ws=ws)
+
+        def conv(i):
+            x, q, sx, ws, y = sets[i]
+            fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, prepared=prep, y=y)
+
+        def graph(fn):
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                for i in range(nsets):
+                    fn(i)
+            return gr
+
+        for i in range(nsets):
+            quant(i)
+            conv(i)
+        torch.cuda.synchronize()
+        gq, gc = graph(quant), graph(conv)
+        gq.replay()
+        gc.replay()
+        _, q_ms = time_graphs(torch, [(gq, reps)])
+        _, c_ms = time_graphs(torch, [(gc, reps)])
+        conv_us = c_ms * 1e3 / (reps * nsets)
+        quant_us = q_ms * 1e3 / (reps * nsets)
+        k_true = R * S * (3 if L["name"] == "conv1" else C)
+        ops = 2.0 * M * O * k_true
+        nbytes = n * bits // 8 + O * K // 4 + 4 * O * K // g + 4 * M * O
+        roof_us = max(ops / (INT8_PEAK_TOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+        layers.append([L["name"], count, round(conv_us, 2), round(roof_us / conv_us, 3)])
+        tot["conv_us"] += count * conv_us
+        tot["quant_us"] += count * quant_us
+        tot["ops"] += count * ops
+        tot["roof_us"] += count * roof_us
+        tot["bytes"] += count * nbytes
+        del sets, gq, gc, prep, codes, alpha
+        torch.cuda.empty_cache()
+    return {"workload": f"ResNet-{depth} conv stack, batch {batch}, G={G}, u{bits} (conv1 at G=4)",
+            "layers_total": sum(c for _, c in stack_layers(fi, depth, batch)), "distinct": len(layers),
+            "sum_conv_us": round(tot["conv_us"], 1), "sum_quantize_us": round(tot["quant_us"], 1),
+            "effective_tops_conv": round(tot["ops"] / (tot["conv_us"] * 1e-6) / 1e12, 1),
+            "effective_tops_with_quantize": round(tot["ops"] / ((tot["conv_us"] + tot["quant_us"]) * 1e-6) / 1e12, 1),
+            "sum_roofline_us": round(tot["roof_us"], 1),
+            "roofline_frac": round(tot["roof_us"] / tot["conv_us"], 4),
+            "algorithmic_bytes": int(tot["bytes"]),
+            "per_layer": layers}
+
+
 def kernel_source_hash(G):
     """sha256 of the conv kernel's sources with // comments and blank lines
     removed, so that a comment edit does not invalidate the counters."""
@@ -251,6 +348,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=100)
     ap.add_argument("--sets", type=int, default=40, help="rotating buffer sets (~29 MB each)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
+    ap.add_argument("--no-stacks", action="store_true", help="skip the ResNet stack measurements")
     ap.add_argument("--direct", action="store_true", help="time the direct per-group kernels")
     ap.add_argument("--profile-steps", type=int, default=0,
                     help="for profilers: run this many eager steps per group size (no graphs, "
@@ -356,6 +454,12 @@ def main():
                     "conv_only_tops": round(ops11 / (r11["conv_us"] * 1e-6) / 1e12, 1),
                     "roofline": roofline(LAYER_1X1, 64, bits, r11["conv_us"])},
     }
+    if not args.no_stacks:
+        out["stacks"] = {}
+        for depth, G, sbits in ((50, 4, 8), (101, 64, 4)):
+            log(f"[bench] ResNet-{depth} stack, G={G}, u{sbits}")
+            out["stacks"][f"resnet{depth}_b64_g{G}_u{sbits}"] = stack_measure(torch, fgq, fi, depth, G, sbits)
+            log(f"[bench] ResNet-{depth}: sum conv {out['stacks'][f'resnet{depth}_b64_g{G}_u{sbits}']['sum_conv_us']} us")
     if not args.no_cpu:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(fi, LAYER, 4, bits)

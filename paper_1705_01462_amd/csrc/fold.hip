@@ -55,12 +55,12 @@ struct FoldArgs {
   int32_t nks, planes_bytes;
 };
 
-template <int kBits, int kNWO, int kNB, bool kSmallC>
+template <int kBits, int kNWO, int kNB, int kCM>
 __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
   constexpr int kTM = kNWM * kNB * 32;
-  using Stager = ActStager<kBits, kTM, kSmallC>;
+  using Stager = StagerFor<kBits, kTM, kCM>;
   constexpr int kXP = Stager::kXP;
   constexpr int kStage = Stager::kStage;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kStage];
@@ -213,12 +213,13 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   a.x.n_mtiles = (a.x.M + kTM - 1) / kTM;
   const int64_t n = static_cast<int64_t>(a.x.n_otiles) * a.x.n_mtiles;
   if (n > 0x7fffffffLL) return FGQ_ERR_SHAPE;
-  if (a.x.C < kKT)
-    hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, true>), dim3(static_cast<uint32_t>(n)),
-                       dim3(kThreads), 0, st, a);
-  else
-    hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, false>), dim3(static_cast<uint32_t>(n)),
-                       dim3(kThreads), 0, st, a);
+  const dim3 grid(static_cast<uint32_t>(n));
+  switch (c_mode(a.x.C)) {
+    case 0: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 0>), grid, dim3(kThreads), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 1>), grid, dim3(kThreads), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 4>), grid, dim3(kThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 8>), grid, dim3(kThreads), 0, st, a); break;
+  }
   return last_launch();
 }
 
@@ -256,7 +257,7 @@ fgq_status launch_bits(const FoldArgs& a, hipStream_t st) {
 
 bool fold_supported(const ConvGeom& g, const uint8_t* q) {
   const PreparedLayout L = prepared_layout(g.O, g.K, g.G);
-  return L.kind == kPrepFold && g.K < (1LL << 17) && ig::igemm_shape_ok(g, q) &&
+  return L.kind == kPrepFold && g.K < (1LL << 17) && ig::igemm_shape_ok(g, q, /*tiny_c=*/true) &&
          3 * L.O32 * L.Kp < (1LL << 31);
 }
 

@@ -38,12 +38,12 @@ struct GroupArgs {
 
 constexpr int kBlkBytes = 2 * 64 * 16;  // one channel tile, one group
 
-template <int kBits, int kNWO, int kNB, bool kSmallC>
+template <int kBits, int kNWO, int kNB, int kCM>
 __global__ __launch_bounds__(kThreads, 1) void group_conv_kernel(GroupArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
   constexpr int kTM = kNWM * kNB * 32;
-  using Stager = ActStager<kBits, kTM, kSmallC>;
+  using Stager = StagerFor<kBits, kTM, kCM>;
   constexpr int kStage = Stager::kStage;
   __shared__ __attribute__((aligned(16))) unsigned char lds[2 * kStage];
 
@@ -174,10 +174,10 @@ fgq_status launch_cfg(const GroupArgs& a0, hipStream_t st) {
   const int64_t n = static_cast<int64_t>(a.x.n_otiles) * a.x.n_mtiles;
   if (n > 0x7fffffffLL) return FGQ_ERR_SHAPE;
   if (a.x.C < kKT)
-    hipLaunchKernelGGL((group_conv_kernel<kBits, kNWO, kNB, true>), dim3(static_cast<uint32_t>(n)),
+    hipLaunchKernelGGL((group_conv_kernel<kBits, kNWO, kNB, 1>), dim3(static_cast<uint32_t>(n)),
                        dim3(kThreads), 0, st, a);
   else
-    hipLaunchKernelGGL((group_conv_kernel<kBits, kNWO, kNB, false>), dim3(static_cast<uint32_t>(n)),
+    hipLaunchKernelGGL((group_conv_kernel<kBits, kNWO, kNB, 0>), dim3(static_cast<uint32_t>(n)),
                        dim3(kThreads), 0, st, a);
   return last_launch();
 }

@@ -169,6 +169,105 @@ struct ActStager {
   }
 };
 
+// Activation staging for C = 4 or 8 (kC), e.g. a first layer whose three
+// image channels are padded to 4: a 16-element piece spans 16/kC taps, and
+// the kC channels of one tap are the only contiguous run, so each tap is
+// loaded on its own (kC bytes, or kC/2 for 4-bit activations) with its own
+// bounds test and the piece is assembled in registers.  Same interface and
+// LDS layout as ActStager.
+template <int kBits, int kTM, int kC>
+struct ActStagerTinyC {
+  static_assert(kC == 4 || kC == 8, "tiny-C staging is for C = 4 or 8");
+  static constexpr int kPieces = kTM * kSlots;
+  static constexpr int kXP = (kPieces + kThreads - 1) / kThreads;
+  static constexpr int kStage = (kTM + (kXP * kThreads - kPieces) / kSlots) * kRowB;
+  static constexpr int kSub = 16 / kC;  // taps per piece
+
+  int rowbase[kXP], hi0[kXP], wi0[kXP], xlds[kXP];
+  bool rowok[kXP];
+  int tk;
+  uint32_t part[kXP][kSub][kC * kBits / 32 > 0 ? kC * kBits / 32 : 1];
+  __amdgpu_buffer_rsrc_t rs;
+
+  __device__ void init(const ActArgs& a, int m0, int tid) {
+    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
+#pragma unroll
+    for (int i = 0; i < kXP; ++i) {
+      const int p = tid + kThreads * i;
+      const int m = m0 + p / kSlots;
+      rowok[i] = (p < kPieces) && (m < a.M);
+      const int mm = rowok[i] ? m : 0;
+      const int wo_ = mm % a.Wo;
+      const int t = mm / a.Wo;
+      const int ho = t % a.Ho;
+      const int b = t / a.Ho;
+      hi0[i] = ho * a.sh - a.ph;
+      wi0[i] = wo_ * a.sw - a.pw;
+      rowbase[i] = (b * a.H + hi0[i]) * a.W + wi0[i];
+      xlds[i] = lds_off(p / kSlots, p % kSlots);
+    }
+    tk = 16 * (tid % kSlots);
+  }
+
+  __device__ void advance(const ActArgs&) { tk += kKT; }
+
+  __device__ void load(const ActArgs& a) {
+#pragma unroll
+    for (int j = 0; j < kSub; ++j) {
+      const int k = tk + j * kC;
+      const int tap = k / kC;
+      const int r = tap / a.S;
+      const int t = tap - r * a.S;
+#pragma unroll
+      for (int i = 0; i < kXP; ++i) {
+        const int hi = hi0[i] + r, wi = wi0[i] + t;
+        const bool ok = rowok[i] & (k < a.K) & (static_cast<unsigned>(hi) < static_cast<unsigned>(a.H)) &
+                        (static_cast<unsigned>(wi) < static_cast<unsigned>(a.W));
+        const int e = (rowbase[i] + r * a.W + t) * kC;  // element offset of the tap
+        if constexpr (kBits == 8 && kC == 4) {
+          part[i][j][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, ok ? static_cast<uint32_t>(e) : kOutOfRange, 0, 0);
+        } else if constexpr (kBits == 8) {
+          const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, ok ? static_cast<uint32_t>(e) : kOutOfRange, 0, 0);
+          part[i][j][0] = static_cast<uint32_t>(v.x);
+          part[i][j][1] = static_cast<uint32_t>(v.y);
+        } else if constexpr (kC == 4) {
+          part[i][j][0] = __builtin_amdgcn_raw_buffer_load_b16(rs, ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange, 0, 0);
+        } else {
+          part[i][j][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange, 0, 0);
+        }
+      }
+    }
+  }
+
+  __device__ void store(unsigned char* base, uint32_t mask8) {
+#pragma unroll
+    for (int i = 0; i < kXP; ++i) {
+      v4i v;
+      if constexpr (kBits == 8) {
+        uint32_t w[4];
+#pragma unroll
+        for (int j = 0; j < kSub; ++j)
+#pragma unroll
+          for (int d = 0; d < kC / 4; ++d) w[j * (kC / 4) + d] = part[i][j][d] ^ mask8;
+        v = v4i{static_cast<int>(w[0]), static_cast<int>(w[1]), static_cast<int>(w[2]), static_cast<int>(w[3])};
+      } else if constexpr (kC == 4) {
+        v = unpack_u4x16(part[i][0][0] | (part[i][1][0] << 16), part[i][2][0] | (part[i][3][0] << 16));
+      } else {
+        v = unpack_u4x16(part[i][0][0], part[i][1][0]);
+      }
+      *reinterpret_cast<v4i*>(base + xlds[i]) = v;
+    }
+  }
+};
+
+// kCM: how the reduction index maps onto taps.  0: C % 16 == 0, C >= 128
+// (at most one tap boundary per step); 1: C % 16 == 0, C < 128; 4 / 8:
+// C = 4 / 8 (tiny-C staging).
+template <int kBits, int kTM, int kCM>
+using StagerFor = typename std::conditional<
+    (kCM <= 1), ActStager<kBits, kTM, kCM == 1>,
+    ActStagerTinyC<kBits, kTM, (kCM == 4 || kCM == 8) ? kCM : 4>>::type;
+
 // Fill the size fields of ActArgs from a validated geometry.
 inline void fill_act_args(const ConvGeom& g, const uint8_t* q, ActArgs* a) {
   a->q = q;
@@ -191,15 +290,20 @@ inline void fill_act_args(const ConvGeom& g, const uint8_t* q, ActArgs* a) {
   a->n_otiles = a->n_mtiles = 0;
 }
 
-// Size limits shared by the matrix-core kernels: 16-channel pieces, 32-bit
-// element offsets, and an activation buffer aligned for 16-byte (uint8) or
-// 8-byte (uint4) loads.
-inline bool igemm_shape_ok(const ConvGeom& g, const uint8_t* q) {
+// Size limits shared by the matrix-core kernels: 16-channel pieces (or the
+// tiny-C staging when allowed), 32-bit element offsets, and an activation
+// buffer aligned for its widest load.
+inline bool igemm_shape_ok(const ConvGeom& g, const uint8_t* q, bool tiny_c = false) {
   const uintptr_t qa = reinterpret_cast<uintptr_t>(q);
   const int64_t in_elems = g.B * g.H * g.W * g.C;
-  return g.C % 16 == 0 && g.K < (1LL << 30) && qa % (g.bits == 8 ? 16 : 8) == 0 &&
-         in_elems < (1LL << 31) && g.M < (1LL << 31) && g.O < (1LL << 30);
+  const bool c16 = g.C % 16 == 0;
+  const bool ctiny = tiny_c && (g.C == 4 || g.C == 8);
+  const uintptr_t align = c16 ? (g.bits == 8 ? 16 : 8) : static_cast<uintptr_t>(g.C * g.bits / 8);
+  return (c16 || ctiny) && g.K < (1LL << 30) && qa % align == 0 && in_elems < (1LL << 31) &&
+         g.M < (1LL << 31) && g.O < (1LL << 30);
 }
+
+inline int c_mode(int64_t C) { return C % 16 == 0 ? (C >= kKT ? 0 : 1) : static_cast<int>(C); }
 
 }  // namespace ig
 }  // namespace fgq

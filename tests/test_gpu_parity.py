@@ -182,6 +182,9 @@ LAYER_CASES = [
     (2, 12, 12, 32, 64, 1, 1, 2, 0, 8, 4),
     (1, 5, 5, 128, 130, 3, 3, 1, 1, 4, 8),
     (2, 15, 15, 4, 16, 7, 7, 2, 3, 4, 8),      # conv1-like, C padded to 4
+    (2, 15, 15, 4, 40, 7, 7, 2, 3, 4, 4),      # the same with 4-bit activations
+    (2, 11, 13, 8, 36, 3, 3, 1, 1, 8, 8),      # C = 8: two taps per 16-channel piece
+    (2, 11, 13, 8, 36, 5, 5, 2, 2, 4, 4),
     (2, 6, 6, 6, 5, 3, 3, 1, 1, 3, 8),         # G = 3, C % 4 != 0
     (2, 6, 6, 16, 9, 3, 3, 1, 1, 1, 4),        # G = 1
     (4, 14, 14, 256, 64, 1, 1, 1, 0, 64, 8),
