@@ -56,7 +56,7 @@ struct FoldArgs {
 };
 
 template <int kBits, int kNWO, int kNB, int kCM>
-__global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
+__global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(FoldArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
   constexpr int kTM = kNWM * kNB * 32;
@@ -127,18 +127,35 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
 
   auto compute = [&](int stage, const v4i (&w)[3][4]) {
     const unsigned char* base = lds + stage * kStage;
-    v4i xf[kNB][4];
+    if constexpr (kNB <= 2) {
+      // Two workgroups share the compute unit: read each K slice's
+      // fragments just before use (fewer live registers); the other
+      // workgroup's waves cover the LDS latency.
 #pragma unroll
-    for (int c = 0; c < kNB; ++c)
+      for (int h = 0; h < 4; ++h) {
+        v4i xf[kNB];
 #pragma unroll
-      for (int h = 0; h < 4; ++h) xf[c][h] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+        for (int c = 0; c < kNB; ++c) xf[c] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
 #pragma unroll
-    for (int h = 0; h < 4; ++h)
+        for (int c = 0; c < kNB; ++c)
+#pragma unroll
+          for (int j = 0; j < 3; ++j)
+            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], w[j][h], acc[j][c], 0, 0, 0);
+      }
+    } else {
+      v4i xf[kNB][4];
 #pragma unroll
       for (int c = 0; c < kNB; ++c)
 #pragma unroll
-        for (int j = 0; j < 3; ++j)
-          acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][h], w[j][h], acc[j][c], 0, 0, 0);
+        for (int h = 0; h < 4; ++h) xf[c][h] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+#pragma unroll
+        for (int c = 0; c < kNB; ++c)
+#pragma unroll
+          for (int j = 0; j < 3; ++j)
+            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][h], w[j][h], acc[j][c], 0, 0, 0);
+    }
   };
 
   // Step ks: prefetch step ks+1 (weights into ring slot (ks+1)%2,
@@ -158,15 +175,17 @@ __global__ __launch_bounds__(kThreads, 1) void fold_conv_kernel(FoldArgs a) {
     // paid once), then the matrix instructions with the prefetch loads and
     // their address arithmetic slotted between them, so the per-CU load
     // path works while the matrix cores do.
+    if constexpr (kNB > 2) {
 #pragma unroll
-    for (int i = 0; i < 4 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      for (int i = 0; i < 4 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-    for (int i = 0; i < 12 + kXP; ++i) {
-      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
-      __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
-      __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+      for (int i = 0; i < 12 + kXP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 12 * kNB - 2 * (12 + kXP) > 0 ? 12 * kNB - 2 * (12 + kXP) : 0, 0);
     }
-    __builtin_amdgcn_sched_group_barrier(0x008, 12 * kNB - 2 * (12 + kXP) > 0 ? 12 * kNB - 2 * (12 + kXP) : 0, 0);
     __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
     xs.store(lds + (1 - u) * kStage, 0x80808080u);  // q - 128 (padding 0 -> -128)
     __syncthreads();
@@ -223,17 +242,18 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   return last_launch();
 }
 
-// Rows per wave (kNB blocks of 32) are chosen so that the workgroups fill
-// the 256 compute units in as few rounds as possible: cost = rounds * kNB.
+// Rows per wave (kNB blocks of 32): the busiest compute unit does
+// ceil(tiles / CUs) workgroups of kNB blocks per SIMD; among equal costs
+// the smaller kNB wins (kNB = 2 runs two workgroups per compute unit).
 template <int kBits, int kNWO>
 fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
   constexpr int kNWM = 4 / kNWO;
   const int64_t otiles = ceil_div(a.x.O, 32 * kNWO);
-  int best = 4;
+  int best = 2;
   int64_t best_cost = -1;
-  for (int nb = 4; nb >= 2; --nb) {
+  for (int nb = 2; nb <= 4; ++nb) {
     const int64_t tiles = otiles * ceil_div(a.x.M, kNWM * nb * 32);
-    const int64_t cost = ceil_div(tiles, 256) * nb;
+    const int64_t cost = ceil_div(tiles, device_cus()) * nb;
     if (best_cost < 0 || cost < best_cost) {
       best_cost = cost;
       best = nb;

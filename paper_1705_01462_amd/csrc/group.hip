@@ -38,8 +38,11 @@ struct GroupArgs {
 
 constexpr int kBlkBytes = 2 * 64 * 16;  // one channel tile, one group
 
+// Two workgroups may share a compute unit (at most 256 registers per lane):
+// with two waves per SIMD, one wave's conversions and multiply-adds run
+// while the other waits on its matrix instructions.
 template <int kBits, int kNWO, int kNB, int kCM>
-__global__ __launch_bounds__(kThreads, 1) void group_conv_kernel(GroupArgs a) {
+__global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
   constexpr int kTM = kNWM * kNB * 32;
@@ -182,17 +185,18 @@ fgq_status launch_cfg(const GroupArgs& a0, hipStream_t st) {
   return last_launch();
 }
 
-// Rows per wave (kNB blocks of 32) are chosen so that the workgroups fill
-// the 256 compute units in as few rounds as possible: cost = rounds * kNB.
+// Rows per wave (kNB blocks of 32): the busiest compute unit does
+// ceil(tiles / CUs) workgroups of kNB blocks per SIMD; among equal costs
+// the smaller kNB wins (more waves to overlap).
 template <int kBits, int kNWO>
 fgq_status launch_nwo(const GroupArgs& a, hipStream_t st) {
   constexpr int kNWM = 4 / kNWO;
   const int64_t otiles = ceil_div(a.x.O, 32 * kNWO);
-  int best = 4;
+  int best = 2;
   int64_t best_cost = -1;
-  for (int nb = 4; nb >= 2; --nb) {
+  for (int nb = 2; nb <= 4; ++nb) {
     const int64_t tiles = otiles * ceil_div(a.x.M, kNWM * nb * 32);
-    const int64_t cost = ceil_div(tiles, 256) * nb;
+    const int64_t cost = ceil_div(tiles, device_cus()) * nb;
     if (best_cost < 0 || cost < best_cost) {
       best_cost = cost;
       best = nb;

@@ -303,6 +303,30 @@ inline bool igemm_shape_ok(const ConvGeom& g, const uint8_t* q, bool tiny_c = fa
          g.M < (1LL << 31) && g.O < (1LL << 30);
 }
 
+// Compute units of the current device (cached per device; 256 if unknown).
+inline int device_cus() {
+  static int cached[64];
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
+    cached[dev] = n;
+  }
+  return cached[dev];
+}
+
+// Dynamic LDS to request so that a grid of `blocks` workgroups, each with
+// `static_lds` bytes of LDS, runs one workgroup per compute unit when it
+// fits in one round: two co-resident workgroups would share every SIMD and
+// both run at half speed while other compute units idle.
+inline size_t spread_lds(int64_t blocks, size_t static_lds) {
+  constexpr size_t kLdsPerCu = 160 * 1024;
+  if (blocks > device_cus()) return 0;
+  const size_t want = kLdsPerCu / 2 + 1024;
+  return want > static_lds ? want - static_lds : 0;
+}
+
 inline int c_mode(int64_t C) { return C % 16 == 0 ? (C >= kKT ? 0 : 1) : static_cast<int>(C); }
 
 }  // namespace ig
