@@ -294,6 +294,37 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
             "per_layer": layers}
 
 
+def gemm_measure(torch, fgq, fi, M=64, K=256, O=128, G=4, bits=8, nsets=8, reps=50):
+    """Latency of the single FGQ GEMM (M=64, K=256, O=128, W ~ N(0, 0.05^2),
+    G=4, uint8): a launch-latency-bound size, reported in microseconds."""
+    w = fi.gauss_weights(O, K, 0.05, "bench-gemm")
+    codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
+    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+    sets = []
+    for i in range(nsets):
+        x = torch.from_numpy(fi.relu_gauss((M, K), "bench-gemm", i)).cuda()
+        q, sx = fgq.fgq_quantize_act(x, bits)
+        y = torch.empty((M, O), dtype=torch.float32, device="cuda")
+        sets.append((q, sx, y))
+
+    def run(i):
+        q, sx, y = sets[i]
+        fgq.fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep, y=y)
+
+    for i in range(nsets):
+        run(i)
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for i in range(nsets):
+            run(i)
+    g.replay()
+    _, ms = time_graphs(torch, [(g, reps)])
+    us = ms * 1e3 / (reps * nsets)
+    return {"workload": f"FGQ GEMM M={M} K={K} O={O}, G={G}, u{bits}", "us_per_call": round(us, 3),
+            "effective_tops": round(2.0 * M * K * O / (us * 1e-6) / 1e12, 3)}
+
+
 def kernel_source_hash(G):
     """sha256 of the conv kernel's sources with // comments and blank lines
     removed, so that a comment edit does not invalidate the counters."""
@@ -454,6 +485,7 @@ def main():
                     "conv_only_tops": round(ops11 / (r11["conv_us"] * 1e-6) / 1e12, 1),
                     "roofline": roofline(LAYER_1X1, 64, bits, r11["conv_us"])},
     }
+    out["gemm_m64"] = gemm_measure(torch, fgq, fi)
     if not args.no_stacks:
         out["stacks"] = {}
         for depth, G, sbits in ((50, 4, 8), (101, 64, 4)):

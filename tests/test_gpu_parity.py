@@ -56,12 +56,20 @@ def summand_magnitude(ref, x_shape, G, bits, O, R, S, stride, pad, row0, nrows):
 
 
 def assert_fold_close(y, y_ref, mag):
-    err = np.abs(y.astype(np.float64) - y_ref.astype(np.float64))
+    """Element-wise within 1e-5 of the summand magnitude, normwise within
+    1e-5; also reports the largest relative error over the outputs that are
+    not near zero (|y_ref| >= 1e-3 rms)."""
+    yr = y_ref.astype(np.float64)
+    err = np.abs(y.astype(np.float64) - yr)
     bound = TOL * mag
     bad = err > bound
     assert not bad.any(), f"{bad.sum()} outputs beyond 1e-5 of the summand magnitude; " \
                           f"worst ratio {np.max(err / np.maximum(mag, 1e-300)):.3e}"
-    assert np.linalg.norm(err) <= TOL * np.linalg.norm(y_ref.astype(np.float64)) + 1e-30
+    assert np.linalg.norm(err) <= TOL * np.linalg.norm(yr) + 1e-30
+    big = np.abs(yr) >= 1e-3 * np.sqrt(np.mean(yr * yr))
+    if big.any():
+        print(f"[parity] max rel error over |y| >= 1e-3 rms: {np.max(err[big] / np.abs(yr[big])):.2e}; "
+              f"max error / summand magnitude: {np.max(err / np.maximum(mag, 1e-300)):.2e}")
 
 
 # ---------------------------------------------------------------------------
@@ -217,11 +225,7 @@ def test_conv_direct_path_bit_exact(case):
     codes, alpha, _, q, sx = gpu_inputs(w, x, G, bits)
     y = fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, G)
     yh = host(y).reshape(-1, O)
-    if G % 64 == 0:   # matrix-core direct path: fp32 epilogue
-        mag = summand_magnitude(ref, x.shape, G, bits, O, R, S, st, pd, 0, yh.shape[0])
-        assert_fold_close(yh, ref["y"], mag)
-    else:
-        np.testing.assert_array_equal(yh.view(np.uint32), ref["y"].view(np.uint32))
+    np.testing.assert_array_equal(yh.view(np.uint32), ref["y"].view(np.uint32))
 
 
 @pytest.mark.parametrize("case", LAYER_CASES)
@@ -323,10 +327,7 @@ def test_full_size_layers_sampled_rows(case):
                               rows=rows)[row0:row0 + 200]
         mag = summand_magnitude(ref, x.shape, G, bits, O, R, S, st, pd, row0, 200)
         assert_fold_close(y_fold[row0:row0 + 200], y_ref, mag)
-        if G % 64 == 0:
-            assert_fold_close(y_dir[row0:row0 + 200], y_ref, mag)
-        else:
-            np.testing.assert_array_equal(y_dir[row0:row0 + 200], y_ref)
+        np.testing.assert_array_equal(y_dir[row0:row0 + 200].view(np.uint32), y_ref.view(np.uint32))
 
 
 @pytest.mark.parametrize("G", [4, 64])
