@@ -1,7 +1,7 @@
 """GPU parity: the HIP path (through the C ABI) against the CPU oracle on the
 same seeded inputs.
 
-Bars (see DESIGN.md): ternary codes, alpha, Delta, quantized activations,
+Bars: ternary codes, alpha, Delta, quantized activations,
 the scale and int32 group sums are bit-exact; the direct per-group layer
 kernel (fp64 alpha epilogue) is bit-exact too; the matrix-core kernels
 (folded-scale for G != 64, per-group for G = 64) are within 1e-5 of the
