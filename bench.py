@@ -41,8 +41,10 @@ TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_conv_b32.json")
 _CSRC = "paper_1705_01462_amd/csrc/"
 # Sources of the convolution kernel that runs at each group size.
 KERNEL_SOURCES = {
-    4: [_CSRC + f for f in ("fold.hip", "igemm.h", "prepare.hip", "fgq_internal.h")],
-    64: [_CSRC + f for f in ("group.hip", "igemm.h", "prepare.hip", "fgq_internal.h")],
+    4: [_CSRC + f for f in ("fold.hip", "fold_kernel.h", "igemm.h", "epilogue.h", "qcode.h", "prepare.hip",
+                            "fgq_internal.h")],
+    64: [_CSRC + f for f in ("group.hip", "group_kernel.h", "igemm.h", "epilogue.h", "qcode.h", "prepare.hip",
+                             "fgq_internal.h")],
 }
 
 
@@ -61,11 +63,12 @@ def layer_dims(L):
     return M, K, Ho, Wo
 
 
-def algorithmic_bytes(L, G, bits):
-    """Activations in + 2-bit codes + fp32 alpha + fp32 output (per launch)."""
+def algorithmic_bytes(L, G, bits, out_bits=32):
+    """Activations in + 2-bit codes + fp32 alpha + output (fp32, or the next
+    layer's 8-/4-bit codes), per launch."""
     M, K, _, _ = layer_dims(L)
     act = L["B"] * L["H"] * L["W"] * L["C"] * bits // 8
-    return act + L["O"] * K // 4 + 4 * L["O"] * K // G + 4 * M * L["O"]
+    return act + L["O"] * K // 4 + 4 * L["O"] * K // G + M * L["O"] * out_bits // 8
 
 
 class Setup:
@@ -90,6 +93,16 @@ class Setup:
             y = torch.empty((L["B"], Ho, Wo, L["O"]), dtype=torch.float32, device="cuda")
             self.sets.append((x, q, sx, ws, y))
         self.shape = (L["B"], L["H"], L["W"], L["C"])
+        # fused next-layer quantization: one output code buffer per set and a
+        # static scale, calibrated from one fp32 output by calibrate()
+        self.q_out = [torch.empty(M * L["O"] * bits // 8, dtype=torch.uint8, device="cuda")
+                      for _ in range(nsets)]
+        self.out_scale = torch.ones(1, dtype=torch.float32, device="cuda")
+
+    def calibrate(self):
+        """Static output scale: the largest fp32 output of set 0 maps to the top code."""
+        self.step(0)
+        self.out_scale.fill_(float(self.sets[0][4].max()) / (2 ** self.bits - 1))
 
     def quantize(self, i):
         x, q, sx, ws, y = self.sets[i]
@@ -100,6 +113,13 @@ class Setup:
         L = self.L
         self.fgq.fgq_conv2d(q, self.bits, sx, self.shape, self.codes, self.alpha, L["O"], L["R"],
                             L["S"], L["stride"], L["pad"], self.G, prepared=self.prep, y=y)
+
+    def conv_q(self, i):
+        x, q, sx, ws, y = self.sets[i]
+        L = self.L
+        self.fgq.fgq_conv2d_q(q, self.bits, sx, self.shape, self.codes, self.alpha, L["O"], L["R"],
+                              L["S"], L["stride"], L["pad"], self.G, self.bits, self.out_scale,
+                              prepared=self.prep, q_out=self.q_out[i])
 
     def step(self, i):
         self.quantize(i)
@@ -159,7 +179,20 @@ def measure(torch, st, steps, warmup, conv_reps=20):
     quant_g.replay()
     _, quant_ms = time_graphs(torch, [(quant_g, conv_reps)])
     quant_us = quant_ms * 1e3 / (conv_reps * nsets)
-    return dict(wall_ms=wall_ms, gpu_ms=gpu_ms, conv_us=conv_us, quant_us=quant_us)
+    # the convolution with the next layer's quantization fused (static scale);
+    # its graph replay is checked against an eager call first
+    st.calibrate()
+    st.conv_q(0)
+    torch.cuda.synchronize()
+    q_eager = st.q_out[0].clone()
+    fused_g = st.graph(st.conv_q, nsets)
+    fused_g.replay()
+    torch.cuda.synchronize()
+    if not torch.equal(st.q_out[0], q_eager):
+        raise RuntimeError("fused graph replay differs from eager execution")
+    _, fused_ms = time_graphs(torch, [(fused_g, conv_reps)])
+    fused_us = fused_ms * 1e3 / (conv_reps * nsets)
+    return dict(wall_ms=wall_ms, gpu_ms=gpu_ms, conv_us=conv_us, quant_us=quant_us, conv_fused_us=fused_us)
 
 
 def cpu_baseline(fi, L, G, bits, budget_s=15.0):
@@ -216,9 +249,12 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
     rotating buffer sets) and counted with its multiplicity.  Inputs are
     seeded ReLU-Gaussian activations of each layer's shape (the layers are
     not chained); conv1 has its 3 input channels padded to 4 and uses
-    groups of 4.  Effective ops use the unpadded conv1 reduction (147)."""
+    groups of 4.  Effective ops use the unpadded conv1 reduction (147).
+    Each layer is also timed with the next layer's quantization fused
+    (fgq_conv2d_q, `bits`-bit codes, static scale from one fp32 output): a
+    chain of such layers needs one fgq_quantize_act, for the network input."""
     layers = []
-    tot = dict(conv_us=0.0, quant_us=0.0, ops=0.0, roof_us=0.0, bytes=0.0)
+    tot = dict(conv_us=0.0, quant_us=0.0, fused_us=0.0, ops=0.0, roof_us=0.0, bytes=0.0, first_quant_us=0.0)
     gen = torch.Generator(device="cuda")
     for li, (L, count) in enumerate(stack_layers(fi, depth, batch)):
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
@@ -244,6 +280,8 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
             ws = torch.empty(fgq.fgq_quantize_ws_bytes(n), dtype=torch.uint8, device="cuda")
             y = torch.empty((B, Ho, Wo, O), dtype=torch.float32, device="cuda")
             sets.append((x, q, sx, ws, y))
+        q_outs = [torch.empty(M * O * bits // 8, dtype=torch.uint8, device="cuda") for _ in range(nsets)]
+        out_scale = torch.ones(1, dtype=torch.float32, device="cuda")
 
         def quant(i):
             x, q, sx, ws, y = sets[i]
@@ -252,6 +290,11 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
         def conv(i):
             x, q, sx, ws, y = sets[i]
             fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, prepared=prep, y=y)
+
+        def conv_q(i):
+            x, q, sx, ws, y = sets[i]
+            fgq.fgq_conv2d_q(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, bits, out_scale,
+                             prepared=prep, q_out=q_outs[i])
 
         def graph(fn):
             gr = torch.cuda.CUDAGraph()
@@ -263,34 +306,46 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
         for i in range(nsets):
             quant(i)
             conv(i)
+        out_scale.fill_(float(sets[0][4].max()) / (2 ** bits - 1))
+        for i in range(nsets):
+            conv_q(i)
         torch.cuda.synchronize()
-        gq, gc = graph(quant), graph(conv)
+        gq, gc, gf = graph(quant), graph(conv), graph(conv_q)
         gq.replay()
         gc.replay()
+        gf.replay()
         _, q_ms = time_graphs(torch, [(gq, reps)])
         _, c_ms = time_graphs(torch, [(gc, reps)])
+        _, f_ms = time_graphs(torch, [(gf, reps)])
         conv_us = c_ms * 1e3 / (reps * nsets)
         quant_us = q_ms * 1e3 / (reps * nsets)
+        fused_us = f_ms * 1e3 / (reps * nsets)
         k_true = R * S * (3 if L["name"] == "conv1" else C)
         ops = 2.0 * M * O * k_true
         nbytes = n * bits // 8 + O * K // 4 + 4 * O * K // g + 4 * M * O
         roof_us = max(ops / (INT8_PEAK_TOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
-        layers.append([L["name"], count, round(conv_us, 2), round(roof_us / conv_us, 3)])
+        layers.append([L["name"], count, round(conv_us, 2), round(roof_us / conv_us, 3), round(fused_us, 2)])
         tot["conv_us"] += count * conv_us
         tot["quant_us"] += count * quant_us
+        tot["fused_us"] += count * fused_us
+        if li == 0:
+            tot["first_quant_us"] = quant_us
         tot["ops"] += count * ops
         tot["roof_us"] += count * roof_us
         tot["bytes"] += count * nbytes
-        del sets, gq, gc, prep, codes, alpha
+        del sets, q_outs, gq, gc, gf, prep, codes, alpha
         torch.cuda.empty_cache()
     return {"workload": f"ResNet-{depth} conv stack, batch {batch}, G={G}, u{bits} (conv1 at G=4)",
             "layers_total": sum(c for _, c in stack_layers(fi, depth, batch)), "distinct": len(layers),
             "sum_conv_us": round(tot["conv_us"], 1), "sum_quantize_us": round(tot["quant_us"], 1),
             "effective_tops_conv": round(tot["ops"] / (tot["conv_us"] * 1e-6) / 1e12, 1),
             "effective_tops_with_quantize": round(tot["ops"] / ((tot["conv_us"] + tot["quant_us"]) * 1e-6) / 1e12, 1),
+            "sum_conv_fused_us": round(tot["fused_us"], 1),
+            "effective_tops_fused_chain": round(tot["ops"] / ((tot["fused_us"] + tot["first_quant_us"]) * 1e-6) / 1e12, 1),
             "sum_roofline_us": round(tot["roof_us"], 1),
             "roofline_frac": round(tot["roof_us"] / tot["conv_us"], 4),
             "algorithmic_bytes": int(tot["bytes"]),
+            "per_layer_columns": ["layer", "count", "conv_us", "roofline_frac", "conv_fused_us"],
             "per_layer": layers}
 
 
@@ -354,22 +409,33 @@ def measured_traffic(L, G):
     return int(e["fetch_bytes"] + e["write_bytes"])
 
 
-def roofline(L, G, bits, conv_us):
+def roofline(L, G, bits, conv_us, out_bits=32):
     M, K, _, _ = layer_dims(L)
-    nbytes = algorithmic_bytes(L, G, bits)
+    nbytes = algorithmic_bytes(L, G, bits, out_bits)
+    kernel = "fgq_conv2d" if out_bits == 32 else "fgq_conv2d_q"
+    traffic = measured_traffic(L, G) if out_bits == 32 else None
     ops = 2.0 * M * L["O"] * K
     t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
     t_mfma = ops / (INT8_PEAK_TOPS * 1e12)
     if t_hbm >= t_mfma:
         achieved = nbytes / (conv_us * 1e-6) / 1e9
         return {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(L, G),
-                "kernel": "fgq_conv2d", "kernel_us": round(conv_us, 3),
+                "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": traffic,
+                "kernel": kernel, "kernel_us": round(conv_us, 3),
                 "algorithmic_bytes": int(nbytes)}
     achieved = ops / (conv_us * 1e-6) / 1e12
     return {"bound": "mfma", "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
-            "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": measured_traffic(L, G),
-            "kernel": "fgq_conv2d", "kernel_us": round(conv_us, 3), "algorithmic_ops": ops}
+            "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": traffic,
+            "kernel": kernel, "kernel_us": round(conv_us, 3), "algorithmic_ops": ops}
+
+
+def fused_entry(L, G, bits, r, ops):
+    """fgq_conv2d_q (8-bit codes of the next layer's activations, static
+    scale) against fgq_conv2d + that layer's separate fgq_quantize_act."""
+    return {"kernel": "fgq_conv2d_q", "out_bits": bits, "conv_fused_us": round(r["conv_fused_us"], 3),
+            "conv_fp32_us": round(r["conv_us"], 3),
+            "chained_layer_tops": round(ops / (r["conv_fused_us"] * 1e-6) / 1e12, 1),
+            "roofline": roofline(L, G, bits, r["conv_fused_us"], out_bits=bits)}
 
 
 def main():
@@ -377,7 +443,9 @@ def main():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=2000)
     ap.add_argument("--warmup", type=int, default=100)
-    ap.add_argument("--sets", type=int, default=40, help="rotating buffer sets (~29 MB each)")
+    ap.add_argument("--sets", type=int, default=96,
+                    help="rotating buffer sets (~32 MB each; the 96 sets of 3.2 MB layer inputs "
+                         "exceed the 256 MB memory-side cache)")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-stacks", action="store_true", help="skip the ResNet stack measurements")
     ap.add_argument("--direct", action="store_true", help="time the direct per-group kernels")
@@ -386,6 +454,8 @@ def main():
                          "no timing) and exit")
     ap.add_argument("--layers", default="conv3x_g4,conv3x_g64,1x1_g64",
                     help="layer configurations for --profile-steps")
+    ap.add_argument("--profile-fused", action="store_true",
+                    help="with --profile-steps: each step also runs fgq_conv2d_q (8-bit output codes)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FGQ layer is "
@@ -408,8 +478,12 @@ def main():
         for name in args.layers.split(","):
             L, G = CONFIGS[name]
             st = Setup(torch, fgq, fi, L, G, bits, 4, folded=not args.direct)
+            if args.profile_fused:
+                st.calibrate()
             for i in range(args.profile_steps):
                 st.step(i % 4)
+                if args.profile_fused:
+                    st.conv_q(i % 4)
             torch.cuda.synchronize()
             log(f"[bench] profile {name} ({layer_key(L, G)}): {args.profile_steps} eager steps done")
             del st
@@ -472,18 +546,21 @@ def main():
         "step_detail": {"conv_us": round(r4["conv_us"], 3), "quantize_us": round(r4["quant_us"], 3),
                         "gpu_ms_per_step": round(r4["gpu_ms"] / args.steps, 5),
                         "conv_only_tops": round(ops / (r4["conv_us"] * 1e-6) / 1e12, 1)},
+        "fused": fused_entry(LAYER, 4, bits, r4, ops),
         "g64": {"workload": "same layer, G=64", "steps": steps64,
                 "value": round(ops / (r64["wall_ms"] / steps64 * 1e-3) / 1e12, 2),
                 "ms_per_step": round(r64["wall_ms"] / steps64, 5),
                 "conv_us": round(r64["conv_us"], 3),
                 "conv_only_tops": round(ops / (r64["conv_us"] * 1e-6) / 1e12, 1),
-                "roofline": roofline(LAYER, 64, bits, r64["conv_us"])},
+                "roofline": roofline(LAYER, 64, bits, r64["conv_us"]),
+                "fused": fused_entry(LAYER, 64, bits, r64, ops)},
         "g64_1x1": {"workload": "ResNet-50 1x1 conv 256->64, 56x56, batch 32, G=64", "steps": steps64,
                     "value": round(ops11 / (r11["wall_ms"] / steps64 * 1e-3) / 1e12, 2),
                     "ms_per_step": round(r11["wall_ms"] / steps64, 5),
                     "conv_us": round(r11["conv_us"], 3), "quantize_us": round(r11["quant_us"], 3),
                     "conv_only_tops": round(ops11 / (r11["conv_us"] * 1e-6) / 1e12, 1),
-                    "roofline": roofline(LAYER_1X1, 64, bits, r11["conv_us"])},
+                    "roofline": roofline(LAYER_1X1, 64, bits, r11["conv_us"]),
+                    "fused": fused_entry(LAYER_1X1, 64, bits, r11, ops11)},
     }
     out["gemm_m64"] = gemm_measure(torch, fgq, fi)
     if not args.no_stacks:

@@ -209,6 +209,35 @@ fgq_status fgq_gemm(const uint8_t* q, int32_t bits, const float* sx,
                     int32_t G, float* y, void* stream);
 
 /*
+ * fgq_conv2d_q / fgq_gemm_q -- the same layers with the next layer's
+ * activation quantization fused into the epilogue (Sec. 4: activations are
+ * quantized before each convolution; the quantization's clamp at 0 is the
+ * ReLU between layers).  Instead of y, writes
+ *   q_out = fgq_quantize_act(y, out_bits, scale_in = out_scale)
+ * for the y that fgq_conv2d / fgq_gemm computes with the same arguments,
+ * bit for bit (same kernels, same arithmetic; the quantization follows
+ * fgq_quantize_act exactly).  The scale is given (a per-layer calibrated
+ * scale); a dynamic scale needs the whole output first and is not fused.
+ *
+ * out_bits  [in]  8 or 4 (4 needs O even)
+ * out_scale [in]  device fp32 scalar, a positive finite value
+ * q_out     [out] NHWC [B][Ho][Wo][O] bytes (8) or [B][Ho][Wo][O/2] (4: the
+ *                 even channel in the low nibble) -- the next layer's q
+ */
+fgq_status fgq_conv2d_q(const uint8_t* q, int32_t bits, const float* sx,
+                        int64_t B, int64_t H, int64_t W, int64_t C,
+                        const uint8_t* codes, const float* alpha,
+                        const void* prepared, int64_t O, int32_t R, int32_t S,
+                        int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                        int32_t pad_w, int32_t G, int32_t out_bits,
+                        const float* out_scale, uint8_t* q_out, void* stream);
+fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx,
+                      int64_t M, int64_t K, const uint8_t* codes,
+                      const float* alpha, const void* prepared, int64_t O,
+                      int32_t G, int32_t out_bits, const float* out_scale,
+                      uint8_t* q_out, void* stream);
+
+/*
  * fgq_group_sums -- the exact integer group sums P[m][o][g] (Sec. 4: 32-bit
  * accumulation) of fgq_conv2d's geometry for output rows m in
  * [row0, row0 + nrows), m = (b*Ho + ho)*Wo + wo.

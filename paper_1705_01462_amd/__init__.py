@@ -49,6 +49,9 @@ _SIGS = {
     "fgq_conv2d": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
                     _I32, _I32, _I32, _I32, _I32, _P, _P], _I32),
     "fgq_gemm": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _P, _P], _I32),
+    "fgq_conv2d_q": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
+                      _I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
+    "fgq_gemm_q": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _I32, _P, _P, _P], _I32),
     "fgq_group_sums": ([_P, _I32, _I64, _I64, _I64, _I64, _P, _I64, _I32, _I32, _I32, _I32,
                         _I32, _I32, _I32, _I64, _I64, _P, _P], _I32),
 }
@@ -185,6 +188,38 @@ def fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=None, y=None):
                         O, G, _dev(y, torch.float32, "y"), _stream())
     _check(rc, "fgq_gemm")
     return y
+
+
+def fgq_conv2d_q(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, G, out_bits, out_scale,
+                 prepared=None, q_out=None):
+    """fgq_conv2d with the next layer's quantization fused: returns uint8
+    codes NHWC [B][Ho][Wo][O] (out_bits 8) or [B][Ho][Wo][O/2] (out_bits 4)
+    with the device scale out_scale (fp32[1])."""
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv_out_hw(H, W, R, S, (sh, sw), (ph, pw))
+    if q_out is None:
+        q_out = torch.empty((B, Ho, Wo, O * out_bits // 8), dtype=torch.uint8, device=q.device)
+    rc = lib().fgq_conv2d_q(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), B, H, W, C,
+                            _dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                            None if prepared is None else _dev(prepared, torch.uint8, "prepared"),
+                            O, R, S, sh, sw, ph, pw, G, out_bits, _dev(out_scale, torch.float32, "out_scale"),
+                            _dev(q_out, torch.uint8, "q_out"), _stream())
+    _check(rc, "fgq_conv2d_q")
+    return q_out
+
+
+def fgq_gemm_q(q, bits, sx, M, K, codes, alpha, O, G, out_bits, out_scale, prepared=None, q_out=None):
+    if q_out is None:
+        q_out = torch.empty((M, O * out_bits // 8), dtype=torch.uint8, device=q.device)
+    rc = lib().fgq_gemm_q(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), M, K,
+                          _dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                          None if prepared is None else _dev(prepared, torch.uint8, "prepared"),
+                          O, G, out_bits, _dev(out_scale, torch.float32, "out_scale"),
+                          _dev(q_out, torch.uint8, "q_out"), _stream())
+    _check(rc, "fgq_gemm_q")
+    return q_out
 
 
 def fgq_group_sums(q, bits, shape, codes, O, R, S, stride, pad, G, row0, nrows, P=None):

@@ -26,12 +26,18 @@ FLAGS = [
 ]
 
 
-# Per-source flags.  group.hip converts every matrix-core result on the
-# vector ALU, so its results must be allocated in ordinary VGPRs (otherwise
-# each value is first copied out of an accumulation register).
+# Per-source flags, by file-name prefix.  The per-group kernels (group*.hip)
+# convert every matrix-core result on the vector ALU, so their results must
+# be allocated in ordinary VGPRs (otherwise each value is first copied out of
+# an accumulation register).
 EXTRA = {
-    "group.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
+    "group": ["-mllvm", "-amdgpu-mfma-vgpr-form=1"],
 }
+
+
+def extra_flags(src):
+    name = os.path.basename(src)
+    return [f for prefix, flags in EXTRA.items() if name.startswith(prefix) for f in flags]
 
 
 def sources():
@@ -40,7 +46,7 @@ def sources():
 
 def _compile(src, verbose):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = ["hipcc", *FLAGS, *EXTRA.get(os.path.basename(src), []), "-c", src, "-o", obj]
+    cmd = ["hipcc", *FLAGS, *extra_flags(src), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -54,7 +60,8 @@ def _compile(src, verbose):
 
 def build(verbose=False, jobs=None):
     os.makedirs(BUILD, exist_ok=True)
-    srcs = sources()
+    # the kernel-heavy sources first, so the parallel compile ends together
+    srcs = sorted(sources(), key=lambda s: not os.path.basename(s).startswith(("fold", "group")))
     jobs = jobs or min(len(srcs), 8)
     with cf.ThreadPoolExecutor(jobs) as ex:
         objs = list(ex.map(lambda s: _compile(s, verbose), srcs))

@@ -47,8 +47,8 @@ bool conv_geom(int64_t B, int64_t H, int64_t W, int64_t C, int64_t O, int32_t R,
 }
 
 fgq_status run_layer(const uint8_t* q, const float* sx, const uint8_t* codes,
-                     const float* alpha, const void* prepared, const ConvGeom& g, float* y,
-                     void* stream) {
+                     const float* alpha, const void* prepared, const ConvGeom& g,
+                     const LayerOut& y, void* stream) {
   hipStream_t st = as_stream(stream);
   if (prepared) {
     if (prepared_layout(g.O, g.K, g.G).kind == kPrepGroup) {
@@ -165,7 +165,23 @@ fgq_status fgq_conv2d(const uint8_t* q, int32_t bits, const float* sx, int64_t B
   if (!conv_geom(B, H, W, C, O, R, S, stride_h, stride_w, pad_h, pad_w, G, bits, &g, &err))
     return err;
   if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
-  return run_layer(q, sx, codes, alpha, prepared, g, y, stream);
+  return run_layer(q, sx, codes, alpha, prepared, g, LayerOut{y, nullptr, nullptr, 0}, stream);
+}
+
+fgq_status fgq_conv2d_q(const uint8_t* q, int32_t bits, const float* sx, int64_t B, int64_t H,
+                        int64_t W, int64_t C, const uint8_t* codes, const float* alpha,
+                        const void* prepared, int64_t O, int32_t R, int32_t S, int32_t stride_h,
+                        int32_t stride_w, int32_t pad_h, int32_t pad_w, int32_t G, int32_t out_bits,
+                        const float* out_scale, uint8_t* q_out, void* stream) {
+  if (!q || !sx || !codes || !alpha || !out_scale || !q_out) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(B, H, W, C, O, R, S, stride_h, stride_w, pad_h, pad_w, G, bits, &g, &err))
+    return err;
+  if (out_bits != 8 && out_bits != 4) return FGQ_ERR_BITS;
+  if (out_bits == 4 && O % 2 != 0) return FGQ_ERR_BITS;
+  if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  return run_layer(q, sx, codes, alpha, prepared, g, LayerOut{nullptr, q_out, out_scale, out_bits}, stream);
 }
 
 fgq_status fgq_gemm(const uint8_t* q, int32_t bits, const float* sx, int64_t M, int64_t K,
@@ -176,7 +192,21 @@ fgq_status fgq_gemm(const uint8_t* q, int32_t bits, const float* sx, int64_t M, 
   fgq_status err;
   if (!conv_geom(1, M, 1, K, O, 1, 1, 1, 1, 0, 0, G, bits, &g, &err)) return err;
   if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
-  return run_layer(q, sx, codes, alpha, prepared, g, y, stream);
+  return run_layer(q, sx, codes, alpha, prepared, g, LayerOut{y, nullptr, nullptr, 0}, stream);
+}
+
+fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx, int64_t M, int64_t K,
+                      const uint8_t* codes, const float* alpha, const void* prepared, int64_t O,
+                      int32_t G, int32_t out_bits, const float* out_scale, uint8_t* q_out,
+                      void* stream) {
+  if (!q || !sx || !codes || !alpha || !out_scale || !q_out) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(1, M, 1, K, O, 1, 1, 1, 1, 0, 0, G, bits, &g, &err)) return err;
+  if (out_bits != 8 && out_bits != 4) return FGQ_ERR_BITS;
+  if (out_bits == 4 && O % 2 != 0) return FGQ_ERR_BITS;
+  if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  return run_layer(q, sx, codes, alpha, prepared, g, LayerOut{nullptr, q_out, out_scale, out_bits}, stream);
 }
 
 fgq_status fgq_group_sums(const uint8_t* q, int32_t bits, int64_t B, int64_t H, int64_t W,

@@ -14,6 +14,7 @@
 // group's codes, accumulated alongside.  Out-of-image taps read q = 0, i.e.
 // q' = -128, so the identity also holds there.
 #include "fgq_internal.h"
+#include "qcode.h"
 
 // Every floating-point expression here is evaluated exactly as written.
 #pragma clang fp contract(off)
@@ -53,11 +54,11 @@ __device__ inline int64_t a_index(const ConvGeom& g, int64_t m, int64_t k) {
 }
 
 // kVec: C % 4 == 0, so four consecutive k share one tap and are contiguous.
-template <int kBits, bool kVec, bool kDot4>
+template <int kBits, bool kVec, bool kDot4, int kOut>
 __global__ __launch_bounds__(256) void exact_conv_kernel(
     const uint8_t* __restrict__ q, const float* __restrict__ sxp,
     const uint8_t* __restrict__ codes, const float* __restrict__ alpha,
-    ConvGeom g, float* __restrict__ y) {
+    ConvGeom g, LayerOut out) {
   __shared__ __attribute__((aligned(16))) int8_t As[kTM * kStride];
   __shared__ __attribute__((aligned(16))) int8_t Ts[kTO * kStride];
   const int tid = threadIdx.x;
@@ -202,16 +203,20 @@ __global__ __launch_bounds__(256) void exact_conv_kernel(
   }
 
   const double sx = static_cast<double>(*sxp);
+  with_out_scale<kOut>(out.scale, [&](const QScale& qs, auto rcp) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int64_t m = m0 + ty + 16 * i;
-    if (m >= g.M) continue;
+    for (int i = 0; i < 4; ++i) {
+      const int64_t m = m0 + ty + 16 * i;
+      if (m >= g.M) continue;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t o = o0 + tx + 16 * j;
-      if (o < g.O) y[m * g.O + o] = static_cast<float>(sx * acc[i][j]);
+      for (int j = 0; j < 4; ++j) {
+        const int64_t o = o0 + tx + 16 * j;  // lanes tx and tx^1 hold channels o and o^1
+        if (o < g.O)
+          emit_out<kOut, decltype(rcp)::value>(out.y, out.q, qs, m * g.O + o, static_cast<int>(o),
+                                               static_cast<float>(sx * acc[i][j]));
+      }
     }
-  }
+  });
 }
 
 // One thread per (row, o, g): P = sum over the group of t * q, exact.
@@ -239,29 +244,39 @@ __global__ __launch_bounds__(256) void group_sums_kernel(
   }
 }
 
-template <int kBits>
-fgq_status launch_exact_bits(const uint8_t* q, const float* sx, const uint8_t* codes,
-                             const float* alpha, const ConvGeom& g, float* y, hipStream_t st) {
+template <int kBits, int kOut>
+fgq_status launch_exact_out(const uint8_t* q, const float* sx, const uint8_t* codes,
+                            const float* alpha, const ConvGeom& g, const LayerOut& y, hipStream_t st) {
   const int64_t gx = ceil_div(g.M, kTM), gy = ceil_div(g.O, kTO);
   if (gx > 0x7fffffffLL || gy > 65535) return FGQ_ERR_SHAPE;
   const dim3 grid(static_cast<uint32_t>(gx), static_cast<uint32_t>(gy));
   const bool vec = (g.C % 4 == 0) && (reinterpret_cast<uintptr_t>(q) % 4 == 0);
   const bool dot4 = g.G % 4 == 0;
   if (vec && dot4)
-    hipLaunchKernelGGL((exact_conv_kernel<kBits, true, true>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
+    hipLaunchKernelGGL((exact_conv_kernel<kBits, true, true, kOut>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
   else if (dot4)
-    hipLaunchKernelGGL((exact_conv_kernel<kBits, false, true>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
+    hipLaunchKernelGGL((exact_conv_kernel<kBits, false, true, kOut>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
   else if (vec)
-    hipLaunchKernelGGL((exact_conv_kernel<kBits, true, false>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
+    hipLaunchKernelGGL((exact_conv_kernel<kBits, true, false, kOut>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
   else
-    hipLaunchKernelGGL((exact_conv_kernel<kBits, false, false>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
+    hipLaunchKernelGGL((exact_conv_kernel<kBits, false, false, kOut>), grid, dim3(256), 0, st, q, sx, codes, alpha, g, y);
   return last_launch();
+}
+
+template <int kBits>
+fgq_status launch_exact_bits(const uint8_t* q, const float* sx, const uint8_t* codes,
+                             const float* alpha, const ConvGeom& g, const LayerOut& y, hipStream_t st) {
+  switch (y.bits) {
+    case 0: return launch_exact_out<kBits, 0>(q, sx, codes, alpha, g, y, st);
+    case 8: return launch_exact_out<kBits, 8>(q, sx, codes, alpha, g, y, st);
+    default: return launch_exact_out<kBits, 4>(q, sx, codes, alpha, g, y, st);
+  }
 }
 
 }  // namespace
 
 fgq_status launch_exact_conv(const uint8_t* q, const float* sx, const uint8_t* codes,
-                             const float* alpha, const ConvGeom& g, float* y, hipStream_t st) {
+                             const float* alpha, const ConvGeom& g, const LayerOut& y, hipStream_t st) {
   return g.bits == 8 ? launch_exact_bits<8>(q, sx, codes, alpha, g, y, st)
                      : launch_exact_bits<4>(q, sx, codes, alpha, g, y, st);
 }

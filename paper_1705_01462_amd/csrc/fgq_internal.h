@@ -22,6 +22,17 @@ struct ConvGeom {
   int32_t R, S, sh, sw, ph, pw, G, bits;
 };
 
+// Where a layer's result goes: fp32 y (bits = 0), or the layer's output
+// fused with the next layer's activation quantization: unsigned `bits` codes
+// of every output value with the device scale *scale, NHWC like y (bits 4:
+// two channels per byte, the even channel in the low nibble; O even).
+struct LayerOut {
+  float* y;
+  uint8_t* q;
+  const float* scale;
+  int32_t bits;
+};
+
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }
 
 inline fgq_status last_launch() {
@@ -70,7 +81,7 @@ fgq_status launch_quantize(const float* x, int64_t n, int32_t bits,
 int32_t quantize_partials(int64_t n);
 fgq_status launch_exact_conv(const uint8_t* q, const float* sx,
                              const uint8_t* codes, const float* alpha,
-                             const ConvGeom& g, float* y, hipStream_t st);
+                             const ConvGeom& g, const LayerOut& out, hipStream_t st);
 fgq_status launch_group_sums(const uint8_t* q, const uint8_t* codes,
                              const ConvGeom& g, int64_t row0, int64_t nrows,
                              int32_t* P, hipStream_t st);
@@ -81,12 +92,12 @@ fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O,
 // check fold_supported first.
 bool fold_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_fold_conv(const uint8_t* q, const float* sx,
-                            const void* prepared, const ConvGeom& g, float* y,
+                            const void* prepared, const ConvGeom& g, const LayerOut& out,
                             hipStream_t st);
 // Per-group int8 MFMA kernel with an fp32 alpha epilogue (G = 64).
 bool group_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_group_conv(const uint8_t* q, const float* sx,
-                             const void* prepared, const ConvGeom& g, float* y,
+                             const void* prepared, const ConvGeom& g, const LayerOut& out,
                              hipStream_t st);
 
 }  // namespace fgq

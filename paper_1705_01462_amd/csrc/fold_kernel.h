@@ -1,0 +1,302 @@
+// fold_kernel.h -- folded-scale FGQ layer on the int8 matrix cores (gfx950):
+// the kernel template and its launch logic.  The output kind is a template
+// parameter (fp32 y, or 8-/4-bit codes of the next layer's activations), and
+// each kind is instantiated in a source file of its own (fold.hip,
+// fold_q8.hip, fold_q4.hip) so that they compile in parallel.
+//
+// With the per-group scales folded into three int8 digit planes (see
+// prepare.hip), the layer is three exact int8 GEMMs sharing one activation
+// operand:
+//   S_j[o][m] = sum_k plane_j[o][k] * q'[m][k],   q' = q ^ 0x80 (uint8) or q (uint4)
+//   y[m][o]   = sum_j (S_j + bias_j[o]) * (s_x * 2^-E_o * 255^j)
+// The integer sums are exact (|S_j| < 2^31 for K < 2^17); the combination
+// is three fp32 conversions and fused multiply-adds per output.
+//
+// Implicit GEMM: row m = (b, ho, wo), k = (r*S + s)*C + c, so a 16-element
+// piece of k (C % 16 == 0) is 16 consecutive channels of one input pixel.
+//
+// Work split.  A 256-thread workgroup owns a tile of output rows x output
+// channels and walks K in steps of 128 (four 32-wide K slices of the
+// v_mfma_i32_32x32x32_i8 instruction, which runs at twice the rate of the
+// 16x16x64 form on gfx950; the prepared K is padded to a multiple of 128
+// with zero weights).  Its four waves are kNWO (channels) x 4/kNWO
+// (rows); each wave owns 32 channels x kNB*32 rows, i.e. kNB 32x32 blocks
+// per digit plane.
+//  * Activations are the 32-row MFMA operand: gathered into LDS once per
+//    workgroup per step (double-buffered, 128-byte rows with the 16-byte
+//    slot XOR-swizzled by (row/2) % 8 so that both the row writes and the
+//    32-row fragment reads hit every bank once per pass) and read by every
+//    wave that shares those rows.
+//  * Weights are the 32-column operand: raw buffer loads straight into
+//    registers (every workgroup reads the same few hundred KB, so they come
+//    from L2).  They are stored in fragment order, so each wave-wide load is
+//    one contiguous kilobyte; a lane's offset is fixed and the K step is the
+//    scalar offset, so the loop spends no vector instructions on them.
+//  * Out-of-image activation pieces are loaded with an offset past the
+//    buffer end, which the hardware returns as zeros (q = 0, then q' = -128
+//    for uint8), so padding needs no select.
+// The accumulators start at the per-plane bias (uint8), and the loads of
+// step ks+1 are interleaved between the matrix instructions of step ks.
+// A lane's 16 accumulators of a block are 16 rows of one channel; for each
+// row the wave stores 32 consecutive channels (128 contiguous bytes).
+// Workgroups are numbered so that consecutive row tiles land on one XCD
+// (shared halos in that XCD's L2).  In-loop index arithmetic is 32-bit and
+// incremental.
+#pragma once
+
+#include "igemm.h"
+#include "epilogue.h"
+#include "qcode.h"
+
+namespace fgq {
+
+struct FoldArgs {
+  ig::ActArgs x;
+  const float* sx;
+  const int8_t* planes;
+  const int32_t* bias;
+  const float* scale;
+  float* y;
+  uint8_t* qo;           // output codes (kOut 8 or 4)
+  const float* oscale;   // their scale
+  int32_t staged;        // epilogue through LDS (epi_staged)
+  int32_t nks, planes_bytes;
+};
+
+// One launcher per output kind: kOut = 0 (fp32 y), 8 or 4 (codes).
+fgq_status launch_fold_out_f32(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_out_q8(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_out_q4(const FoldArgs& a, int bits, hipStream_t st);
+
+namespace {
+
+using namespace ig;
+
+template <int kBits, int kNWO, int kNB, int kCM, int kOut>
+__global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(FoldArgs a) {
+  constexpr int kNWM = 4 / kNWO;
+  constexpr int kTO = 32 * kNWO;
+  constexpr int kTM = kNWM * kNB * 32;
+  using Stager = StagerFor<kBits, kTM, kCM>;
+  constexpr int kXP = Stager::kXP;
+  constexpr int kStage = Stager::kStage;
+  constexpr int kLds = 2 * kStage > EpiTile<kOut, kNWO>::kBytes ? 2 * kStage : EpiTile<kOut, kNWO>::kBytes;
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kLds];
+
+  const int tid = threadIdx.x;
+  const int lane = tid % 64, wave = tid / 64;
+  const int wo = wave % kNWO, wm = wave / kNWO;
+  const int tile = xcd_swizzle(blockIdx.x, a.x.n_otiles * a.x.n_mtiles);
+  const int o0 = (tile % a.x.n_otiles) * kTO + 32 * wo;  // this wave's first channel
+  const int m0 = (tile / a.x.n_otiles) * kTM;             // workgroup's first row
+
+  const __amdgpu_buffer_rsrc_t wrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.planes), 0, a.planes_bytes, kBufFlags);
+
+  // ---- weight fragments: lane supplies channel o0 + lane%32, k-slot
+  // 16*(lane/32) of K half h; the fragment-ordered planes put the wave's
+  // 64 lanes x 16 bytes of (tile, step, plane, half) in one kilobyte.
+  const int wbase = (o0 / 32) * a.nks * static_cast<int>(kFoldTileBytes) + 16 * lane;
+
+  Stager xs;
+  xs.init(a.x, m0, tid);
+
+  // A step covers two 64-wide fragment blocks (K quarters hq = 2*blk + h).
+  // Loads past the last block read zeros or another tile's weights; they
+  // are never used.
+  v4i wring[2][3][4];
+  auto load_w = [&](auto U, int ks) {
+    constexpr int u = decltype(U)::value;
+#pragma unroll
+    for (int blk = 0; blk < 2; ++blk) {
+      const int kso = (2 * ks + blk) * static_cast<int>(kFoldTileBytes);
+#pragma unroll
+      for (int j = 0; j < 3; ++j)
+#pragma unroll
+        for (int h = 0; h < 2; ++h)
+          wring[u][j][2 * blk + h] =
+              __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, kso, 0);
+    }
+  };
+
+  // Accumulators start at the uint8 offset term 128 * sum_k plane_j[o][k]
+  // of the lane's channel, so the epilogue needs no integer additions.
+  v16i acc[3][kNB];
+  {
+    const int oc = o0 + lane % 32;
+#pragma unroll
+    for (int j = 0; j < 3; ++j) {
+      const int bj = (kBits == 8 && oc < a.x.O) ? a.bias[j * a.x.O + oc] : 0;
+      v16i init;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) init[r] = bj;
+#pragma unroll
+      for (int c = 0; c < kNB; ++c) acc[j][c] = init;
+    }
+  }
+
+  // A-operand fragment addresses (row = wave rows + 32c + lane%32, slot
+  // 2*quarter + lane/32)
+  int afrag[kNB][4];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c)
+#pragma unroll
+    for (int h = 0; h < 4; ++h) afrag[c][h] = lds_off(wm * kNB * 32 + 32 * c + lane % 32, 2 * h + lane / 32);
+
+  auto compute = [&](int stage, const v4i (&w)[3][4]) {
+    const unsigned char* base = lds + stage * kStage;
+    if constexpr (kNB <= 2) {
+      // Two workgroups share the compute unit: read each K slice's
+      // fragments just before use (fewer live registers); the other
+      // workgroup's waves cover the LDS latency.
+#pragma unroll
+      for (int h = 0; h < 4; ++h) {
+        v4i xf[kNB];
+#pragma unroll
+        for (int c = 0; c < kNB; ++c) xf[c] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+#pragma unroll
+        for (int c = 0; c < kNB; ++c)
+#pragma unroll
+          for (int j = 0; j < 3; ++j)
+            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], w[j][h], acc[j][c], 0, 0, 0);
+      }
+    } else {
+      v4i xf[kNB][4];
+#pragma unroll
+      for (int c = 0; c < kNB; ++c)
+#pragma unroll
+        for (int h = 0; h < 4; ++h) xf[c][h] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+#pragma unroll
+      for (int h = 0; h < 4; ++h)
+#pragma unroll
+        for (int c = 0; c < kNB; ++c)
+#pragma unroll
+          for (int j = 0; j < 3; ++j)
+            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][h], w[j][h], acc[j][c], 0, 0, 0);
+    }
+  };
+
+  // Step ks: prefetch step ks+1 (weights into ring slot (ks+1)%2,
+  // activations into registers), feed the matrix cores from LDS stage ks%2
+  // and ring slot ks%2, then publish the prefetched activations to the
+  // other LDS stage.  Loads past the last step are clamped (weights) or
+  // read nothing (activations), so the step has no data-dependent branch;
+  // the loop is unrolled by 2 so that ring indices are constants.
+  const int nk = (a.x.K + kKT - 1) / kKT;
+  auto step = [&](auto U, int ks) {
+    constexpr int u = decltype(U)::value;
+    load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
+    xs.advance(a.x);
+    xs.load(a.x);
+    compute(u, wring[u]);
+    // Schedule: every fragment read first (distinct registers, LDS latency
+    // paid once), then the matrix instructions with the prefetch loads and
+    // their address arithmetic slotted between them, so the per-CU load
+    // path works while the matrix cores do.
+    if constexpr (kNB > 2) {
+#pragma unroll
+      for (int i = 0; i < 4 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+#pragma unroll
+      for (int i = 0; i < 12 + kXP; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
+        __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 12 * kNB - 2 * (12 + kXP) > 0 ? 12 * kNB - 2 * (12 + kXP) : 0, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
+    xs.store(lds + (1 - u) * kStage, 0x80808080u);  // q - 128 (padding 0 -> -128)
+    __syncthreads();
+  };
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  load_w(I0{}, 0);
+  xs.load(a.x);
+  xs.store(lds, 0x80808080u);
+  __syncthreads();
+  int ks = 0;
+  for (; ks + 2 <= nk; ks += 2) {
+    step(I0{}, ks);
+    step(I1{}, ks + 1);
+  }
+  if (ks < nk) step(I0{}, ks);
+
+  // ---- epilogue: lane holds rows m of channel o.
+  const int o = o0 + lane % 32;
+  const float sx = *a.sx;
+  const float c0 = o < a.x.O ? sx * a.scale[o] : 0.0f;
+  const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
+  // locals: a byte store may alias anything, including the argument block
+  const OutPtrs out{a.y, a.qo, a.x.M, a.x.O};
+  const bool staged = a.staged != 0;
+  with_out_scale<kOut>(a.oscale, [&](const QScale& qs, auto rcp) {
+    constexpr bool kR = decltype(rcp)::value;
+    auto val = [&](int c, int r) {
+      const float f2 = static_cast<float>(acc[2][c][r]);
+      const float f1 = static_cast<float>(acc[1][c][r]);
+      const float f0 = static_cast<float>(acc[0][c][r]);
+      return fmaf(f2, c2, fmaf(f1, c1, f0 * c0));
+    };
+    if (staged)
+      store_staged<kOut, kNWO, kNB, kR>(lds, out, qs, m0, o0 - 32 * wo, wm, wo, tid, val);
+    else
+      store_direct<kOut, kNB, kR>(out, qs, m0 + wm * kNB * 32, o, lane, val);
+  });
+}
+
+template <int kOut, int kBits, int kNWO, int kNB>
+fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
+  constexpr int kTO = 32 * kNWO, kTM = (4 / kNWO) * kNB * 32;
+  FoldArgs a = a0;
+  a.x.n_otiles = (a.x.O + kTO - 1) / kTO;
+  a.x.n_mtiles = (a.x.M + kTM - 1) / kTM;
+  const int64_t n = static_cast<int64_t>(a.x.n_otiles) * a.x.n_mtiles;
+  if (n > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  const dim3 grid(static_cast<uint32_t>(n));
+  switch (c_mode(a.x.C)) {
+    case 0: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 0, kOut>), grid, dim3(kThreads), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 1, kOut>), grid, dim3(kThreads), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 4, kOut>), grid, dim3(kThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 8, kOut>), grid, dim3(kThreads), 0, st, a); break;
+  }
+  return last_launch();
+}
+
+// Rows per wave (kNB blocks of 32): the busiest compute unit does
+// ceil(tiles / CUs) workgroups of kNB blocks per SIMD; among equal costs
+// the smaller kNB wins (kNB = 2 runs two workgroups per compute unit).
+template <int kOut, int kBits, int kNWO>
+fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
+  constexpr int kNWM = 4 / kNWO;
+  const int64_t otiles = ceil_div(a.x.O, 32 * kNWO);
+  int best = 2;
+  int64_t best_cost = -1;
+  for (int nb = 2; nb <= 4; ++nb) {
+    const int64_t tiles = otiles * ceil_div(a.x.M, kNWM * nb * 32);
+    const int64_t cost = ceil_div(tiles, device_cus()) * nb;
+    if (best_cost < 0 || cost < best_cost) {
+      best_cost = cost;
+      best = nb;
+    }
+  }
+  switch (best) {
+    case 2: return launch_cfg<kOut, kBits, kNWO, 2>(a, st);
+    case 3: return launch_cfg<kOut, kBits, kNWO, 3>(a, st);
+    default: return launch_cfg<kOut, kBits, kNWO, 4>(a, st);
+  }
+}
+
+template <int kOut, int kBits>
+fgq_status launch_bits(const FoldArgs& a, hipStream_t st) {
+  if (a.x.O > 64) return launch_nwo<kOut, kBits, 4>(a, st);
+  if (a.x.O > 32) return launch_nwo<kOut, kBits, 2>(a, st);
+  return launch_nwo<kOut, kBits, 1>(a, st);
+}
+
+template <int kOut>
+fgq_status launch_out(const FoldArgs& a, int bits, hipStream_t st) {
+  return bits == 8 ? launch_bits<kOut, 8>(a, st) : launch_bits<kOut, 4>(a, st);
+}
+
+}  // namespace
+}  // namespace fgq

@@ -1,0 +1,9 @@
+// fold_q8.hip -- the folded-scale layer kernels that emit 8-bit codes of
+// the next layer's activations.
+#include "fold_kernel.h"
+
+namespace fgq {
+
+fgq_status launch_fold_out_q8(const FoldArgs& a, int bits, hipStream_t st) { return launch_out<8>(a, bits, st); }
+
+}  // namespace fgq

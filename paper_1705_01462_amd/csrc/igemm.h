@@ -1,5 +1,5 @@
 // igemm.h -- pieces shared by the matrix-core implicit-GEMM convolution
-// kernels (fold.hip, group.hip).
+// kernels (fold_kernel.h, group_kernel.h).
 //
 // Implicit GEMM: output row m = (b, ho, wo), reduction index
 // k = (r*S + s)*C + c, so a 16-element piece of k (C % 16 == 0) is 16

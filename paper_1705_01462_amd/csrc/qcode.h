@@ -1,0 +1,103 @@
+// qcode.h -- the unsigned activation code of one value (Sec. 4: activations
+// quantized with one scale per tensor), shared by the quantize kernel and
+// the convolution epilogues that emit quantized activations:
+//   code = min(max(rint(v / s), 0), qmax), qmax = 2^bits - 1,
+// with the correctly rounded quotient v / s and rint rounding half to even,
+// so that codes are reproducible bit for bit; NaN maps to 0.
+//
+// The quotient is formed from the correctly rounded reciprocal y = 1/s,
+// taken once per scale: q0 = v*y is within one ulp of v/s, the residual
+// v - q0*s is exact in one fused multiply-add, and q0 + (v - q0*s)*y rounded
+// once is the correctly rounded quotient (Markstein's theorem on a single
+// correction step, valid while s, y and the quotient are normal numbers).
+// q0 is first clamped to +-2^24: a quotient that large saturates the code
+// either way, and the clamp keeps the residual finite when v*y overflows
+// (an infinite v still gives an infinite, hence saturated, quotient).  When
+// s or y is not a normal number, plain division; that choice is uniform
+// over a launch and is made once, outside the loops over values
+// (with_rcp).
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <type_traits>
+
+namespace fgq {
+
+struct QScale {
+  float s, y, qmax;
+  bool rcp;
+};
+
+__device__ inline QScale make_qscale(float s, int bits) {
+#pragma clang fp contract(off)
+  QScale c;
+  c.s = s;
+  c.y = 1.0f / s;
+  c.qmax = bits == 8 ? 255.0f : 15.0f;
+  const float kMinNormal = 1.17549435e-38f;
+  // the same in every lane: made a scalar, so that branches on it are uniform
+  c.rcp = __builtin_amdgcn_readfirstlane(
+              static_cast<int>(s >= kMinNormal && c.y >= kMinNormal && c.y < __builtin_huge_valf())) != 0;
+  return c;
+}
+
+template <bool kRcp>
+__device__ inline unsigned qcode(float v, const QScale& c) {
+#pragma clang fp contract(off)
+  float q;
+  if constexpr (kRcp) {
+    const float q0 = fminf(fmaxf(v * c.y, -16777216.0f), 16777216.0f);
+    q = fmaf(fmaf(-q0, c.s, v), c.y, q0);
+  } else {
+    q = v / c.s;
+  }
+  const float r = fminf(fmaxf(rintf(q), 0.0f), c.qmax);  // NaN -> 0
+  return static_cast<unsigned>(r);
+}
+
+// f(std::true_type{}) when the scale admits the reciprocal form, else
+// f(std::false_type{}); f passes the flag on to qcode / emit_out.
+template <class F>
+__device__ inline void with_rcp(const QScale& c, F&& f) {
+  if (c.rcp)
+    f(std::true_type{});
+  else
+    f(std::false_type{});
+}
+
+// One output value of a layer, at element index e = m*O + o, by output
+// kind: kOut = 0 stores fp32 to y; kOut = 8 stores its code as one byte;
+// kOut = 4 packs two codes per byte (the lanes holding channels o and o^1
+// must call together; the even one writes).  All stores are non-temporal:
+// the output is written once, and streaming it out leaves no dirty lines in
+// the per-XCD L2 caches for the end of the kernel to write back.
+template <int kOut, bool kRcp = true>
+__device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t e, int o, float v) {
+  if constexpr (kOut == 0) {
+    __builtin_nontemporal_store(v, y + e);
+  } else if constexpr (kOut == 8) {
+    __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), q + e);
+  } else {
+    static_assert(kOut == 4, "output kind");
+    const unsigned c = qcode<kRcp>(v, qs);
+    const unsigned other = static_cast<unsigned>(__builtin_amdgcn_mov_dpp(static_cast<int>(c), 0xB1, 0xF, 0xF, false));
+    if ((o & 1) == 0) __builtin_nontemporal_store(static_cast<uint8_t>(c | (other << 4)), q + (e >> 1));
+  }
+}
+
+// The store loop of a layer epilogue, run as f(qs, rcp) with the output
+// kind's scale: for codes, qs is the scale read from `scale` and rcp the
+// reciprocal-form flag as a type (see with_rcp); for fp32 output neither is
+// used.
+template <int kOut, class F>
+__device__ inline void with_out_scale(const float* scale, F&& f) {
+  if constexpr (kOut == 0) {
+    f(QScale{}, std::true_type{});
+  } else {
+    const QScale qs = make_qscale(*scale, kOut);
+    with_rcp(qs, [&](auto rcp) { f(qs, rcp); });
+  }
+}
+
+}  // namespace fgq

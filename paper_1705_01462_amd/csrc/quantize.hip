@@ -11,16 +11,11 @@
 // round trip plus its bytes.  Each pass-2 thread turns 16 (u8) or 32 (u4)
 // values into one 16-byte store.
 //
-// The quotient x/s is the correctly rounded one and rint rounds half to
-// even, so the codes are reproducible bit for bit.  It is not computed with
-// the full division sequence (about ten vector instructions, which made
-// pass 2 compute-bound) but from the correctly rounded reciprocal y = 1/s,
-// taken once: q = x*y is within one ulp of x/s, the residual x - q*s is
-// exact in one fused multiply-add, and q + (x - q*s)*y rounded once is the
-// correctly rounded quotient (Markstein's theorem on a single correction
-// step, valid while s, y and the quotient stay normal).  When s or y is
-// not a normal number the kernel divides the ordinary way.
+// The codes (qcode.h) use the correctly rounded quotient x/s from the
+// reciprocal and one exact correction rather than the full division
+// sequence, which made pass 2 compute-bound.
 #include "fgq_internal.h"
+#include "qcode.h"
 
 // The quotient arithmetic below relies on each operation being rounded as
 // written.
@@ -73,23 +68,6 @@ __global__ __launch_bounds__(kThreads) void absmax_partial_kernel(
   if (threadIdx.x == 0) partials[blockIdx.x] = m;
 }
 
-__device__ inline unsigned qval(float v, float s, float qmax) {
-  float r = rintf(v / s);
-  r = fminf(fmaxf(r, 0.0f), qmax);  // NaN -> 0
-  return static_cast<unsigned>(r);
-}
-
-// qval with x/s from the reciprocal y = RN(1/s) and one exact correction
-// (s, y normal).  An infinite first product (x = inf, or x/s beyond the
-// float range) is already the correctly rounded quotient.
-__device__ inline unsigned qval_rcp(float v, float s, float y, float qmax) {
-  const float q0 = v * y;
-  const float res = fmaf(-q0, s, v);
-  const float q = fabsf(q0) < __builtin_huge_valf() ? fmaf(res, y, q0) : q0;
-  const float r = fminf(fmaxf(rintf(q), 0.0f), qmax);  // NaN -> 0
-  return static_cast<unsigned>(r);
-}
-
 template <int kBits, bool kAligned>
 __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const float* __restrict__ x, int64_t n, const float* __restrict__ scale_in,
@@ -134,45 +112,48 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
   if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = s;
 
   // 3. quantize and store
-  const float y = 1.0f / s;
-  const float kMinNormal = 1.17549435e-38f;
-  const bool rcp = s >= kMinNormal && y >= kMinNormal && y < __builtin_huge_valf();
-  auto code = [&](float val) { return rcp ? qval_rcp(val, s, y, qmax) : qval(val, s, qmax); };
-  if (have) {
-    uint32_t out[kBytes / 4];
+  const QScale qs = make_qscale(s, kBits);
+  with_rcp(qs, [&](auto rcp) {
+    auto code = [&](float val) { return qcode<decltype(rcp)::value>(val, qs); };
+    if (have) {
+      uint32_t out[kBytes / 4];
 #pragma unroll
-    for (int wd = 0; wd < kBytes / 4; ++wd) {
-      uint32_t word = 0;
-      if (kBits == 8) {
+      for (int wd = 0; wd < kBytes / 4; ++wd) {
+        uint32_t word = 0;
+        if (kBits == 8) {
 #pragma unroll
-        for (int b = 0; b < 4; ++b) word |= code(v[4 * wd + b]) << (8 * b);
+          for (int b = 0; b < 4; ++b) word |= code(v[4 * wd + b]) << (8 * b);
+        } else {
+#pragma unroll
+          for (int b = 0; b < 8; ++b) word |= code(v[8 * wd + b]) << (4 * b);
+        }
+        out[wd] = word;
+      }
+      uint8_t* dst = q + ch * kBytes;
+      if (kAligned) {
+#pragma unroll
+        for (int i = 0; i < kBytes / 16; ++i) {
+          typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+          const u32x4 w = {out[4 * i], out[4 * i + 1], out[4 * i + 2], out[4 * i + 3]};
+          __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(dst) + i);
+        }
       } else {
 #pragma unroll
-        for (int b = 0; b < 8; ++b) word |= code(v[8 * wd + b]) << (4 * b);
+        for (int i = 0; i < kBytes; ++i) dst[i] = static_cast<uint8_t>(out[i / 4] >> (8 * (i % 4)));
       }
-      out[wd] = word;
     }
-    uint8_t* dst = q + ch * kBytes;
-    if (kAligned) {
-#pragma unroll
-      for (int i = 0; i < kBytes / 16; ++i)
-        reinterpret_cast<uint4*>(dst)[i] = make_uint4(out[4 * i], out[4 * i + 1], out[4 * i + 2], out[4 * i + 3]);
-    } else {
-#pragma unroll
-      for (int i = 0; i < kBytes; ++i) dst[i] = static_cast<uint8_t>(out[i / 4] >> (8 * (i % 4)));
+    // 4. the tail (fewer than kPer values), one byte per thread of the grid
+    const int64_t done = nchunks * kPer;
+    const int64_t tail_bytes = kBits == 8 ? (n - done) : (n - done) / 2;
+    if (ch < tail_bytes) {
+      if (kBits == 8) {
+        q[done + ch] = static_cast<uint8_t>(code(x[done + ch]));
+      } else {
+        const int64_t e = done + 2 * ch;
+        q[e / 2] = static_cast<uint8_t>(code(x[e]) | (code(x[e + 1]) << 4));
+      }
     }
-  }
-  // 4. the tail (fewer than kPer values), one byte per thread of the grid
-  const int64_t done = nchunks * kPer;
-  const int64_t tail_bytes = kBits == 8 ? (n - done) : (n - done) / 2;
-  if (ch < tail_bytes) {
-    if (kBits == 8) {
-      q[done + ch] = static_cast<uint8_t>(code(x[done + ch]));
-    } else {
-      const int64_t e = done + 2 * ch;
-      q[e / 2] = static_cast<uint8_t>(code(x[e]) | (code(x[e + 1]) << 4));
-    }
-  }
+  });
 }
 
 int64_t pass2_blocks(int64_t n, int32_t bits) {

@@ -78,6 +78,17 @@ def test_quantize_validation():
 
 
 @no_device
+def test_fused_layer_validation():
+    L = fgq.lib()
+    args = lambda O, ob, sc, qo: (P, 8, P, 2, 8, 8, 16, P, P, None, O, 3, 3, 1, 1, 1, 1, 4, ob, sc, qo, None)
+    assert L.fgq_conv2d_q(*args(16, 7, P, P)) == 4          # FGQ_ERR_BITS: out_bits
+    assert L.fgq_conv2d_q(*args(15, 4, P, P)) == 4          # 4-bit output needs even O
+    assert L.fgq_conv2d_q(*args(16, 8, None, P)) == 1       # FGQ_ERR_NULL: scale
+    assert L.fgq_conv2d_q(*args(16, 8, P, None)) == 1       # FGQ_ERR_NULL: q_out
+    assert L.fgq_gemm_q(P, 8, P, 4, 16, P, P, None, 15, 4, 4, P, P, None) == 4
+
+
+@no_device
 def test_layer_validation():
     L = fgq.lib()
     conv = L.fgq_conv2d

@@ -8,6 +8,11 @@ own shape rather than chained, so that each comparison starts from the
 same bytes on both sides (a chained run would have to feed the oracle the
 GPU's own quantized input anyway).  conv1 has its 3 input channels padded to
 4 and uses groups of 4 in both stacks, since 64 does not divide 4.
+
+Each layer also runs with the next layer's quantization fused
+(fgq_conv2d_q, codes of the stack's activation width), which must equal its
+fp32 output quantized by fgq_quantize_act with the same scale, bit for bit,
+over the whole output.
 """
 import numpy as np
 import pytest
@@ -82,3 +87,11 @@ def test_stack_layer_sampled_rows(depth, G, bits, L):
         assert not bad.any(), (f"rows [{row0}, {row0 + n}): {bad.sum()} outputs beyond 1e-5 of the "
                                f"summand magnitude, worst {np.max(err / np.maximum(mag, 1e-300)):.3e}")
         assert np.linalg.norm(err) <= TOL * np.linalg.norm(y_ref.astype(np.float64)) + 1e-30
+
+    # the fused next-layer quantization, whole output, bit for bit
+    y_dev = y.reshape(-1)
+    s_out = torch.tensor([0.9 * float(y_dev.max()) / (2 ** bits - 1)], dtype=torch.float32, device="cuda")
+    q_fused = fgq.fgq_conv2d_q(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, bits, s_out,
+                               prepared=prep)
+    q_two, _ = fgq.fgq_quantize_act(y_dev, bits, scale_in=s_out)
+    assert torch.equal(q_fused.reshape(-1), q_two), "fused quantization differs from conv + quantize"
