@@ -98,15 +98,18 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   // 64 lanes x 16 bytes of (tile, step, plane, half) in one kilobyte.
   const int wbase = (o0 / 32) * a.nks * static_cast<int>(kFoldTileBytes) + 16 * lane;
 
+  const int nk = (a.x.K + kKT - 1) / kKT;
   Stager xs;
   xs.init(a.x, m0, tid);
 
   // A step covers two 64-wide fragment blocks (K quarters hq = 2*blk + h).
-  // Loads past the last block read zeros or another tile's weights; they
-  // are never used.
+  // The step is the scalar offset, which the buffer range check does not
+  // cover, so a step past the last is clamped to the last one (those loads
+  // are never used).
   v4i wring[2][3][4];
   auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
+    ks = ks < nk ? ks : nk - 1;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       const int kso = (2 * ks + blk) * static_cast<int>(kFoldTileBytes);
@@ -179,30 +182,34 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   // Step ks: prefetch step ks+1 (weights into ring slot (ks+1)%2,
   // activations into registers), feed the matrix cores from LDS stage ks%2
   // and ring slot ks%2, then publish the prefetched activations to the
-  // other LDS stage.  Loads past the last step are clamped (weights) or
-  // read nothing (activations), so the step has no data-dependent branch;
-  // the loop is unrolled by 2 so that ring indices are constants.
-  const int nk = (a.x.K + kKT - 1) / kKT;
+  // other LDS stage.  After the last step the prefetch repeats the last
+  // step's weights (clamped) or reads nothing (activations), so the step has
+  // no data-dependent branch; the loop is unrolled by 2 so that ring indices
+  // are constants.
   auto step = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
-    load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
+    // Activation loads first: the publish at the end of the step waits for
+    // them, and the memory counter is in order, so weight loads issued
+    // before them would be waited for too.
     xs.advance(a.x);
     xs.load(a.x);
+    __builtin_amdgcn_sched_barrier(0);
+    load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
     compute(u, wring[u]);
     // Schedule: every fragment read first (distinct registers, LDS latency
-    // paid once), then the matrix instructions with the prefetch loads and
-    // their address arithmetic slotted between them, so the per-CU load
-    // path works while the matrix cores do.
+    // paid once), then the matrix instructions with the weight prefetch
+    // loads and their address arithmetic slotted between them, so the per-CU
+    // load path works while the matrix cores do.
     if constexpr (kNB > 2) {
 #pragma unroll
       for (int i = 0; i < 4 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-      for (int i = 0; i < 12 + kXP; ++i) {
+      for (int i = 0; i < 12; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 12 * kNB - 2 * (12 + kXP) > 0 ? 12 * kNB - 2 * (12 + kXP) : 0, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 12 * kNB - 24, 0);
     }
     __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
     xs.store(lds + (1 - u) * kStage, 0x80808080u);  // q - 128 (padding 0 -> -128)

@@ -82,15 +82,18 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
   const int wbase = (o0 / 32) * a.nks * kBlkBytes + 16 * lane;
   const int abase = 4 * (o0 + lane % 32);
 
+  const int nk = (a.x.K + kKT - 1) / kKT;
   Stager xs;
   xs.init(a.x, m0, tid);
 
-  // Weights and scales of one step (two groups): loads past the last group
-  // read zeros or another tile's weights and are never used.
+  // Weights and scales of one step (two groups).  The step is the scalar
+  // offset, which the buffer range check does not cover, so a step past the
+  // last is clamped to the last one (those loads are never used).
   v4i wring[2][2][2];
   float aring[2][2];
   auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
+    ks = ks < nk ? ks : nk - 1;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
       const int g = 2 * ks + blk;
@@ -146,13 +149,16 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
 
   // Step ks: prefetch step ks+1, feed the matrix cores from LDS stage ks%2,
   // then publish the prefetched activations to the other stage.
-  const int nk = (a.x.K + kKT - 1) / kKT;
   constexpr uint32_t kMask = 0x7F7F7F7Fu;  // q -> 127 - q
   auto step = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
-    load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
+    // Activation loads first: the publish at the end of the step waits for
+    // them, and the memory counter is in order, so weight loads issued
+    // before them would be waited for too.
     xs.advance(a.x);
     xs.load(a.x);
+    __builtin_amdgcn_sched_barrier(0);
+    load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
     compute(u, wring[u], aring[u]);
     __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
     xs.store(lds + (1 - u) * kStage, kMask);
