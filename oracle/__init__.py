@@ -44,9 +44,16 @@ def lib():
                                  _c_i64, _c_i64, _c_i32, _c_p]
         L.orc_gemm.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i32,
                                _c_i32, _c_p]
+        L.orc_dfp_alpha.argtypes = [_c_p, _c_i64, _c_i32, _c_p, _c_p]
+        L.orc_conv2d_dfp.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_i64, _c_i64, _c_p, _c_p,
+                                     _c_i32, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32,
+                                     _c_i32, _c_i64, _c_i64, _c_i32, _c_p]
+        L.orc_gemm_dfp.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_p, _c_p, _c_i32, _c_i64,
+                                   _c_i32, _c_i32, _c_p]
         L.orc_max_threads.argtypes = []
         for f in ("orc_ternarize_group", "orc_ternarize", "orc_quantize_act",
-                  "orc_group_sums_conv", "orc_conv2d", "orc_gemm", "orc_max_threads"):
+                  "orc_group_sums_conv", "orc_conv2d", "orc_gemm", "orc_dfp_alpha",
+                  "orc_conv2d_dfp", "orc_gemm_dfp", "orc_max_threads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -167,6 +174,41 @@ def gemm(q, bits, sx, M, K, codes, alpha, O, G, nthreads=0):
     alpha = np.ascontiguousarray(alpha, dtype=np.float32)
     _check(lib().orc_gemm(_ptr(q), bits, float(sx), M, K, _ptr(codes), _ptr(alpha), O, G,
                           nthreads, _ptr(y)))
+    return y
+
+
+def dfp_alpha(alpha, bits):
+    """Sec. 4 fixed-point group scales: returns (A int8, same shape as alpha; fl)."""
+    alpha = np.ascontiguousarray(alpha, dtype=np.float32)
+    A = np.zeros(alpha.shape, np.int8)
+    fl = np.zeros(1, np.int32)
+    _check(lib().orc_dfp_alpha(_ptr(alpha), alpha.size, bits, _ptr(A), _ptr(fl)))
+    return A, int(fl[0])
+
+
+def conv2d_dfp(q, bits, sx, shape, codes, A, fl, O, R, S, stride, pad, G, rows=None, nthreads=0):
+    """fp32 output [B*Ho*Wo][O] of the fixed-point-scale layer; rows as in conv2d."""
+    B, H, W, C = shape
+    Ho, Wo = conv_out_hw(H, W, R, S, stride, pad)
+    M = B * Ho * Wo
+    y = np.full((M, O), np.nan, np.float32)
+    row0, nrows = (0, -1) if rows is None else rows
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    A = np.ascontiguousarray(A, dtype=np.int8)
+    _check(lib().orc_conv2d_dfp(_ptr(q), bits, float(sx), B, H, W, C, _ptr(codes), _ptr(A), fl, O,
+                                R, S, stride[0], stride[1], pad[0], pad[1], G, row0, nrows,
+                                nthreads, _ptr(y)))
+    return y
+
+
+def gemm_dfp(q, bits, sx, M, K, codes, A, fl, O, G, nthreads=0):
+    y = np.zeros((M, O), np.float32)
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    A = np.ascontiguousarray(A, dtype=np.int8)
+    _check(lib().orc_gemm_dfp(_ptr(q), bits, float(sx), M, K, _ptr(codes), _ptr(A), fl, O, G,
+                              nthreads, _ptr(y)))
     return y
 
 

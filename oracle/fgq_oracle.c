@@ -364,4 +364,102 @@ int orc_gemm(const uint8_t* q, int32_t bits, float sx, int64_t M, int64_t K,
   return ORC_OK;
 }
 
+/* ------------------------------------------------------------------------ */
+/* Fixed-point group scales (Sec. 4)                                          */
+/* ------------------------------------------------------------------------ */
+
+int orc_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A,
+                  int32_t* fl) {
+  if (!alpha || !A || !fl) return ORC_ERR_NULL;
+  if (bits != 8 && bits != 4) return ORC_ERR_BITS;
+  if (n < 0) return ORC_ERR_SHAPE;
+  double amax = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (!isfinite(alpha[i]) || alpha[i] < 0.0f) return ORC_ERR_NONFINITE;
+    if (alpha[i] > amax) amax = alpha[i];
+  }
+  int32_t f = 0;
+  if (amax > 0.0) {
+    /* amax = m 2^e with m in [0.5, 1): log2(amax) lies in [e-1, e), and
+     * equals e-1 only when m = 0.5 */
+    int e;
+    double m = frexp(amax, &e);
+    int ceil_log2 = (m == 0.5) ? e - 1 : e;
+    f = bits - (ceil_log2 + 1);
+  }
+  const double amax_code = (double)((1 << (bits - 1)) - 1);
+  for (int64_t i = 0; i < n; ++i) {
+    double v = amax > 0.0 ? nearbyint(ldexp((double)alpha[i], f)) : 0.0;
+    if (v > amax_code) v = amax_code;
+    A[i] = (int8_t)v;
+  }
+  *fl = f;
+  return ORC_OK;
+}
+
+int orc_conv2d_dfp(const uint8_t* q, int32_t bits, float sx, int64_t B,
+                   int64_t H, int64_t W, int64_t C, const uint8_t* codes,
+                   const int8_t* A, int32_t fl, int64_t O, int32_t R,
+                   int32_t S, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
+                   int32_t G, int64_t row0, int64_t nrows, int32_t nthreads,
+                   float* y) {
+  if (!q || !codes || !A || !y) return ORC_ERR_NULL;
+  if (bits != 8 && bits != 4) return ORC_ERR_BITS;
+  geom_t g;
+  int rc = conv_geom(B, H, W, C, O, R, S, sh, sw, ph, pw, &g);
+  if (rc) return rc;
+  if (G < 1 || C % G != 0) return ORC_ERR_GROUP;
+  const int64_t M = g.B * g.Ho * g.Wo;
+  if (nrows < 0) {
+    row0 = 0;
+    nrows = M;
+  }
+  if (row0 < 0 || row0 + nrows > M) return ORC_ERR_SHAPE;
+  const int64_t K = g.K, ng = K / G;
+  int8_t* t = (int8_t*)malloc((size_t)(O * K));
+  if (!t) return ORC_ERR_SHAPE;
+  orc_unpack_codes(codes, O, K, t);
+  const double scale = (double)sx * ldexp(1.0, -fl);
+  const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 16) num_threads(nt)
+  for (int64_t m = row0; m < row0 + nrows; ++m) {
+    for (int64_t o = 0; o < O; ++o) {
+      int64_t acc = 0;
+      for (int64_t k = 0; k < K; ++k)
+        acc += (int64_t)A[o * ng + k / G] * (int64_t)t[o * K + k] *
+               (int64_t)conv_a(q, bits, &g, m, k);
+      y[m * O + o] = (float)((double)acc * scale);
+    }
+  }
+  free(t);
+  return ORC_OK;
+}
+
+int orc_gemm_dfp(const uint8_t* q, int32_t bits, float sx, int64_t M,
+                 int64_t K, const uint8_t* codes, const int8_t* A, int32_t fl,
+                 int64_t O, int32_t G, int32_t nthreads, float* y) {
+  if (!q || !codes || !A || !y) return ORC_ERR_NULL;
+  if (bits != 8 && bits != 4) return ORC_ERR_BITS;
+  if (M < 1 || K < 1 || O < 1) return ORC_ERR_SHAPE;
+  if (G < 1 || K % G != 0) return ORC_ERR_GROUP;
+  const int64_t ng = K / G;
+  int8_t* t = (int8_t*)malloc((size_t)(O * K));
+  if (!t) return ORC_ERR_SHAPE;
+  orc_unpack_codes(codes, O, K, t);
+  const double scale = (double)sx * ldexp(1.0, -fl);
+  const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 16) num_threads(nt)
+  for (int64_t m = 0; m < M; ++m) {
+    for (int64_t o = 0; o < O; ++o) {
+      int64_t acc = 0;
+      for (int64_t k = 0; k < K; ++k)
+        acc += (int64_t)A[o * ng + k / G] * (int64_t)t[o * K + k] *
+               (int64_t)act_at(q, bits, m * K + k);
+      y[m * O + o] = (float)((double)acc * scale);
+    }
+  }
+  free(t);
+  return ORC_OK;
+}
+
 int orc_max_threads(void) { return omp_get_max_threads(); }

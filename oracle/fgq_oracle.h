@@ -23,6 +23,11 @@
  *   orc_conv2d        y = s_x * sum_g alpha_g * P_g for an implicit-GEMM conv
  *   orc_gemm          (Sec. 3.1 Eq. (2) applied to a layer; one multiply per
  *                     group, Sec. 4 Discussion).
+ *   orc_dfp_alpha     the group scales quantized to an 8- or 4-bit dynamic
+ *                     fixed point with one exponent per layer (Sec. 4,
+ *                     experimental setup).
+ *   orc_conv2d_dfp    the layer with those scales: an exact integer sum of
+ *   orc_gemm_dfp      (A_g t_k) q_k and one scaling by s_x 2^-fl (Sec. 4).
  *
  * Parity status: ternarize, quantize, group sums, conv2d and gemm are pinned
  * by the tests (brute-force enumeration, Lemma 1 statistics, closed forms,
@@ -33,7 +38,8 @@
  *   codes     2-bit, reduction index k = (r*S + s)*C + c, row o holds
  *             ceil(K/4) bytes; element k sits in bits [2(k%4), 2(k%4)+1] of
  *             byte k/4; 00 -> 0, 01 -> +1, 11 -> -1 (10 never written)
- *   alpha     fp32 [O][K/G], group g = k / G
+ *   alpha     fp32 [O][K/G], group g = k / G (fixed point: int8 A [O][K/G]
+ *             and one fractional length fl per layer)
  *   acts      NHWC, u8 one per byte or u4 two per byte (even element in the
  *             low nibble)
  *   output    fp32 NHWC [B][Ho][Wo][O] (GEMM: [M][O])
@@ -98,6 +104,30 @@ int orc_conv2d(const uint8_t* q, int32_t bits, float sx, int64_t B, int64_t H,
 int orc_gemm(const uint8_t* q, int32_t bits, float sx, int64_t M, int64_t K,
              const uint8_t* codes, const float* alpha, int64_t O, int32_t G,
              int32_t nthreads, float* y);
+
+/* Sec. 4: alpha[0..n) quantized to a `bits`-bit (8|4) signed dynamic fixed
+ * point with one fractional length for the whole layer.  With amax the
+ * largest alpha: integer length il = ceil(log2 amax) + 1, fl = bits - il,
+ * A[i] = clamp(rint(alpha[i] * 2^fl), 0, 2^(bits-1) - 1), so the quantized
+ * scale is A * 2^-fl.  amax = 0: fl = 0 and every A is 0.
+ * ORC_ERR_NONFINITE for NaN, Inf or a negative alpha. */
+int orc_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A,
+                  int32_t* fl);
+
+/* y[m][o] = fp32( double(S) * (double(s_x) * 2^-fl) ) with the exact
+ * integer S = sum_k A[o][k/G] * t[o][k] * a[m][k]; rows as in orc_conv2d.
+ * (For |S| < 2^29 the double product is exact, so y is the correctly
+ * rounded value of s_x * 2^-fl * S.) */
+int orc_conv2d_dfp(const uint8_t* q, int32_t bits, float sx, int64_t B,
+                   int64_t H, int64_t W, int64_t C, const uint8_t* codes,
+                   const int8_t* A, int32_t fl, int64_t O, int32_t R,
+                   int32_t S, int32_t sh, int32_t sw, int32_t ph, int32_t pw,
+                   int32_t G, int64_t row0, int64_t nrows, int32_t nthreads,
+                   float* y);
+
+int orc_gemm_dfp(const uint8_t* q, int32_t bits, float sx, int64_t M,
+                 int64_t K, const uint8_t* codes, const int8_t* A, int32_t fl,
+                 int64_t O, int32_t G, int32_t nthreads, float* y);
 
 int orc_max_threads(void);
 
