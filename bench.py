@@ -63,12 +63,12 @@ def layer_dims(L):
     return M, K, Ho, Wo
 
 
-def algorithmic_bytes(L, G, bits, out_bits=32):
-    """Activations in + 2-bit codes + fp32 alpha + output (fp32, or the next
-    layer's 8-/4-bit codes), per launch."""
+def algorithmic_bytes(L, G, bits, out_bits=32, alpha_bytes=4):
+    """Activations in + 2-bit codes + alpha (fp32, or one byte as a fixed-point
+    code) + output (fp32, or the next layer's 8-/4-bit codes), per launch."""
     M, K, _, _ = layer_dims(L)
     act = L["B"] * L["H"] * L["W"] * L["C"] * bits // 8
-    return act + L["O"] * K // 4 + 4 * L["O"] * K // G + M * L["O"] * out_bits // 8
+    return act + L["O"] * K // 4 + alpha_bytes * L["O"] * K // G + M * L["O"] * out_bits // 8
 
 
 class Setup:
@@ -81,6 +81,8 @@ class Setup:
         w = fi.he_weights(L["O"], L["C"], L["R"], L["S"], "bench", G)
         self.codes, self.alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
         self.prep = fgq.fgq_prepare_weights(self.codes, self.alpha, L["O"], K, G) if folded else None
+        # the same layer with 8-bit fixed-point group scales
+        self.prep_dfp = fgq.fgq_prepare_weights_dfp(self.codes, self.alpha, L["O"], K, G, 8)
         n = L["B"] * L["H"] * L["W"] * L["C"]
         base = [torch.from_numpy(fi.relu_gauss((n,), "bench-x", i)).cuda() for i in range(4)]
         wsb = fgq.fgq_quantize_ws_bytes(n)
@@ -107,6 +109,12 @@ class Setup:
     def quantize(self, i):
         x, q, sx, ws, y = self.sets[i]
         self.fgq.fgq_quantize_act(x, self.bits, q=q, scale_out=sx, ws=ws)
+
+    def conv_dfp(self, i):
+        x, q, sx, ws, y = self.sets[i]
+        L = self.L
+        self.fgq.fgq_conv2d_dfp(q, self.bits, sx, self.shape, self.codes, self.prep_dfp, L["O"], L["R"],
+                                L["S"], L["stride"], L["pad"], self.G, out=y)
 
     def conv(self, i):
         x, q, sx, ws, y = self.sets[i]
@@ -192,7 +200,13 @@ def measure(torch, st, steps, warmup, conv_reps=20):
         raise RuntimeError("fused graph replay differs from eager execution")
     _, fused_ms = time_graphs(torch, [(fused_g, conv_reps)])
     fused_us = fused_ms * 1e3 / (conv_reps * nsets)
-    return dict(wall_ms=wall_ms, gpu_ms=gpu_ms, conv_us=conv_us, quant_us=quant_us, conv_fused_us=fused_us)
+    # the layer with 8-bit fixed-point scales
+    dfp_g = st.graph(st.conv_dfp, nsets)
+    dfp_g.replay()
+    _, dfp_ms = time_graphs(torch, [(dfp_g, conv_reps)])
+    dfp_us = dfp_ms * 1e3 / (conv_reps * nsets)
+    return dict(wall_ms=wall_ms, gpu_ms=gpu_ms, conv_us=conv_us, quant_us=quant_us, conv_fused_us=fused_us,
+                conv_dfp_us=dfp_us)
 
 
 def cpu_baseline(fi, L, G, bits, budget_s=15.0):
@@ -252,9 +266,12 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
     groups of 4.  Effective ops use the unpadded conv1 reduction (147).
     Each layer is also timed with the next layer's quantization fused
     (fgq_conv2d_q, `bits`-bit codes, static scale from one fp32 output): a
-    chain of such layers needs one fgq_quantize_act, for the network input."""
+    chain of such layers needs one fgq_quantize_act, for the network input.
+    Finally each layer runs as the paper's own pipeline (Sec. 4): 8-bit
+    fixed-point group scales (fgq_conv2d_dfp) with the fused output codes."""
     layers = []
-    tot = dict(conv_us=0.0, quant_us=0.0, fused_us=0.0, ops=0.0, roof_us=0.0, bytes=0.0, first_quant_us=0.0)
+    tot = dict(conv_us=0.0, quant_us=0.0, fused_us=0.0, dfp_us=0.0, ops=0.0, roof_us=0.0, bytes=0.0,
+               first_quant_us=0.0)
     gen = torch.Generator(device="cuda")
     for li, (L, count) in enumerate(stack_layers(fi, depth, batch)):
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
@@ -266,6 +283,7 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
         codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), g)
         K = R * S * C
         prep = fgq.fgq_prepare_weights(codes, alpha, O, K, g)
+        prep_dfp = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, g, 8)
         n = B * H * W * C
         Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
         M = B * Ho * Wo
@@ -296,6 +314,11 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
             fgq.fgq_conv2d_q(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, bits, out_scale,
                              prepared=prep, q_out=q_outs[i])
 
+        def conv_dfp_q(i):
+            x, q, sx, ws, y = sets[i]
+            fgq.fgq_conv2d_dfp(q, bits, sx, (B, H, W, C), codes, prep_dfp, O, R, S, st, pd, g, bits, out_scale,
+                               out=q_outs[i])
+
         def graph(fn):
             gr = torch.cuda.CUDAGraph()
             with torch.cuda.graph(gr):
@@ -309,31 +332,37 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
         out_scale.fill_(float(sets[0][4].max()) / (2 ** bits - 1))
         for i in range(nsets):
             conv_q(i)
+            conv_dfp_q(i)
         torch.cuda.synchronize()
-        gq, gc, gf = graph(quant), graph(conv), graph(conv_q)
+        gq, gc, gf, gd = graph(quant), graph(conv), graph(conv_q), graph(conv_dfp_q)
         gq.replay()
         gc.replay()
         gf.replay()
+        gd.replay()
         _, q_ms = time_graphs(torch, [(gq, reps)])
         _, c_ms = time_graphs(torch, [(gc, reps)])
         _, f_ms = time_graphs(torch, [(gf, reps)])
+        _, d_ms = time_graphs(torch, [(gd, reps)])
         conv_us = c_ms * 1e3 / (reps * nsets)
         quant_us = q_ms * 1e3 / (reps * nsets)
         fused_us = f_ms * 1e3 / (reps * nsets)
+        dfp_us = d_ms * 1e3 / (reps * nsets)
         k_true = R * S * (3 if L["name"] == "conv1" else C)
         ops = 2.0 * M * O * k_true
         nbytes = n * bits // 8 + O * K // 4 + 4 * O * K // g + 4 * M * O
         roof_us = max(ops / (INT8_PEAK_TOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
-        layers.append([L["name"], count, round(conv_us, 2), round(roof_us / conv_us, 3), round(fused_us, 2)])
+        layers.append([L["name"], count, round(conv_us, 2), round(roof_us / conv_us, 3), round(fused_us, 2),
+                       round(dfp_us, 2)])
         tot["conv_us"] += count * conv_us
         tot["quant_us"] += count * quant_us
         tot["fused_us"] += count * fused_us
+        tot["dfp_us"] += count * dfp_us
         if li == 0:
             tot["first_quant_us"] = quant_us
         tot["ops"] += count * ops
         tot["roof_us"] += count * roof_us
         tot["bytes"] += count * nbytes
-        del sets, q_outs, gq, gc, gf, prep, codes, alpha
+        del sets, q_outs, gq, gc, gf, gd, prep, prep_dfp, codes, alpha
         torch.cuda.empty_cache()
     return {"workload": f"ResNet-{depth} conv stack, batch {batch}, G={G}, u{bits} (conv1 at G=4)",
             "layers_total": sum(c for _, c in stack_layers(fi, depth, batch)), "distinct": len(layers),
@@ -342,10 +371,13 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
             "effective_tops_with_quantize": round(tot["ops"] / ((tot["conv_us"] + tot["quant_us"]) * 1e-6) / 1e12, 1),
             "sum_conv_fused_us": round(tot["fused_us"], 1),
             "effective_tops_fused_chain": round(tot["ops"] / ((tot["fused_us"] + tot["first_quant_us"]) * 1e-6) / 1e12, 1),
+            "sum_conv_dfp_fused_us": round(tot["dfp_us"], 1),
+            "effective_tops_dfp_fused_chain": round(tot["ops"] / ((tot["dfp_us"] + tot["first_quant_us"]) * 1e-6) / 1e12, 1),
             "sum_roofline_us": round(tot["roof_us"], 1),
             "roofline_frac": round(tot["roof_us"] / tot["conv_us"], 4),
             "algorithmic_bytes": int(tot["bytes"]),
-            "per_layer_columns": ["layer", "count", "conv_us", "roofline_frac", "conv_fused_us"],
+            "per_layer_columns": ["layer", "count", "conv_us", "roofline_frac", "conv_fused_us",
+                                  "conv_dfp8_fused_us"],
             "per_layer": layers}
 
 
@@ -409,11 +441,11 @@ def measured_traffic(L, G):
     return int(e["fetch_bytes"] + e["write_bytes"])
 
 
-def roofline(L, G, bits, conv_us, out_bits=32):
+def roofline(L, G, bits, conv_us, out_bits=32, kernel=None, alpha_bytes=4):
     M, K, _, _ = layer_dims(L)
-    nbytes = algorithmic_bytes(L, G, bits, out_bits)
-    kernel = "fgq_conv2d" if out_bits == 32 else "fgq_conv2d_q"
-    traffic = measured_traffic(L, G) if out_bits == 32 else None
+    nbytes = algorithmic_bytes(L, G, bits, out_bits, alpha_bytes)
+    kernel = kernel or ("fgq_conv2d" if out_bits == 32 else "fgq_conv2d_q")
+    traffic = measured_traffic(L, G) if kernel == "fgq_conv2d" else None
     ops = 2.0 * M * L["O"] * K
     t_hbm = nbytes / (HBM_PEAK_GBS * 1e9)
     t_mfma = ops / (INT8_PEAK_TOPS * 1e12)
@@ -427,6 +459,14 @@ def roofline(L, G, bits, conv_us, out_bits=32):
     return {"bound": "mfma", "achieved": round(achieved, 1), "peak": INT8_PEAK_TOPS, "unit": "TFLOP/s",
             "frac": round(achieved / INT8_PEAK_TOPS, 4), "traffic": traffic,
             "kernel": kernel, "kernel_us": round(conv_us, 3), "algorithmic_ops": ops}
+
+
+def dfp_entry(L, G, bits, r, ops):
+    """fgq_conv2d_dfp: the same layer with 8-bit fixed-point group scales
+    (one exponent per layer; one int8 matrix pass, exact integer result)."""
+    return {"kernel": "fgq_conv2d_dfp", "alpha_bits": 8, "conv_us": round(r["conv_dfp_us"], 3),
+            "conv_only_tops": round(ops / (r["conv_dfp_us"] * 1e-6) / 1e12, 1),
+            "roofline": roofline(L, G, bits, r["conv_dfp_us"], kernel="fgq_conv2d_dfp", alpha_bytes=1)}
 
 
 def fused_entry(L, G, bits, r, ops):
@@ -547,20 +587,23 @@ def main():
                         "gpu_ms_per_step": round(r4["gpu_ms"] / args.steps, 5),
                         "conv_only_tops": round(ops / (r4["conv_us"] * 1e-6) / 1e12, 1)},
         "fused": fused_entry(LAYER, 4, bits, r4, ops),
+        "dfp": dfp_entry(LAYER, 4, bits, r4, ops),
         "g64": {"workload": "same layer, G=64", "steps": steps64,
                 "value": round(ops / (r64["wall_ms"] / steps64 * 1e-3) / 1e12, 2),
                 "ms_per_step": round(r64["wall_ms"] / steps64, 5),
                 "conv_us": round(r64["conv_us"], 3),
                 "conv_only_tops": round(ops / (r64["conv_us"] * 1e-6) / 1e12, 1),
                 "roofline": roofline(LAYER, 64, bits, r64["conv_us"]),
-                "fused": fused_entry(LAYER, 64, bits, r64, ops)},
+                "fused": fused_entry(LAYER, 64, bits, r64, ops),
+                "dfp": dfp_entry(LAYER, 64, bits, r64, ops)},
         "g64_1x1": {"workload": "ResNet-50 1x1 conv 256->64, 56x56, batch 32, G=64", "steps": steps64,
                     "value": round(ops11 / (r11["wall_ms"] / steps64 * 1e-3) / 1e12, 2),
                     "ms_per_step": round(r11["wall_ms"] / steps64, 5),
                     "conv_us": round(r11["conv_us"], 3), "quantize_us": round(r11["quant_us"], 3),
                     "conv_only_tops": round(ops11 / (r11["conv_us"] * 1e-6) / 1e12, 1),
                     "roofline": roofline(LAYER_1X1, 64, bits, r11["conv_us"]),
-                    "fused": fused_entry(LAYER_1X1, 64, bits, r11, ops11)},
+                    "fused": fused_entry(LAYER_1X1, 64, bits, r11, ops11),
+                    "dfp": dfp_entry(LAYER_1X1, 64, bits, r11, ops11)},
     }
     out["gemm_m64"] = gemm_measure(torch, fgq, fi)
     if not args.no_stacks:

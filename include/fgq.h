@@ -63,7 +63,8 @@ enum {
   FGQ_ERR_SHAPE = 2,       /* non-positive or inconsistent sizes */
   FGQ_ERR_GROUP = 3,       /* G < 1 or G does not divide C (or K) */
   FGQ_ERR_BITS = 4,        /* bits not 8|4, or odd C / n with bits=4 */
-  FGQ_ERR_NONFINITE = 5,   /* fgq_ternarize met NaN or Inf weights */
+  FGQ_ERR_NONFINITE = 5,   /* fgq_ternarize met NaN or Inf weights (the
+                              fixed-point calls: NaN, Inf or negative alpha) */
   FGQ_ERR_HIP = 6,         /* HIP runtime error (also: no device) */
   FGQ_ERR_UNSUPPORTED = 7, /* method or path not available for the shape */
   FGQ_ERR_WORKSPACE = 8    /* workspace missing or too small */
@@ -187,7 +188,7 @@ fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha,
  *                every buffer is below 2^31 bytes: the per-group kernel for
  *                G = 64 (int32 group sums, fp32 alpha epilogue, at most
  *                K/64 + 1 fp32 roundings relative to s_x*sum_g alpha_g|P_g|)
- *                and the folded-scale kernel for other G (K < 2^17);
+ *                and the folded-scale kernel for other G (K <= 65536);
  *                otherwise the direct kernel runs.
  * y        [out] fp32 [B][Ho][Wo][O]
  */
@@ -236,6 +237,62 @@ fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx,
                       const float* alpha, const void* prepared, int64_t O,
                       int32_t G, int32_t out_bits, const float* out_scale,
                       uint8_t* q_out, void* stream);
+
+/*
+ * Fixed-point group scales (Sec. 4: the scaling factors are quantized to an
+ * 8- or 4-bit fixed point; 32-bit accumulation).
+ *
+ * fgq_dfp_alpha -- alpha quantized to a `bits`-bit (8|4) signed dynamic
+ * fixed point with one fractional length for the whole layer: with amax the
+ * largest alpha, integer length il = ceil(log2 amax) + 1, fl = bits - il,
+ * A = clamp(rint(alpha * 2^fl), 0, 2^(bits-1) - 1) (ties to even), so the
+ * quantized scale is A * 2^-fl; amax = 0 gives fl = 0 and A = 0.
+ *   alpha [in]  fp32, n values (e.g. a layer's [O][K/G] scales)
+ *   A     [out] int8, n values
+ *   fl    [out] device int32 scalar
+ * Synchronizes `stream`; FGQ_ERR_NONFINITE if an alpha is NaN, Inf or
+ * negative (outputs then unspecified).
+ *
+ * fgq_prepare_weights_dfp -- the constants of the layer with those scales:
+ * the int8 weights A[o][g(k)] * t[o][k] (one plane, the folded kernel's
+ * operand order), their uint8 offset term, fl, and the dequantized scales.
+ * 1 byte per weight plus 4 per group.  prepared: device buffer of
+ * fgq_prepared_bytes_dfp(O, K, G) bytes, 256-byte aligned, opaque.
+ * Synchronizes `stream`; FGQ_ERR_NONFINITE as for fgq_dfp_alpha.
+ *
+ * fgq_conv2d_dfp / fgq_gemm_dfp -- the layer
+ *   y = fp32( double(S) * (double(s_x) * 2^-fl) ),
+ *   S[m][o] = sum_k A[o][g(k)] t[o][k] q[m][k]   (exact int32),
+ * which is the correctly rounded value of s_x 2^-fl S whenever |S| < 2^29
+ * (K < 16577 for uint8).  Bit-identical on every path: the one-plane
+ * matrix-core kernel when C % 16 == 0 (or C = 4, 8), q is aligned as for
+ * fgq_conv2d and K <= 65536; otherwise the direct kernel on the dequantized
+ * scales.  Arguments as for fgq_conv2d / fgq_gemm, with the scales taken
+ * from `prepared` (codes are still read by the direct path).
+ *   out_bits  [in]  0: out is fp32 y; 8 or 4: out receives the codes of
+ *                   fgq_quantize_act(y, out_bits, scale_in = out_scale),
+ *                   laid out as q_out of fgq_conv2d_q (4 needs O even)
+ *   out_scale [in]  device fp32 scalar when out_bits != 0, else ignored
+ */
+fgq_status fgq_dfp_alpha(const float* alpha, int64_t n, int32_t bits,
+                         int8_t* A, int32_t* fl, void* stream);
+size_t fgq_prepared_bytes_dfp(int64_t O, int64_t K, int32_t G);
+fgq_status fgq_prepare_weights_dfp(const uint8_t* codes, const float* alpha,
+                                   int64_t O, int64_t K, int32_t G,
+                                   int32_t alpha_bits, void* prepared,
+                                   size_t prepared_bytes, void* stream);
+fgq_status fgq_conv2d_dfp(const uint8_t* q, int32_t bits, const float* sx,
+                          int64_t B, int64_t H, int64_t W, int64_t C,
+                          const uint8_t* codes, const void* prepared,
+                          int64_t O, int32_t R, int32_t S, int32_t stride_h,
+                          int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                          int32_t G, int32_t out_bits, const float* out_scale,
+                          void* out, void* stream);
+fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx,
+                        int64_t M, int64_t K, const uint8_t* codes,
+                        const void* prepared, int64_t O, int32_t G,
+                        int32_t out_bits, const float* out_scale, void* out,
+                        void* stream);
 
 /*
  * fgq_group_sums -- the exact integer group sums P[m][o][g] (Sec. 4: 32-bit

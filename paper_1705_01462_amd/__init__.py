@@ -54,6 +54,12 @@ _SIGS = {
     "fgq_gemm_q": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _I32, _P, _P, _P], _I32),
     "fgq_group_sums": ([_P, _I32, _I64, _I64, _I64, _I64, _P, _I64, _I32, _I32, _I32, _I32,
                         _I32, _I32, _I32, _I64, _I64, _P, _P], _I32),
+    "fgq_dfp_alpha": ([_P, _I64, _I32, _P, _P, _P], _I32),
+    "fgq_prepared_bytes_dfp": ([_I64, _I64, _I32], _SZ),
+    "fgq_prepare_weights_dfp": ([_P, _P, _I64, _I64, _I32, _I32, _P, _SZ, _P], _I32),
+    "fgq_conv2d_dfp": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _I64, _I32, _I32, _I32,
+                        _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
+    "fgq_gemm_dfp": ([_P, _I32, _P, _I64, _I64, _P, _P, _I64, _I32, _I32, _P, _P, _P], _I32),
 }
 
 
@@ -220,6 +226,76 @@ def fgq_gemm_q(q, bits, sx, M, K, codes, alpha, O, G, out_bits, out_scale, prepa
                           _dev(q_out, torch.uint8, "q_out"), _stream())
     _check(rc, "fgq_gemm_q")
     return q_out
+
+
+def fgq_dfp_alpha(alpha, bits, A=None, fl=None):
+    """Fixed-point group scales (one fractional length per layer): returns
+    (A int8 tensor shaped like alpha, fl int32[1] device scalar)."""
+    if A is None:
+        A = torch.empty(alpha.shape, dtype=torch.int8, device=alpha.device)
+    if fl is None:
+        fl = torch.empty(1, dtype=torch.int32, device=alpha.device)
+    rc = lib().fgq_dfp_alpha(_dev(alpha, torch.float32, "alpha"), alpha.numel(), bits,
+                             _dev(A, torch.int8, "A"), _dev(fl, torch.int32, "fl"), _stream())
+    _check(rc, "fgq_dfp_alpha")
+    return A, fl
+
+
+def fgq_prepared_bytes_dfp(O, K, G):
+    return int(lib().fgq_prepared_bytes_dfp(O, K, G))
+
+
+def fgq_prepare_weights_dfp(codes, alpha, O, K, G, alpha_bits, prepared=None):
+    """Constants of the layer with fixed-point scales (opaque uint8 buffer)."""
+    nb = fgq_prepared_bytes_dfp(O, K, G)
+    if nb == 0:
+        raise FgqError(3, "fgq_prepare_weights_dfp")
+    if prepared is None:
+        prepared = torch.empty(nb, dtype=torch.uint8, device=codes.device)
+    if prepared.data_ptr() % 256:
+        raise ValueError("prepared buffer must be 256-byte aligned")
+    rc = lib().fgq_prepare_weights_dfp(_dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                                       O, K, G, alpha_bits, ctypes.c_void_p(prepared.data_ptr()), nb,
+                                       _stream())
+    _check(rc, "fgq_prepare_weights_dfp")
+    return prepared
+
+
+def _dfp_out(shape_rows, O, out_bits, device, out):
+    if out is not None:
+        return out
+    if out_bits == 0:
+        return torch.empty(shape_rows + (O,), dtype=torch.float32, device=device)
+    return torch.empty(shape_rows + (O * out_bits // 8,), dtype=torch.uint8, device=device)
+
+
+def fgq_conv2d_dfp(q, bits, sx, shape, codes, prepared, O, R, S, stride, pad, G, out_bits=0,
+                   out_scale=None, out=None):
+    """The layer with fixed-point scales: fp32 y [B][Ho][Wo][O] (out_bits 0)
+    or the next layer's codes (out_bits 8 or 4, with out_scale)."""
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv_out_hw(H, W, R, S, (sh, sw), (ph, pw))
+    out = _dfp_out((B, Ho, Wo), O, out_bits, q.device, out)
+    rc = lib().fgq_conv2d_dfp(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), B, H, W, C,
+                              _dev(codes, torch.uint8, "codes"), _dev(prepared, torch.uint8, "prepared"),
+                              O, R, S, sh, sw, ph, pw, G, out_bits,
+                              None if out_scale is None else _dev(out_scale, torch.float32, "out_scale"),
+                              ctypes.c_void_p(out.data_ptr()), _stream())
+    _check(rc, "fgq_conv2d_dfp")
+    return out
+
+
+def fgq_gemm_dfp(q, bits, sx, M, K, codes, prepared, O, G, out_bits=0, out_scale=None, out=None):
+    out = _dfp_out((M,), O, out_bits, q.device, out)
+    rc = lib().fgq_gemm_dfp(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), M, K,
+                            _dev(codes, torch.uint8, "codes"), _dev(prepared, torch.uint8, "prepared"),
+                            O, G, out_bits,
+                            None if out_scale is None else _dev(out_scale, torch.float32, "out_scale"),
+                            ctypes.c_void_p(out.data_ptr()), _stream())
+    _check(rc, "fgq_gemm_dfp")
+    return out
 
 
 def fgq_group_sums(q, bits, shape, codes, O, R, S, stride, pad, G, row0, nrows, P=None):

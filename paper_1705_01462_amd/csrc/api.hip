@@ -60,6 +60,42 @@ fgq_status run_layer(const uint8_t* q, const float* sx, const uint8_t* codes,
   return launch_exact_conv(q, sx, codes, alpha, g, y, st);
 }
 
+// The layer with fixed-point scales: the one-plane folded kernel when the
+// shape allows it, else the direct kernel on the dequantized scales stored
+// in the prepared buffer (every alpha*P product and their fp64 sum are then
+// exact, so both give fp32(double(S) * (double(s_x) * 2^-fl))).
+fgq_status run_layer_dfp(const uint8_t* q, const float* sx, const uint8_t* codes,
+                         const void* prepared, const ConvGeom& g, const LayerOut& y, void* stream) {
+  hipStream_t st = as_stream(stream);
+  if (fold_dfp_supported(g, q)) return launch_fold_dfp_conv(q, sx, prepared, g, y, st);
+  const PreparedLayout L = prepared_layout_dfp(g.O, g.K, g.G);
+  const float* alpha_q = reinterpret_cast<const float*>(static_cast<const char*>(prepared) + L.alpha_off);
+  return launch_exact_conv(q, sx, codes, alpha_q, g, y, st);
+}
+
+// Output of a *_dfp layer call: fp32 (out_bits 0) or codes.
+bool layer_out(int32_t out_bits, const float* out_scale, void* out, int64_t O, LayerOut* lo,
+               fgq_status* err) {
+  if (out_bits == 0) {
+    *lo = LayerOut{static_cast<float*>(out), nullptr, nullptr, 0};
+    return true;
+  }
+  if (out_bits != 8 && out_bits != 4) {
+    *err = FGQ_ERR_BITS;
+    return false;
+  }
+  if (out_bits == 4 && O % 2 != 0) {
+    *err = FGQ_ERR_BITS;
+    return false;
+  }
+  if (!out_scale) {
+    *err = FGQ_ERR_NULL;
+    return false;
+  }
+  *lo = LayerOut{nullptr, static_cast<uint8_t*>(out), out_scale, out_bits};
+  return true;
+}
+
 }  // namespace
 
 extern "C" {
@@ -207,6 +243,73 @@ fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx, int64_t M
   if (out_bits == 4 && O % 2 != 0) return FGQ_ERR_BITS;
   if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
   return run_layer(q, sx, codes, alpha, prepared, g, LayerOut{nullptr, q_out, out_scale, out_bits}, stream);
+}
+
+fgq_status fgq_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A, int32_t* fl,
+                         void* stream) {
+  if (!alpha || !A || !fl) return FGQ_ERR_NULL;
+  if (bits != 8 && bits != 4) return FGQ_ERR_BITS;
+  if (n < 1) return FGQ_ERR_SHAPE;
+  hipStream_t st = as_stream(stream);
+  fgq_status rc = launch_dfp_alpha(alpha, n, bits, A, fl, st);
+  if (rc != FGQ_OK) return rc;
+  int32_t host = 0;
+  FGQ_TRY_HIP(hipMemcpyAsync(&host, fl, sizeof(host), hipMemcpyDeviceToHost, st));
+  FGQ_TRY_HIP(hipStreamSynchronize(st));
+  return host == INT32_MIN ? FGQ_ERR_NONFINITE : FGQ_OK;
+}
+
+size_t fgq_prepared_bytes_dfp(int64_t O, int64_t K, int32_t G) {
+  if (O < 1 || K < 1 || G < 1 || K % G != 0) return 0;
+  return static_cast<size_t>(prepared_layout_dfp(O, K, G).total);
+}
+
+fgq_status fgq_prepare_weights_dfp(const uint8_t* codes, const float* alpha, int64_t O, int64_t K,
+                                   int32_t G, int32_t alpha_bits, void* prepared,
+                                   size_t prepared_bytes, void* stream) {
+  if (!codes || !alpha || !prepared) return FGQ_ERR_NULL;
+  if (O < 1 || K < 1) return FGQ_ERR_SHAPE;
+  if (G < 1 || K % G != 0) return FGQ_ERR_GROUP;
+  if (alpha_bits != 8 && alpha_bits != 4) return FGQ_ERR_BITS;
+  if (O > (1LL << 31) || K > (1LL << 31)) return FGQ_ERR_SHAPE;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  if (prepared_bytes < static_cast<size_t>(prepared_layout_dfp(O, K, G).total)) return FGQ_ERR_WORKSPACE;
+  hipStream_t st = as_stream(stream);
+  fgq_status rc = launch_prepare_dfp(codes, alpha, O, K, G, alpha_bits, prepared, st);
+  if (rc != FGQ_OK) return rc;
+  int32_t host = 0;
+  FGQ_TRY_HIP(hipMemcpyAsync(&host, prepared, sizeof(host), hipMemcpyDeviceToHost, st));
+  FGQ_TRY_HIP(hipStreamSynchronize(st));
+  return host == INT32_MIN ? FGQ_ERR_NONFINITE : FGQ_OK;
+}
+
+fgq_status fgq_conv2d_dfp(const uint8_t* q, int32_t bits, const float* sx, int64_t B, int64_t H,
+                          int64_t W, int64_t C, const uint8_t* codes, const void* prepared,
+                          int64_t O, int32_t R, int32_t S, int32_t stride_h, int32_t stride_w,
+                          int32_t pad_h, int32_t pad_w, int32_t G, int32_t out_bits,
+                          const float* out_scale, void* out, void* stream) {
+  if (!q || !sx || !codes || !prepared || !out) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(B, H, W, C, O, R, S, stride_h, stride_w, pad_h, pad_w, G, bits, &g, &err))
+    return err;
+  LayerOut lo;
+  if (!layer_out(out_bits, out_scale, out, O, &lo, &err)) return err;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  return run_layer_dfp(q, sx, codes, prepared, g, lo, stream);
+}
+
+fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx, int64_t M, int64_t K,
+                        const uint8_t* codes, const void* prepared, int64_t O, int32_t G,
+                        int32_t out_bits, const float* out_scale, void* out, void* stream) {
+  if (!q || !sx || !codes || !prepared || !out) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(1, M, 1, K, O, 1, 1, 1, 1, 0, 0, G, bits, &g, &err)) return err;
+  LayerOut lo;
+  if (!layer_out(out_bits, out_scale, out, O, &lo, &err)) return err;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  return run_layer_dfp(q, sx, codes, prepared, g, lo, stream);
 }
 
 fgq_status fgq_group_sums(const uint8_t* q, int32_t bits, int64_t B, int64_t H, int64_t W,

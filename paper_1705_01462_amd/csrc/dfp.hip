@@ -1,0 +1,180 @@
+// dfp.hip -- fixed-point group scales (Sec. 4: the scaling factors are
+// quantized to an 8- or 4-bit fixed point) and the constants of the layer
+// that uses them.
+//
+// Scales: one fractional length fl per layer (a dynamic fixed point whose
+// exponent is shared by the layer).  With amax the largest alpha, the
+// integer length is il = ceil(log2 amax) + 1 and fl = bits - il; a scale is
+// A * 2^-fl with A = clamp(rint(alpha * 2^fl), 0, 2^(bits-1) - 1), a signed
+// code, so that A * t fits int8.
+//
+// Layer: with w'[o][k] = A[o][g(k)] * t[o][k] in [-127, 127] the layer is one
+// exact int8 product S = sum_k w' q, and y = fp32(double(S) * (double(s_x) *
+// 2^-fl)), which is the correctly rounded value of s_x 2^-fl S whenever
+// |S| < 2^29.  The planes are written in the folded kernel's fragment order
+// with one plane, plus the uint8 offset term 128 * sum_k w' and the
+// dequantized scales A * 2^-fl for the direct kernel.
+#include <limits.h>
+
+#include "fgq_internal.h"
+
+// Every floating-point expression here is evaluated exactly as written.
+#pragma clang fp contract(off)
+
+namespace fgq {
+
+PreparedLayout prepared_layout_dfp(int64_t O, int64_t K, int32_t G) {
+  PreparedLayout L;
+  L.kind = kPrepDfp;
+  L.O32 = round_up(O, 32);
+  L.Kp = round_up(K, 2 * kFoldKStep);
+  L.nks = L.Kp / kFoldKStep;
+  L.planes_off = kDfpHeaderBytes;
+  L.bias_off = round_up(L.planes_off + L.O32 * L.Kp, 256);
+  L.alpha_off = round_up(L.bias_off + 4 * O, 256);
+  L.total = round_up(L.alpha_off + 4 * O * (K / G), 256);
+  L.scale_off = L.total;
+  return L;
+}
+
+namespace {
+
+constexpr int kThreads = 256;
+constexpr int kExpThreads = 1024;
+
+// One workgroup: the largest alpha, then fl (INT32_MIN if any alpha is NaN,
+// Inf or negative).
+__global__ __launch_bounds__(kExpThreads) void dfp_exponent_kernel(const float* __restrict__ alpha,
+                                                                   int64_t n, int32_t bits,
+                                                                   int32_t* __restrict__ fl) {
+  __shared__ float red[kExpThreads / 64];
+  __shared__ int badw[kExpThreads / 64];
+  float amax = 0.0f;
+  int bad = 0;
+  for (int64_t i = threadIdx.x; i < n; i += kExpThreads) {
+    const float a = alpha[i];
+    bad |= !(a >= 0.0f && a < __builtin_huge_valf());  // NaN, Inf or negative
+    amax = fmaxf(amax, a);
+  }
+  for (int off = 32; off > 0; off >>= 1) {
+    amax = fmaxf(amax, __shfl_xor(amax, off));
+    bad |= __shfl_xor(bad, off);
+  }
+  const int lane = threadIdx.x % 64, wid = threadIdx.x / 64;
+  if (lane == 0) {
+    red[wid] = amax;
+    badw[wid] = bad;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    for (int i = 1; i < kExpThreads / 64; ++i) {
+      amax = fmaxf(amax, red[i]);
+      bad |= badw[i];
+    }
+    amax = fmaxf(amax, red[0]);
+    bad |= badw[0];
+    int32_t f = 0;
+    if (amax > 0.0f) {
+      int e;
+      const float m = frexpf(amax, &e);  // amax = m 2^e, m in [0.5, 1)
+      const int ceil_log2 = m == 0.5f ? e - 1 : e;
+      f = bits - (ceil_log2 + 1);
+    }
+    fl[0] = bad ? INT_MIN : f;
+  }
+}
+
+__device__ inline int dfp_code(float alpha, int32_t fl, int32_t bits) {
+  const double top = static_cast<double>((1 << (bits - 1)) - 1);
+  double v = rint(ldexp(static_cast<double>(alpha), fl));
+  v = v > top ? top : v;
+  return static_cast<int>(v);
+}
+
+__global__ __launch_bounds__(kThreads) void dfp_codes_kernel(const float* __restrict__ alpha, int64_t n,
+                                                             int32_t bits, const int32_t* __restrict__ flp,
+                                                             int8_t* __restrict__ A) {
+  const int32_t fl = *flp;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kThreads + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kThreads)
+    A[i] = fl == INT_MIN ? 0 : static_cast<int8_t>(dfp_code(alpha[i], fl, bits));
+}
+
+// Byte offset of channel o, reduction index k in the one-plane fragment order.
+__device__ inline int64_t frag_offset1(int64_t nks, int64_t o, int64_t k) {
+  const int64_t tile = o / 32, ks = k / kFoldKStep;
+  const int kk = static_cast<int>(k % kFoldKStep);
+  const int half = kk / 32, lane = static_cast<int>(o % 32) + 32 * ((kk % 32) / 16);
+  return ((tile * nks + ks) * 2 + half) * 1024 + lane * 16 + (kk % 16);
+}
+
+// One block per channel of the padded channel range.
+__global__ __launch_bounds__(kThreads) void prepare_dfp_kernel(
+    const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O, int64_t K,
+    int32_t G, int32_t bits, int64_t Kp, const int32_t* __restrict__ flp, int8_t* __restrict__ planes,
+    int32_t* __restrict__ bias, float* __restrict__ alpha_q) {
+  __shared__ int64_t red[kThreads / 64];
+  const int64_t o = blockIdx.x;
+  const int64_t nks = Kp / kFoldKStep;
+  const int32_t fl = *flp;
+  if (o >= O || fl == INT_MIN) {  // padding channel (or rejected scales)
+    for (int64_t k = threadIdx.x; k < Kp; k += kThreads) planes[frag_offset1(nks, o, k)] = 0;
+    return;
+  }
+  const int64_t ng = K / G;
+  const int64_t rb = ceil_div(K, 4);
+  for (int64_t gi = threadIdx.x; gi < ng; gi += kThreads)
+    alpha_q[o * ng + gi] =
+        static_cast<float>(ldexp(static_cast<double>(dfp_code(alpha[o * ng + gi], fl, bits)), -fl));
+  int64_t s = 0;
+  for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
+    int v = 0;
+    if (k < K) {
+      const uint32_t c = (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u;
+      const int t = c == 1 ? 1 : (c == 3 ? -1 : 0);
+      v = t * dfp_code(alpha[o * ng + k / G], fl, bits);
+    }
+    planes[frag_offset1(nks, o, k)] = static_cast<int8_t>(v);
+    s += v;
+  }
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (threadIdx.x % 64 == 0) red[threadIdx.x / 64] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t v = 0;
+    for (int i = 0; i < kThreads / 64; ++i) v += red[i];
+    bias[o] = static_cast<int32_t>(128 * v);
+  }
+}
+
+}  // namespace
+
+fgq_status launch_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A, int32_t* fl,
+                            hipStream_t st) {
+  hipLaunchKernelGGL(dfp_exponent_kernel, dim3(1), dim3(kExpThreads), 0, st, alpha, n, bits, fl);
+  if (hipGetLastError() != hipSuccess) return FGQ_ERR_HIP;
+  if (A && n > 0) {
+    const int64_t blocks = ceil_div(n, kThreads) < 4096 ? ceil_div(n, kThreads) : 4096;
+    hipLaunchKernelGGL(dfp_codes_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, st,
+                       alpha, n, bits, fl, A);
+  }
+  return last_launch();
+}
+
+fgq_status launch_prepare_dfp(const uint8_t* codes, const float* alpha, int64_t O, int64_t K,
+                              int32_t G, int32_t alpha_bits, void* prepared, hipStream_t st) {
+  const PreparedLayout L = prepared_layout_dfp(O, K, G);
+  char* base = static_cast<char*>(prepared);
+  int32_t* fl = reinterpret_cast<int32_t*>(base);
+  fgq_status rc = launch_dfp_alpha(alpha, O * (K / G), alpha_bits, nullptr, fl, st);
+  if (rc != FGQ_OK) return rc;
+  if (L.O32 > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  hipLaunchKernelGGL(prepare_dfp_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0, st,
+                     codes, alpha, O, K, G, alpha_bits, L.Kp, fl,
+                     reinterpret_cast<int8_t*>(base + L.planes_off),
+                     reinterpret_cast<int32_t*>(base + L.bias_off),
+                     reinterpret_cast<float*>(base + L.alpha_off));
+  return last_launch();
+}
+
+}  // namespace fgq

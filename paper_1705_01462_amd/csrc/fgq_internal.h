@@ -54,21 +54,33 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 //               [O32/32][Kp/64][3 planes][2 K halves][64 lanes][16 bytes]
 //      bias   : int32 [3][O]  128 * sum_k plane_j[o][k] (uint8 offset term)
 //      scale  : fp32  [O]     2^-E_o
+// A third kind is written by fgq_prepare_weights_dfp (any G), for the layer
+// with fixed-point group scales:
+//      header : int32 fl, the fractional length of the layer's scales
+//      planes : int8 A[o][g(k)] * t[o][k], one plane,
+//               [O32/32][Kp/64][1 plane][2 K halves][64 lanes][16 bytes]
+//      bias   : int32 [O]     128 * sum_k plane[o][k]
+//      alpha  : fp32 [O][K/G] the dequantized scales A * 2^-fl (direct path)
 // In the fragment order, lane l of (channel tile, 64-wide K block, plane,
 // half) holds channel 32*tile + l%32, k = 64*block + 32*half + 16*(l/32) +
 // [0, 16), so each wave-wide 16-byte load is one contiguous kilobyte.
 // Channels >= O, k >= K (and their alpha) are zero; Kp is a multiple of 128.
-enum PrepKind { kPrepFold = 0, kPrepGroup = 1 };
+enum PrepKind { kPrepFold = 0, kPrepGroup = 1, kPrepDfp = 2 };
 struct PreparedLayout {
   int kind;
   int64_t O32, Kp, nks, planes_off, bias_off, scale_off, alpha_off, total;
 };
 constexpr int64_t kFoldKStep = 64;
 constexpr int64_t kFoldTileBytes = 3 * 2 * 64 * 16;  // one channel tile, one K block
+constexpr int64_t kDfpHeaderBytes = 256;
+// Largest K of the int8 folded kernels: with uint8 activations the int32
+// accumulator holds up to 255 * 127 * K, below 2^31 for K <= 65536.
+constexpr int64_t kFoldMaxK = 65536;
 // The per-group kernel accumulates one fp32 product per group; with at most
 // 160 groups its rounding error stays below 1e-5 of the summand magnitude.
 constexpr int64_t kGroupMaxGroups = 160;
 PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G);
+PreparedLayout prepared_layout_dfp(int64_t O, int64_t K, int32_t G);
 
 // Launchers (return FGQ_OK or FGQ_ERR_HIP); arguments already validated.
 fgq_status launch_ternarize(const float* w, int64_t O, int64_t C, int32_t R,
@@ -88,12 +100,24 @@ fgq_status launch_group_sums(const uint8_t* q, const uint8_t* codes,
 fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O,
                           int64_t K, int32_t G, void* prepared,
                           hipStream_t st);
+// Fixed-point group scales: the layer exponent into *fl (INT32_MIN when an
+// alpha is NaN, Inf or negative) and the codes A (A may be NULL).
+fgq_status launch_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A,
+                            int32_t* fl, hipStream_t st);
+fgq_status launch_prepare_dfp(const uint8_t* codes, const float* alpha, int64_t O,
+                              int64_t K, int32_t G, int32_t alpha_bits, void* prepared,
+                              hipStream_t st);
 // Folded-scale int8 MFMA kernel (prepared layout of kind fold); callers
-// check fold_supported first.
+// check fold_supported first.  The dfp variant runs the one-plane layer of
+// kind dfp on the same kernel.
 bool fold_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_fold_conv(const uint8_t* q, const float* sx,
                             const void* prepared, const ConvGeom& g, const LayerOut& out,
                             hipStream_t st);
+bool fold_dfp_supported(const ConvGeom& g, const uint8_t* q);
+fgq_status launch_fold_dfp_conv(const uint8_t* q, const float* sx,
+                                const void* prepared, const ConvGeom& g, const LayerOut& out,
+                                hipStream_t st);
 // Per-group int8 MFMA kernel with an fp32 alpha epilogue (G = 64).
 bool group_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_group_conv(const uint8_t* q, const float* sx,

@@ -6,7 +6,7 @@ namespace fgq {
 
 bool fold_supported(const ConvGeom& g, const uint8_t* q) {
   const PreparedLayout L = prepared_layout(g.O, g.K, g.G);
-  return L.kind == kPrepFold && g.K < (1LL << 17) && ig::igemm_shape_ok(g, q, /*tiny_c=*/true) &&
+  return L.kind == kPrepFold && g.K <= kFoldMaxK && ig::igemm_shape_ok(g, q, /*tiny_c=*/true) &&
          3 * L.O32 * L.Kp < (1LL << 31);
 }
 
@@ -23,6 +23,7 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.y = out.y;
   a.qo = out.q;
   a.oscale = out.scale;
+  a.fl = nullptr;
   a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);

@@ -1,0 +1,41 @@
+// fold_dfp.hip -- the layer with fixed-point group scales (dfp.hip) on the
+// folded kernel with one weight plane: host entry and the fp32-output
+// instantiation.
+#include "fold_kernel.h"
+
+namespace fgq {
+
+bool fold_dfp_supported(const ConvGeom& g, const uint8_t* q) {
+  const PreparedLayout L = prepared_layout_dfp(g.O, g.K, g.G);
+  return g.K <= kFoldMaxK && ig::igemm_shape_ok(g, q, /*tiny_c=*/true) && L.O32 * L.Kp < (1LL << 31);
+}
+
+fgq_status launch_fold_dfp_conv(const uint8_t* q, const float* sx, const void* prepared,
+                                const ConvGeom& g, const LayerOut& out, hipStream_t st) {
+  const PreparedLayout L = prepared_layout_dfp(g.O, g.K, g.G);
+  const char* base = static_cast<const char*>(prepared);
+  FoldArgs a;
+  ig::fill_act_args(g, q, &a.x);
+  a.sx = sx;
+  a.planes = reinterpret_cast<const int8_t*>(base + L.planes_off);
+  a.bias = reinterpret_cast<const int32_t*>(base + L.bias_off);
+  a.scale = nullptr;
+  a.y = out.y;
+  a.qo = out.q;
+  a.oscale = out.scale;
+  a.fl = reinterpret_cast<const int32_t*>(base);
+  a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
+  a.nks = static_cast<int32_t>(L.nks);
+  a.planes_bytes = static_cast<int32_t>(L.O32 * L.Kp);
+  switch (out.bits) {
+    case 0: return launch_fold_dfp_out_f32(a, g.bits, st);
+    case 8: return launch_fold_dfp_out_q8(a, g.bits, st);
+    default: return launch_fold_dfp_out_q4(a, g.bits, st);
+  }
+}
+
+fgq_status launch_fold_dfp_out_f32(const FoldArgs& a, int bits, hipStream_t st) {
+  return launch_out<0, true>(a, bits, st);
+}
+
+}  // namespace fgq

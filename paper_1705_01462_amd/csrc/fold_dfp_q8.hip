@@ -1,0 +1,11 @@
+// fold_dfp_q8.hip -- the fixed-point-scale layer kernels that emit 8-bit
+// codes of the next layer's activations.
+#include "fold_kernel.h"
+
+namespace fgq {
+
+fgq_status launch_fold_dfp_out_q8(const FoldArgs& a, int bits, hipStream_t st) {
+  return launch_out<8, true>(a, bits, st);
+}
+
+}  // namespace fgq

@@ -2,15 +2,19 @@
 // the kernel template and its launch logic.  The output kind is a template
 // parameter (fp32 y, or 8-/4-bit codes of the next layer's activations), and
 // each kind is instantiated in a source file of its own (fold.hip,
-// fold_q8.hip, fold_q4.hip) so that they compile in parallel.
+// fold_q8.hip, fold_q4.hip; fold_dfp*.hip for fixed-point scales) so that
+// they compile in parallel.
 //
 // With the per-group scales folded into three int8 digit planes (see
 // prepare.hip), the layer is three exact int8 GEMMs sharing one activation
 // operand:
 //   S_j[o][m] = sum_k plane_j[o][k] * q'[m][k],   q' = q ^ 0x80 (uint8) or q (uint4)
 //   y[m][o]   = sum_j (S_j + bias_j[o]) * (s_x * 2^-E_o * 255^j)
-// The integer sums are exact (|S_j| < 2^31 for K < 2^17); the combination
-// is three fp32 conversions and fused multiply-adds per output.
+// The integer sums are exact (|S_j + bias_j| <= 255 * 127 * K < 2^31 for
+// K <= 65536); the combination is three fp32 conversions and fused
+// multiply-adds per output.  With fixed-point scales (kDfp, see dfp.hip)
+// the scale is already in the single plane A*t, and the output is
+// fp32(double(S) * (double(s_x) * 2^-fl)).
 //
 // Implicit GEMM: row m = (b, ho, wo), k = (r*S + s)*C + c, so a 16-element
 // piece of k (C % 16 == 0) is 16 consecutive channels of one input pixel.
@@ -59,6 +63,7 @@ struct FoldArgs {
   float* y;
   uint8_t* qo;           // output codes (kOut 8 or 4)
   const float* oscale;   // their scale
+  const int32_t* fl;     // fixed-point scales: fractional length (prepared header)
   int32_t staged;        // epilogue through LDS (epi_staged)
   int32_t nks, planes_bytes;
 };
@@ -67,12 +72,15 @@ struct FoldArgs {
 fgq_status launch_fold_out_f32(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_out_q4(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_dfp_out_f32(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_dfp_out_q8(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_dfp_out_q4(const FoldArgs& a, int bits, hipStream_t st);
 
 namespace {
 
 using namespace ig;
 
-template <int kBits, int kNWO, int kNB, int kCM, int kOut>
+template <int kBits, int kNWO, int kNB, int kCM, int kOut, bool kDfp>
 __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(FoldArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
@@ -96,7 +104,9 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   // ---- weight fragments: lane supplies channel o0 + lane%32, k-slot
   // 16*(lane/32) of K half h; the fragment-ordered planes put the wave's
   // 64 lanes x 16 bytes of (tile, step, plane, half) in one kilobyte.
-  const int wbase = (o0 / 32) * a.nks * static_cast<int>(kFoldTileBytes) + 16 * lane;
+  constexpr int kPlanes = kDfp ? 1 : 3;        // weight planes (fixed-point scales: one)
+  constexpr int kTileB = kPlanes * 2 * 1024;   // bytes of one channel tile, one 64-wide K block
+  const int wbase = (o0 / 32) * a.nks * kTileB + 16 * lane;
 
   const int nk = (a.x.K + kKT - 1) / kKT;
   Stager xs;
@@ -106,15 +116,15 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   // The step is the scalar offset, which the buffer range check does not
   // cover, so a step past the last is clamped to the last one (those loads
   // are never used).
-  v4i wring[2][3][4];
+  v4i wring[2][kPlanes][4];
   auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
     ks = ks < nk ? ks : nk - 1;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
-      const int kso = (2 * ks + blk) * static_cast<int>(kFoldTileBytes);
+      const int kso = (2 * ks + blk) * kTileB;
 #pragma unroll
-      for (int j = 0; j < 3; ++j)
+      for (int j = 0; j < kPlanes; ++j)
 #pragma unroll
         for (int h = 0; h < 2; ++h)
           wring[u][j][2 * blk + h] =
@@ -124,11 +134,11 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 
   // Accumulators start at the uint8 offset term 128 * sum_k plane_j[o][k]
   // of the lane's channel, so the epilogue needs no integer additions.
-  v16i acc[3][kNB];
+  v16i acc[kPlanes][kNB];
   {
     const int oc = o0 + lane % 32;
 #pragma unroll
-    for (int j = 0; j < 3; ++j) {
+    for (int j = 0; j < kPlanes; ++j) {
       const int bj = (kBits == 8 && oc < a.x.O) ? a.bias[j * a.x.O + oc] : 0;
       v16i init;
 #pragma unroll
@@ -146,7 +156,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 #pragma unroll
     for (int h = 0; h < 4; ++h) afrag[c][h] = lds_off(wm * kNB * 32 + 32 * c + lane % 32, 2 * h + lane / 32);
 
-  auto compute = [&](int stage, const v4i (&w)[3][4]) {
+  auto compute = [&](int stage, const v4i (&w)[kPlanes][4]) {
     const unsigned char* base = lds + stage * kStage;
     if constexpr (kNB <= 2) {
       // Two workgroups share the compute unit: read each K slice's
@@ -160,7 +170,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 #pragma unroll
         for (int c = 0; c < kNB; ++c)
 #pragma unroll
-          for (int j = 0; j < 3; ++j)
+          for (int j = 0; j < kPlanes; ++j)
             acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], w[j][h], acc[j][c], 0, 0, 0);
       }
     } else {
@@ -174,7 +184,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 #pragma unroll
         for (int c = 0; c < kNB; ++c)
 #pragma unroll
-          for (int j = 0; j < 3; ++j)
+          for (int j = 0; j < kPlanes; ++j)
             acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][h], w[j][h], acc[j][c], 0, 0, 0);
     }
   };
@@ -204,12 +214,12 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 #pragma unroll
       for (int i = 0; i < 4 * kNB; ++i) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
 #pragma unroll
-      for (int i = 0; i < 12; ++i) {
+      for (int i = 0; i < 4 * kPlanes; ++i) {
         __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
         __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
         __builtin_amdgcn_sched_group_barrier(0x002, 4, 0);
       }
-      __builtin_amdgcn_sched_group_barrier(0x008, 12 * kNB - 24, 0);
+      __builtin_amdgcn_sched_group_barrier(0x008, 4 * kPlanes * kNB - 8 * kPlanes, 0);
     }
     __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
     xs.store(lds + (1 - u) * kStage, 0x80808080u);  // q - 128 (padding 0 -> -128)
@@ -231,27 +241,36 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   // ---- epilogue: lane holds rows m of channel o.
   const int o = o0 + lane % 32;
   const float sx = *a.sx;
-  const float c0 = o < a.x.O ? sx * a.scale[o] : 0.0f;
-  const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
   // locals: a byte store may alias anything, including the argument block
   const OutPtrs out{a.y, a.qo, a.x.M, a.x.O};
   const bool staged = a.staged != 0;
-  with_out_scale<kOut>(a.oscale, [&](const QScale& qs, auto rcp) {
-    constexpr bool kR = decltype(rcp)::value;
-    auto val = [&](int c, int r) {
-      const float f2 = static_cast<float>(acc[2][c][r]);
-      const float f1 = static_cast<float>(acc[1][c][r]);
+  auto emit = [&](auto val) {
+    with_out_scale<kOut>(a.oscale, [&](const QScale& qs, auto rcp) {
+      constexpr bool kR = decltype(rcp)::value;
+      if (staged)
+        store_staged<kOut, kNWO, kNB, kR>(lds, out, qs, m0, o0 - 32 * wo, wm, wo, tid, val);
+      else
+        store_direct<kOut, kNB, kR>(out, qs, m0 + wm * kNB * 32, o, lane, val);
+    });
+  };
+  if constexpr (kDfp) {
+    // y = fp32(double(S) * (double(s_x) * 2^-fl)); the scale is exact.
+    const int32_t fl = *a.fl;  // INT32_MIN marks rejected scales (never negated)
+    const double cd = fl > -2048 && fl < 2048 ? static_cast<double>(sx) * ldexp(1.0, -fl) : 0.0;
+    emit([&](int c, int r) { return static_cast<float>(static_cast<double>(acc[0][c][r]) * cd); });
+  } else {
+    const float c0 = o < a.x.O ? sx * a.scale[o] : 0.0f;
+    const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
+    emit([&](int c, int r) {
+      const float f2 = static_cast<float>(acc[2 % kPlanes][c][r]);
+      const float f1 = static_cast<float>(acc[1 % kPlanes][c][r]);
       const float f0 = static_cast<float>(acc[0][c][r]);
       return fmaf(f2, c2, fmaf(f1, c1, f0 * c0));
-    };
-    if (staged)
-      store_staged<kOut, kNWO, kNB, kR>(lds, out, qs, m0, o0 - 32 * wo, wm, wo, tid, val);
-    else
-      store_direct<kOut, kNB, kR>(out, qs, m0 + wm * kNB * 32, o, lane, val);
-  });
+    });
+  }
 }
 
-template <int kOut, int kBits, int kNWO, int kNB>
+template <int kOut, bool kDfp, int kBits, int kNWO, int kNB>
 fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   constexpr int kTO = 32 * kNWO, kTM = (4 / kNWO) * kNB * 32;
   FoldArgs a = a0;
@@ -261,10 +280,10 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   if (n > 0x7fffffffLL) return FGQ_ERR_SHAPE;
   const dim3 grid(static_cast<uint32_t>(n));
   switch (c_mode(a.x.C)) {
-    case 0: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 0, kOut>), grid, dim3(kThreads), 0, st, a); break;
-    case 1: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 1, kOut>), grid, dim3(kThreads), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 4, kOut>), grid, dim3(kThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 8, kOut>), grid, dim3(kThreads), 0, st, a); break;
+    case 0: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 0, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 1, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 4, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 8, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
   }
   return last_launch();
 }
@@ -272,7 +291,7 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
 // Rows per wave (kNB blocks of 32): the busiest compute unit does
 // ceil(tiles / CUs) workgroups of kNB blocks per SIMD; among equal costs
 // the smaller kNB wins (kNB = 2 runs two workgroups per compute unit).
-template <int kOut, int kBits, int kNWO>
+template <int kOut, bool kDfp, int kBits, int kNWO>
 fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
   constexpr int kNWM = 4 / kNWO;
   const int64_t otiles = ceil_div(a.x.O, 32 * kNWO);
@@ -287,22 +306,22 @@ fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
     }
   }
   switch (best) {
-    case 2: return launch_cfg<kOut, kBits, kNWO, 2>(a, st);
-    case 3: return launch_cfg<kOut, kBits, kNWO, 3>(a, st);
-    default: return launch_cfg<kOut, kBits, kNWO, 4>(a, st);
+    case 2: return launch_cfg<kOut, kDfp, kBits, kNWO, 2>(a, st);
+    case 3: return launch_cfg<kOut, kDfp, kBits, kNWO, 3>(a, st);
+    default: return launch_cfg<kOut, kDfp, kBits, kNWO, 4>(a, st);
   }
 }
 
-template <int kOut, int kBits>
+template <int kOut, bool kDfp, int kBits>
 fgq_status launch_bits(const FoldArgs& a, hipStream_t st) {
-  if (a.x.O > 64) return launch_nwo<kOut, kBits, 4>(a, st);
-  if (a.x.O > 32) return launch_nwo<kOut, kBits, 2>(a, st);
-  return launch_nwo<kOut, kBits, 1>(a, st);
+  if (a.x.O > 64) return launch_nwo<kOut, kDfp, kBits, 4>(a, st);
+  if (a.x.O > 32) return launch_nwo<kOut, kDfp, kBits, 2>(a, st);
+  return launch_nwo<kOut, kDfp, kBits, 1>(a, st);
 }
 
-template <int kOut>
+template <int kOut, bool kDfp = false>
 fgq_status launch_out(const FoldArgs& a, int bits, hipStream_t st) {
-  return bits == 8 ? launch_bits<kOut, 8>(a, st) : launch_bits<kOut, 4>(a, st);
+  return bits == 8 ? launch_bits<kOut, kDfp, 8>(a, st) : launch_bits<kOut, kDfp, 4>(a, st);
 }
 
 }  // namespace

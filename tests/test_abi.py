@@ -27,7 +27,8 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, n), n
     # the binding wraps every entry point under the same name
     for n in ("fgq_ternarize", "fgq_quantize_act", "fgq_prepare_weights", "fgq_conv2d",
-              "fgq_gemm", "fgq_group_sums"):
+              "fgq_gemm", "fgq_group_sums", "fgq_conv2d_q", "fgq_gemm_q", "fgq_dfp_alpha",
+              "fgq_prepare_weights_dfp", "fgq_conv2d_dfp", "fgq_gemm_dfp"):
         assert callable(getattr(fgq, n))
 
 
@@ -86,6 +87,38 @@ def test_fused_layer_validation():
     assert L.fgq_conv2d_q(*args(16, 8, None, P)) == 1       # FGQ_ERR_NULL: scale
     assert L.fgq_conv2d_q(*args(16, 8, P, None)) == 1       # FGQ_ERR_NULL: q_out
     assert L.fgq_gemm_q(P, 8, P, 4, 16, P, P, None, 15, 4, 4, P, P, None) == 4
+
+
+def test_prepared_bytes_dfp():
+    L = fgq.lib()
+    # header 256, one int8 plane O32*Kp, bias 4*O, dequantized scales 4*O*K/G
+    plane = 128 * 1152
+    bias_off = 256 + plane
+    alpha_off = bias_off + 512
+    assert L.fgq_prepared_bytes_dfp(128, 1152, 4) == alpha_off + 4 * 128 * 288
+    assert L.fgq_prepared_bytes_dfp(128, 1152, 5) == 0
+    # O padded to 32, K to 128
+    assert L.fgq_prepared_bytes_dfp(33, 100, 4) % 256 == 0
+    assert L.fgq_prepared_bytes_dfp(33, 100, 4) >= 256 + 64 * 128 + 4 * 33 + 4 * 33 * 25
+
+
+@no_device
+def test_dfp_validation():
+    L = fgq.lib()
+    assert L.fgq_dfp_alpha(None, 4, 8, P, P, None) == 1
+    assert L.fgq_dfp_alpha(P, 4, 6, P, P, None) == 4
+    assert L.fgq_dfp_alpha(P, 0, 8, P, P, None) == 2
+    assert L.fgq_prepare_weights_dfp(P, P, 16, 64, 4, 6, P, 1 << 20, None) == 4   # alpha bits
+    assert L.fgq_prepare_weights_dfp(P, P, 16, 64, 3, 8, P, 1 << 20, None) == 3   # G
+    assert L.fgq_prepare_weights_dfp(P, P, 16, 64, 4, 8, P, 16, None) == 8        # too small
+    conv = lambda ob, O, sc, prep: L.fgq_conv2d_dfp(P, 8, P, 2, 8, 8, 16, P, prep, O, 3, 3, 1, 1,
+                                                    1, 1, 4, ob, sc, P, None)
+    assert conv(7, 16, P, P) == 4                                  # out_bits
+    assert conv(4, 15, P, P) == 4                                  # 4-bit output needs even O
+    assert conv(8, 16, None, P) == 1                               # scale for codes
+    assert conv(0, 16, None, None) == 1                            # prepared required
+    assert conv(0, 16, None, ctypes.c_void_p(0x1001)) == 8         # prepared alignment
+    assert L.fgq_gemm_dfp(P, 8, P, 4, 16, P, P, 16, 5, 0, None, P, None) == 3
 
 
 @no_device
