@@ -50,10 +50,15 @@ def lib():
                                      _c_i32, _c_i64, _c_i64, _c_i32, _c_p]
         L.orc_gemm_dfp.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_p, _c_p, _c_i32, _c_i64,
                                    _c_i32, _c_i32, _c_p]
+        L.orc_w8_quantize.argtypes = [_c_p, _c_i64, _c_p, _c_p]
+        L.orc_conv2d_w8.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_i64, _c_i64, _c_p, _c_i32,
+                                    _c_i64, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i64,
+                                    _c_i64, _c_i32, _c_p]
         L.orc_max_threads.argtypes = []
         for f in ("orc_ternarize_group", "orc_ternarize", "orc_quantize_act",
                   "orc_group_sums_conv", "orc_conv2d", "orc_gemm", "orc_dfp_alpha",
-                  "orc_conv2d_dfp", "orc_gemm_dfp", "orc_max_threads"):
+                  "orc_conv2d_dfp", "orc_gemm_dfp", "orc_w8_quantize", "orc_conv2d_w8",
+                  "orc_max_threads"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -209,6 +214,29 @@ def gemm_dfp(q, bits, sx, M, K, codes, A, fl, O, G, nthreads=0):
     A = np.ascontiguousarray(A, dtype=np.int8)
     _check(lib().orc_gemm_dfp(_ptr(q), bits, float(sx), M, K, _ptr(codes), _ptr(A), fl, O, G,
                               nthreads, _ptr(y)))
+    return y
+
+
+def w8_quantize(w):
+    """First layer at 8-bit weights: returns (W8 int8, same shape as w; fl)."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    W8 = np.zeros(w.shape, np.int8)
+    fl = np.zeros(1, np.int32)
+    _check(lib().orc_w8_quantize(_ptr(w), w.size, _ptr(W8), _ptr(fl)))
+    return W8, int(fl[0])
+
+
+def conv2d_w8(q, bits, sx, shape, W8, fl, O, R, S, stride, pad, rows=None, nthreads=0):
+    """fp32 output [B*Ho*Wo][O] of the 8-bit-weight layer; W8 is [O][C][R][S]."""
+    B, H, W, C = shape
+    Ho, Wo = conv_out_hw(H, W, R, S, stride, pad)
+    M = B * Ho * Wo
+    y = np.full((M, O), np.nan, np.float32)
+    row0, nrows = (0, -1) if rows is None else rows
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    W8 = np.ascontiguousarray(W8, dtype=np.int8)
+    _check(lib().orc_conv2d_w8(_ptr(q), bits, float(sx), B, H, W, C, _ptr(W8), fl, O, R, S,
+                               stride[0], stride[1], pad[0], pad[1], row0, nrows, nthreads, _ptr(y)))
     return y
 
 

@@ -462,4 +462,67 @@ int orc_gemm_dfp(const uint8_t* q, int32_t bits, float sx, int64_t M,
   return ORC_OK;
 }
 
+/* ------------------------------------------------------------------------ */
+/* First layer at 8-bit weights (Sec. 4, 8w-8a)                               */
+/* ------------------------------------------------------------------------ */
+
+int orc_w8_quantize(const float* w, int64_t n, int8_t* W8, int32_t* fl) {
+  if (!w || !W8 || !fl) return ORC_ERR_NULL;
+  if (n < 0) return ORC_ERR_SHAPE;
+  double wmax = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (!isfinite(w[i])) return ORC_ERR_NONFINITE;
+    double a = fabs((double)w[i]);
+    if (a > wmax) wmax = a;
+  }
+  int32_t f = 0;
+  if (wmax > 0.0) {
+    int e;
+    double m = frexp(wmax, &e); /* wmax = m 2^e, m in [0.5, 1) */
+    int ceil_log2 = (m == 0.5) ? e - 1 : e;
+    f = 8 - (ceil_log2 + 1);
+  }
+  for (int64_t i = 0; i < n; ++i) {
+    double v = wmax > 0.0 ? nearbyint(ldexp((double)w[i], f)) : 0.0;
+    if (v > 127.0) v = 127.0;
+    if (v < -128.0) v = -128.0;
+    W8[i] = (int8_t)v;
+  }
+  *fl = f;
+  return ORC_OK;
+}
+
+int orc_conv2d_w8(const uint8_t* q, int32_t bits, float sx, int64_t B,
+                  int64_t H, int64_t W, int64_t C, const int8_t* W8,
+                  int32_t fl, int64_t O, int32_t R, int32_t S, int32_t sh,
+                  int32_t sw, int32_t ph, int32_t pw, int64_t row0,
+                  int64_t nrows, int32_t nthreads, float* y) {
+  if (!q || !W8 || !y) return ORC_ERR_NULL;
+  if (bits != 8 && bits != 4) return ORC_ERR_BITS;
+  geom_t g;
+  int rc = conv_geom(B, H, W, C, O, R, S, sh, sw, ph, pw, &g);
+  if (rc) return rc;
+  const int64_t M = g.B * g.Ho * g.Wo;
+  if (nrows < 0) {
+    row0 = 0;
+    nrows = M;
+  }
+  if (row0 < 0 || row0 + nrows > M) return ORC_ERR_SHAPE;
+  const double scale = (double)sx * ldexp(1.0, -fl);
+  const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 16) num_threads(nt)
+  for (int64_t m = row0; m < row0 + nrows; ++m) {
+    for (int64_t o = 0; o < O; ++o) {
+      int64_t acc = 0;
+      for (int64_t c = 0; c < C; ++c)
+        for (int32_t r = 0; r < R; ++r)
+          for (int32_t s = 0; s < S; ++s)
+            acc += (int64_t)W8[((o * C + c) * R + r) * S + s] *
+                   (int64_t)conv_a(q, bits, &g, m, ((int64_t)r * S + s) * C + c);
+      y[m * O + o] = (float)((double)acc * scale);
+    }
+  }
+  return ORC_OK;
+}
+
 int orc_max_threads(void) { return omp_get_max_threads(); }

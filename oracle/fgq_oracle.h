@@ -28,6 +28,9 @@
  *                     experimental setup).
  *   orc_conv2d_dfp    the layer with those scales: an exact integer sum of
  *   orc_gemm_dfp      (A_g t_k) q_k and one scaling by s_x 2^-fl (Sec. 4).
+ *   orc_w8_quantize   the first layer kept at 8-bit weights (Sec. 4, 8w-8a):
+ *   orc_conv2d_w8     weights as an 8-bit dynamic fixed point, one exponent
+ *                     per layer, and that layer computed the same way.
  *
  * Parity status: ternarize, quantize, group sums, conv2d and gemm are pinned
  * by the tests (brute-force enumeration, Lemma 1 statistics, closed forms,
@@ -128,6 +131,22 @@ int orc_conv2d_dfp(const uint8_t* q, int32_t bits, float sx, int64_t B,
 int orc_gemm_dfp(const uint8_t* q, int32_t bits, float sx, int64_t M,
                  int64_t K, const uint8_t* codes, const int8_t* A, int32_t fl,
                  int64_t O, int32_t G, int32_t nthreads, float* y);
+
+/* Sec. 4 (first layer at 8w-8a): w[0..n) quantized to a signed 8-bit
+ * dynamic fixed point with one fractional length for the layer.  With wmax
+ * the largest |w|: il = ceil(log2 wmax) + 1, fl = 8 - il,
+ * W8[i] = clamp(rint(w[i] * 2^fl), -128, 127); wmax = 0: fl = 0, W8 = 0.
+ * ORC_ERR_NONFINITE for NaN or Inf. */
+int orc_w8_quantize(const float* w, int64_t n, int8_t* W8, int32_t* fl);
+
+/* y[m][o] = fp32( double(S) * (double(s_x) * 2^-fl) ) with the exact integer
+ * S = sum_{c,r,s} W8[o][c][r][s] * a[m][(r*S + s)*C + c] (W8 in the weights'
+ * [O][C][R][S] order); rows as in orc_conv2d. */
+int orc_conv2d_w8(const uint8_t* q, int32_t bits, float sx, int64_t B,
+                  int64_t H, int64_t W, int64_t C, const int8_t* W8,
+                  int32_t fl, int64_t O, int32_t R, int32_t S, int32_t sh,
+                  int32_t sw, int32_t ph, int32_t pw, int64_t row0,
+                  int64_t nrows, int32_t nthreads, float* y);
 
 int orc_max_threads(void);
 

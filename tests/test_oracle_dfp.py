@@ -132,3 +132,63 @@ def test_conv_dfp_exact_rational():
             exact = Fraction(float(sx)) * int(Ssum[o, m]) / Fraction(2) ** fl
             assert abs(int(Ssum[o, m])) < 2 ** 29
             assert np.float32(float(exact)) == y[m, o]
+
+
+# ---------------------------------------------------------------------------
+# First layer at 8-bit weights (Sec. 4: 8w-8a)
+# ---------------------------------------------------------------------------
+
+def w8_examples():
+    rows = []
+    for line in open(os.path.join(HERE, "golden", "w8_weight_examples.txt")):
+        line = line.strip()
+        if not line or line.startswith("#"):
+            continue
+        ws, fl, W8 = (f.strip() for f in line.split(";"))
+        rows.append(([float(v) for v in ws.split()], int(fl), [int(v) for v in W8.split()]))
+    return rows
+
+
+@pytest.mark.parametrize("ws,fl,W8", w8_examples())
+def test_w8_worked_examples(ws, fl, W8):
+    got, got_fl = oracle.w8_quantize(np.array(ws, np.float32))
+    assert got_fl == fl
+    assert got.tolist() == W8
+
+
+def test_w8_properties():
+    w = fi.he_weights(64, 4, 7, 7, "w8-props")
+    W8, fl = oracle.w8_quantize(w)
+    scale = Fraction(2) ** fl
+    wmax = Fraction(float(np.abs(w).max()))
+    assert Fraction(64) < wmax * scale <= Fraction(128)
+    for a, code in zip(w.ravel(), W8.ravel()):
+        v = Fraction(float(a)) * scale
+        if -128 < code < 127:
+            assert abs(v - int(code)) <= Fraction(1, 2)
+    with pytest.raises(oracle.OracleError):
+        oracle.w8_quantize(np.array([0.1, np.inf], np.float32))
+
+
+@pytest.mark.parametrize("case", [(2, 15, 15, 4, 16, 7, 7, 2, 3, 8), (2, 9, 7, 16, 12, 3, 3, 1, 1, 4),
+                                  (1, 8, 8, 3, 8, 3, 3, 2, 1, 8)])
+def test_conv_w8_equals_integer_convolution(case):
+    """S from a float64 library convolution of the integer weights and codes
+    (every partial sum is an integer below 2^53, so exact), then the output
+    formula evaluated with exact rationals."""
+    B, H, W, C, O, R, S, st, pd, bits = case
+    w = fi.he_weights(O, C, R, S, "w8-lib", case)
+    x = fi.relu_gauss((B, H, W, C), "w8-lib", case)
+    W8, fl = oracle.w8_quantize(w)
+    q, sx = oracle.quantize_act(x, bits)
+    y = oracle.conv2d_w8(q, bits, sx, x.shape, W8, fl, O, R, S, (st, st), (pd, pd))
+    n = B * H * W * C
+    qv = q[:n].astype(np.int64) if bits == 8 else np.stack([q & 15, q >> 4], 1).ravel()[:n].astype(np.int64)
+    xin = torch.from_numpy(qv.reshape(B, H, W, C).transpose(0, 3, 1, 2).astype(np.float64))
+    Sint = F.conv2d(xin, torch.from_numpy(W8.astype(np.float64)), stride=st, padding=pd)
+    Sint = Sint.permute(0, 2, 3, 1).reshape(-1, O).numpy()
+    assert np.all(np.abs(Sint) < 2 ** 29)
+    for m in range(0, Sint.shape[0], max(1, Sint.shape[0] // 40)):
+        for o in range(O):
+            exact = Fraction(float(sx)) * int(round(Sint[m, o])) / Fraction(2) ** fl
+            assert np.float32(float(exact)) == y[m, o]
