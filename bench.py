@@ -268,7 +268,8 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
     (fgq_conv2d_q, `bits`-bit codes, static scale from one fp32 output): a
     chain of such layers needs one fgq_quantize_act, for the network input.
     Finally each layer runs as the paper's own pipeline (Sec. 4): 8-bit
-    fixed-point group scales (fgq_conv2d_dfp) with the fused output codes."""
+    fixed-point group scales (fgq_conv2d_dfp) with the fused output codes,
+    and conv1 at 8-bit weights (fgq_conv2d_w8)."""
     layers = []
     tot = dict(conv_us=0.0, quant_us=0.0, fused_us=0.0, dfp_us=0.0, ops=0.0, roof_us=0.0, bytes=0.0,
                first_quant_us=0.0)
@@ -284,6 +285,8 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
         K = R * S * C
         prep = fgq.fgq_prepare_weights(codes, alpha, O, K, g)
         prep_dfp = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, g, 8)
+        # the paper keeps the first layer at 8-bit weights (8w-8a)
+        prep_w8 = fgq.fgq_prepare_weights_w8(torch.from_numpy(w).cuda()) if L["name"] == "conv1" else None
         n = B * H * W * C
         Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
         M = B * Ho * Wo
@@ -316,8 +319,12 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
 
         def conv_dfp_q(i):
             x, q, sx, ws, y = sets[i]
-            fgq.fgq_conv2d_dfp(q, bits, sx, (B, H, W, C), codes, prep_dfp, O, R, S, st, pd, g, bits, out_scale,
-                               out=q_outs[i])
+            if prep_w8 is not None:
+                fgq.fgq_conv2d_w8(q, bits, sx, (B, H, W, C), prep_w8, O, R, S, st, pd, bits, out_scale,
+                                  out=q_outs[i])
+            else:
+                fgq.fgq_conv2d_dfp(q, bits, sx, (B, H, W, C), codes, prep_dfp, O, R, S, st, pd, g, bits,
+                                   out_scale, out=q_outs[i])
 
         def graph(fn):
             gr = torch.cuda.CUDAGraph()
@@ -362,7 +369,7 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
         tot["ops"] += count * ops
         tot["roof_us"] += count * roof_us
         tot["bytes"] += count * nbytes
-        del sets, q_outs, gq, gc, gf, gd, prep, prep_dfp, codes, alpha
+        del sets, q_outs, gq, gc, gf, gd, prep, prep_dfp, prep_w8, codes, alpha
         torch.cuda.empty_cache()
     return {"workload": f"ResNet-{depth} conv stack, batch {batch}, G={G}, u{bits} (conv1 at G=4)",
             "layers_total": sum(c for _, c in stack_layers(fi, depth, batch)), "distinct": len(layers),

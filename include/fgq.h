@@ -64,7 +64,8 @@ enum {
   FGQ_ERR_GROUP = 3,       /* G < 1 or G does not divide C (or K) */
   FGQ_ERR_BITS = 4,        /* bits not 8|4, or odd C / n with bits=4 */
   FGQ_ERR_NONFINITE = 5,   /* fgq_ternarize met NaN or Inf weights (the
-                              fixed-point calls: NaN, Inf or negative alpha) */
+                              fixed-point calls: NaN, Inf or negative alpha;
+                              the 8-bit weights: NaN or Inf) */
   FGQ_ERR_HIP = 6,         /* HIP runtime error (also: no device) */
   FGQ_ERR_UNSUPPORTED = 7, /* method or path not available for the shape */
   FGQ_ERR_WORKSPACE = 8    /* workspace missing or too small */
@@ -293,6 +294,35 @@ fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx,
                         const void* prepared, int64_t O, int32_t G,
                         int32_t out_bits, const float* out_scale, void* out,
                         void* stream);
+
+/*
+ * First layer at 8-bit weights (Sec. 4 keeps the first layer at 8w-8a).
+ *
+ * fgq_prepare_weights_w8 -- the weights w (fp32 [O][C][R][S]) as a signed
+ * 8-bit dynamic fixed point with one fractional length for the layer: with
+ * wmax = max |w|, fl = 8 - (ceil(log2 wmax) + 1), W8 = clamp(rint(w * 2^fl),
+ * -128, 127) (ties to even; wmax = 0 gives fl = 0), stored in the layout of
+ * fgq_prepare_weights_dfp.  prepared: fgq_prepared_bytes_w8(O, C, R, S)
+ * bytes, 256-byte aligned.  Synchronizes `stream`; FGQ_ERR_NONFINITE if a
+ * weight is NaN or Inf.
+ *
+ * fgq_conv2d_w8 -- y = fp32( double(S) * (double(s_x) * 2^-fl) ),
+ * S[m][o] = sum_k W8[o][k] q[m][k] (exact int32), on the one-plane
+ * matrix-core kernel; needs C % 16 == 0 or C = 4, 8 (a first layer with
+ * its 3 image channels padded to 4), q aligned as for fgq_conv2d and
+ * R*S*C <= 65536, else FGQ_ERR_UNSUPPORTED.  out_bits / out_scale / out as
+ * for fgq_conv2d_dfp.
+ */
+size_t fgq_prepared_bytes_w8(int64_t O, int64_t C, int32_t R, int32_t S);
+fgq_status fgq_prepare_weights_w8(const float* w, int64_t O, int64_t C,
+                                  int32_t R, int32_t S, void* prepared,
+                                  size_t prepared_bytes, void* stream);
+fgq_status fgq_conv2d_w8(const uint8_t* q, int32_t bits, const float* sx,
+                         int64_t B, int64_t H, int64_t W, int64_t C,
+                         const void* prepared, int64_t O, int32_t R, int32_t S,
+                         int32_t stride_h, int32_t stride_w, int32_t pad_h,
+                         int32_t pad_w, int32_t out_bits,
+                         const float* out_scale, void* out, void* stream);
 
 /*
  * fgq_group_sums -- the exact integer group sums P[m][o][g] (Sec. 4: 32-bit

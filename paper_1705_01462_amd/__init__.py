@@ -60,6 +60,10 @@ _SIGS = {
     "fgq_conv2d_dfp": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _I64, _I32, _I32, _I32,
                         _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
     "fgq_gemm_dfp": ([_P, _I32, _P, _I64, _I64, _P, _P, _I64, _I32, _I32, _P, _P, _P], _I32),
+    "fgq_prepared_bytes_w8": ([_I64, _I64, _I32, _I32], _SZ),
+    "fgq_prepare_weights_w8": ([_P, _I64, _I64, _I32, _I32, _P, _SZ, _P], _I32),
+    "fgq_conv2d_w8": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _I64, _I32, _I32, _I32, _I32,
+                       _I32, _I32, _I32, _P, _P, _P], _I32),
 }
 
 
@@ -295,6 +299,34 @@ def fgq_gemm_dfp(q, bits, sx, M, K, codes, prepared, O, G, out_bits=0, out_scale
                             None if out_scale is None else _dev(out_scale, torch.float32, "out_scale"),
                             ctypes.c_void_p(out.data_ptr()), _stream())
     _check(rc, "fgq_gemm_dfp")
+    return out
+
+
+def fgq_prepare_weights_w8(w, prepared=None):
+    """First layer at 8-bit weights: w fp32 [O][C][R][S] -> opaque uint8 buffer."""
+    O, C, R, S = w.shape
+    nb = int(lib().fgq_prepared_bytes_w8(O, C, R, S))
+    if prepared is None:
+        prepared = torch.empty(nb, dtype=torch.uint8, device=w.device)
+    if prepared.data_ptr() % 256:
+        raise ValueError("prepared buffer must be 256-byte aligned")
+    rc = lib().fgq_prepare_weights_w8(_dev(w, torch.float32, "w"), O, C, R, S,
+                                      ctypes.c_void_p(prepared.data_ptr()), nb, _stream())
+    _check(rc, "fgq_prepare_weights_w8")
+    return prepared
+
+
+def fgq_conv2d_w8(q, bits, sx, shape, prepared, O, R, S, stride, pad, out_bits=0, out_scale=None, out=None):
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv_out_hw(H, W, R, S, (sh, sw), (ph, pw))
+    out = _dfp_out((B, Ho, Wo), O, out_bits, q.device, out)
+    rc = lib().fgq_conv2d_w8(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), B, H, W, C,
+                             _dev(prepared, torch.uint8, "prepared"), O, R, S, sh, sw, ph, pw, out_bits,
+                             None if out_scale is None else _dev(out_scale, torch.float32, "out_scale"),
+                             ctypes.c_void_p(out.data_ptr()), _stream())
+    _check(rc, "fgq_conv2d_w8")
     return out
 
 

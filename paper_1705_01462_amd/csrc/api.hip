@@ -312,6 +312,45 @@ fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx, int64_t
   return run_layer_dfp(q, sx, codes, prepared, g, lo, stream);
 }
 
+size_t fgq_prepared_bytes_w8(int64_t O, int64_t C, int32_t R, int32_t S) {
+  if (O < 1 || C < 1 || R < 1 || S < 1) return 0;
+  return static_cast<size_t>(prepared_layout_dfp(O, C * R * S, static_cast<int32_t>(C)).total);
+}
+
+fgq_status fgq_prepare_weights_w8(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
+                                  void* prepared, size_t prepared_bytes, void* stream) {
+  if (!w || !prepared) return FGQ_ERR_NULL;
+  if (O < 1 || C < 1 || R < 1 || S < 1) return FGQ_ERR_SHAPE;
+  if (O > (1LL << 31) || C * R * S > (1LL << 31)) return FGQ_ERR_SHAPE;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  if (prepared_bytes < fgq_prepared_bytes_w8(O, C, R, S)) return FGQ_ERR_WORKSPACE;
+  hipStream_t st = as_stream(stream);
+  fgq_status rc = launch_prepare_w8(w, O, C, R, S, prepared, st);
+  if (rc != FGQ_OK) return rc;
+  int32_t host = 0;
+  FGQ_TRY_HIP(hipMemcpyAsync(&host, prepared, sizeof(host), hipMemcpyDeviceToHost, st));
+  FGQ_TRY_HIP(hipStreamSynchronize(st));
+  return host == INT32_MIN ? FGQ_ERR_NONFINITE : FGQ_OK;
+}
+
+fgq_status fgq_conv2d_w8(const uint8_t* q, int32_t bits, const float* sx, int64_t B, int64_t H,
+                         int64_t W, int64_t C, const void* prepared, int64_t O, int32_t R,
+                         int32_t S, int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,
+                         int32_t out_bits, const float* out_scale, void* out, void* stream) {
+  if (!q || !sx || !prepared || !out) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  // one group per tap (G = C): the layout does not depend on the grouping
+  if (!conv_geom(B, H, W, C, O, R, S, stride_h, stride_w, pad_h, pad_w, static_cast<int32_t>(C), bits,
+                 &g, &err))
+    return err;
+  LayerOut lo;
+  if (!layer_out(out_bits, out_scale, out, O, &lo, &err)) return err;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  if (!fold_dfp_supported(g, q)) return FGQ_ERR_UNSUPPORTED;
+  return launch_fold_dfp_conv(q, sx, prepared, g, lo, as_stream(stream));
+}
+
 fgq_status fgq_group_sums(const uint8_t* q, int32_t bits, int64_t B, int64_t H, int64_t W,
                           int64_t C, const uint8_t* codes, int64_t O, int32_t R, int32_t S,
                           int32_t stride_h, int32_t stride_w, int32_t pad_h, int32_t pad_w,

@@ -14,6 +14,12 @@
 // |S| < 2^29.  The planes are written in the folded kernel's fragment order
 // with one plane, plus the uint8 offset term 128 * sum_k w' and the
 // dequantized scales A * 2^-fl for the direct kernel.
+//
+// First layer at 8-bit weights (Sec. 4 keeps it at 8w-8a): the weights
+// themselves as a signed 8-bit dynamic fixed point with one fractional
+// length, fl = 8 - (ceil(log2 max|w|) + 1), W8 = clamp(rint(w * 2^fl),
+// -128, 127), in the same prepared layout (W8 as the plane); the layer is
+// then computed exactly like the fixed-point-scale layer.
 #include <limits.h>
 
 #include "fgq_internal.h"
@@ -42,8 +48,9 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kExpThreads = 1024;
 
-// One workgroup: the largest alpha, then fl (INT32_MIN if any alpha is NaN,
-// Inf or negative).
+// One workgroup: the largest alpha (kSigned: the largest |w|), then fl
+// (INT32_MIN if a value is NaN or Inf, or, for scales, negative).
+template <bool kSigned>
 __global__ __launch_bounds__(kExpThreads) void dfp_exponent_kernel(const float* __restrict__ alpha,
                                                                    int64_t n, int32_t bits,
                                                                    int32_t* __restrict__ fl) {
@@ -52,8 +59,8 @@ __global__ __launch_bounds__(kExpThreads) void dfp_exponent_kernel(const float* 
   float amax = 0.0f;
   int bad = 0;
   for (int64_t i = threadIdx.x; i < n; i += kExpThreads) {
-    const float a = alpha[i];
-    bad |= !(a >= 0.0f && a < __builtin_huge_valf());  // NaN, Inf or negative
+    const float a = kSigned ? fabsf(alpha[i]) : alpha[i];
+    bad |= !(a >= 0.0f && a < __builtin_huge_valf());  // NaN, Inf or (scales) negative
     amax = fmaxf(amax, a);
   }
   for (int off = 32; off > 0; off >>= 1) {
@@ -147,11 +154,63 @@ __global__ __launch_bounds__(kThreads) void prepare_dfp_kernel(
   }
 }
 
+// First layer at 8-bit weights: one block per channel of the padded range;
+// w is [O][C][R][S], k = (r*S + s)*C + c.
+__global__ __launch_bounds__(kThreads) void prepare_w8_kernel(
+    const float* __restrict__ w, int64_t O, int64_t C, int32_t R, int32_t S, int64_t Kp,
+    const int32_t* __restrict__ flp, int8_t* __restrict__ planes, int32_t* __restrict__ bias) {
+  __shared__ int64_t red[kThreads / 64];
+  const int64_t o = blockIdx.x;
+  const int64_t nks = Kp / kFoldKStep;
+  const int64_t K = C * R * S;
+  const int32_t fl = *flp;
+  if (o >= O || fl == INT_MIN) {
+    for (int64_t k = threadIdx.x; k < Kp; k += kThreads) planes[frag_offset1(nks, o, k)] = 0;
+    return;
+  }
+  int64_t s = 0;
+  for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
+    int v = 0;
+    if (k < K) {
+      const int64_t c = k % C, rs = k / C;
+      const int64_t sx = rs % S, r = rs / S;
+      double d = rint(ldexp(static_cast<double>(w[((o * C + c) * R + r) * S + sx]), fl));
+      d = d > 127.0 ? 127.0 : (d < -128.0 ? -128.0 : d);
+      v = static_cast<int>(d);
+    }
+    planes[frag_offset1(nks, o, k)] = static_cast<int8_t>(v);
+    s += v;
+  }
+  for (int off = 32; off > 0; off >>= 1) s += __shfl_xor(s, off);
+  if (threadIdx.x % 64 == 0) red[threadIdx.x / 64] = s;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    int64_t v = 0;
+    for (int i = 0; i < kThreads / 64; ++i) v += red[i];
+    bias[o] = static_cast<int32_t>(128 * v);
+  }
+}
+
 }  // namespace
+
+fgq_status launch_prepare_w8(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
+                             void* prepared, hipStream_t st) {
+  const int64_t K = C * R * S;
+  const PreparedLayout L = prepared_layout_dfp(O, K, static_cast<int32_t>(C));
+  char* base = static_cast<char*>(prepared);
+  int32_t* fl = reinterpret_cast<int32_t*>(base);
+  hipLaunchKernelGGL(dfp_exponent_kernel<true>, dim3(1), dim3(kExpThreads), 0, st, w, O * K, 8, fl);
+  if (hipGetLastError() != hipSuccess) return FGQ_ERR_HIP;
+  if (L.O32 > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  hipLaunchKernelGGL(prepare_w8_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0, st, w, O,
+                     C, R, S, L.Kp, fl, reinterpret_cast<int8_t*>(base + L.planes_off),
+                     reinterpret_cast<int32_t*>(base + L.bias_off));
+  return last_launch();
+}
 
 fgq_status launch_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A, int32_t* fl,
                             hipStream_t st) {
-  hipLaunchKernelGGL(dfp_exponent_kernel, dim3(1), dim3(kExpThreads), 0, st, alpha, n, bits, fl);
+  hipLaunchKernelGGL(dfp_exponent_kernel<false>, dim3(1), dim3(kExpThreads), 0, st, alpha, n, bits, fl);
   if (hipGetLastError() != hipSuccess) return FGQ_ERR_HIP;
   if (A && n > 0) {
     const int64_t blocks = ceil_div(n, kThreads) < 4096 ? ceil_div(n, kThreads) : 4096;

@@ -104,6 +104,10 @@ fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O,
 // alpha is NaN, Inf or negative) and the codes A (A may be NULL).
 fgq_status launch_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A,
                             int32_t* fl, hipStream_t st);
+// First layer at 8-bit weights: the fixed-point prepared layout (with one
+// group per tap, G = C) with W8 as the plane.
+fgq_status launch_prepare_w8(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
+                             void* prepared, hipStream_t st);
 fgq_status launch_prepare_dfp(const uint8_t* codes, const float* alpha, int64_t O,
                               int64_t K, int32_t G, int32_t alpha_bits, void* prepared,
                               hipStream_t st);

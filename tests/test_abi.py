@@ -28,7 +28,8 @@ def test_library_exports_every_declared_symbol():
     # the binding wraps every entry point under the same name
     for n in ("fgq_ternarize", "fgq_quantize_act", "fgq_prepare_weights", "fgq_conv2d",
               "fgq_gemm", "fgq_group_sums", "fgq_conv2d_q", "fgq_gemm_q", "fgq_dfp_alpha",
-              "fgq_prepare_weights_dfp", "fgq_conv2d_dfp", "fgq_gemm_dfp"):
+              "fgq_prepare_weights_dfp", "fgq_conv2d_dfp", "fgq_gemm_dfp",
+              "fgq_prepare_weights_w8", "fgq_conv2d_w8"):
         assert callable(getattr(fgq, n))
 
 
@@ -119,6 +120,24 @@ def test_dfp_validation():
     assert conv(0, 16, None, None) == 1                            # prepared required
     assert conv(0, 16, None, ctypes.c_void_p(0x1001)) == 8         # prepared alignment
     assert L.fgq_gemm_dfp(P, 8, P, 4, 16, P, P, 16, 5, 0, None, P, None) == 3
+
+
+def test_prepared_bytes_w8():
+    L = fgq.lib()
+    # the fixed-point layout with one group per tap: header, plane, bias, R*S scales per channel
+    assert L.fgq_prepared_bytes_w8(64, 4, 7, 7) == L.fgq_prepared_bytes_dfp(64, 196, 4)
+    assert L.fgq_prepared_bytes_w8(0, 4, 7, 7) == 0
+
+
+@no_device
+def test_w8_validation():
+    L = fgq.lib()
+    assert L.fgq_prepare_weights_w8(None, 64, 4, 7, 7, P, 1 << 20, None) == 1
+    assert L.fgq_prepare_weights_w8(P, 64, 4, 7, 7, P, 16, None) == 8
+    assert L.fgq_prepare_weights_w8(P, 64, 0, 7, 7, P, 1 << 20, None) == 2
+    conv = lambda ob, sc: L.fgq_conv2d_w8(P, 8, P, 2, 8, 8, 16, P, 16, 3, 3, 1, 1, 1, 1, ob, sc, P, None)
+    assert conv(5, P) == 4
+    assert conv(8, None) == 1
 
 
 @no_device

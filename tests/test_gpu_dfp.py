@@ -164,3 +164,48 @@ def test_benchmark_layer_dfp_sampled_rows(G):
         y_ref = oracle.conv2d_dfp(ref["q"], 8, ref["s"], shape, ref["codes"], ref["A"], ref["fl"], O, R, S,
                                   (1, 1), (1, 1), G, rows=(row0, 128))[row0:row0 + 128]
         np.testing.assert_array_equal(y[row0:row0 + 128].view(np.uint32), y_ref.view(np.uint32))
+
+
+# ---------------------------------------------------------------------------
+# First layer at 8-bit weights (Sec. 4: 8w-8a)
+# ---------------------------------------------------------------------------
+
+W8_CASES = [
+    # B, H, W, C, O, R, S, stride, pad, bits
+    (2, 23, 23, 4, 64, 7, 7, 2, 3, 8),      # ResNet conv1 shape, image padded to 4 channels
+    (2, 9, 7, 16, 24, 3, 3, 1, 1, 8),
+    (2, 11, 11, 8, 33, 5, 5, 1, 2, 4),      # tiny C = 8, uint4 input, odd O
+    (1, 10, 10, 64, 96, 1, 1, 2, 0, 8),
+]
+
+
+@pytest.mark.parametrize("case", W8_CASES)
+def test_conv2d_w8_bit_exact(case):
+    B, H, W, C, O, R, S, st, pd, bits = case
+    w = fi.he_weights(O, C, R, S, "gpu-w8", case)
+    x = fi.relu_gauss((B, H, W, C), "gpu-w8", case)
+    prep = fgq.fgq_prepare_weights_w8(dev(w))
+    q, sx = fgq.fgq_quantize_act(dev(x), bits)
+    y = host(fgq.fgq_conv2d_w8(q, bits, sx, x.shape, prep, O, R, S, st, pd)).reshape(-1, O)
+    W8, fl = oracle.w8_quantize(w)
+    qr, sr = oracle.quantize_act(x, bits)
+    y_ref = oracle.conv2d_w8(qr, bits, sr, x.shape, W8, fl, O, R, S, (st, st), (pd, pd))
+    np.testing.assert_array_equal(y.view(np.uint32), y_ref.view(np.uint32))
+    if O % 2 == 0:
+        s_out = np.float32(0.7 * float(y_ref.max()) / 255)
+        got = host(fgq.fgq_conv2d_w8(q, bits, sx, x.shape, prep, O, R, S, st, pd, 8,
+                                     dev(np.array([s_out], np.float32)))).ravel()
+        np.testing.assert_array_equal(got, oracle.quantize_act(y_ref.ravel(), 8, s_out)[0])
+
+
+def test_conv2d_w8_unsupported_and_bad_weights():
+    w = fi.he_weights(8, 3, 3, 3, "gpu-w8-c3")
+    prep = fgq.fgq_prepare_weights_w8(dev(w))
+    q, sx = fgq.fgq_quantize_act(dev(fi.relu_gauss((1, 6, 6, 3), "gpu-w8-c3")), 8)
+    with pytest.raises(fgq.FgqError) as e:
+        fgq.fgq_conv2d_w8(q, 8, sx, (1, 6, 6, 3), prep, 8, 3, 3, 1, 1)
+    assert e.value.code == 7
+    w[3, 1, 2, 0] = np.nan
+    with pytest.raises(fgq.FgqError) as e:
+        fgq.fgq_prepare_weights_w8(dev(w))
+    assert e.value.code == 5
