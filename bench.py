@@ -388,6 +388,98 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
             "per_layer": layers}
 
 
+def alexnet_measure(torch, fgq, fi, batch=64, G=4, bits=8, nsets=3, reps=10):
+    """The AlexNet-shaped layers at batch `batch`, G=4, uint8: each layer timed
+    at its full shape (graph replays over rotating sets) two ways: ternary
+    weights with fp32 group scales and fp32 output (fgq_conv2d; the
+    fully-connected layers, M = batch, through fgq_gemm_ws with split K),
+    and the paper's pipeline (conv1 at 8-bit weights, the others with 8-bit
+    fixed-point scales, fused 8-bit outputs; fgq_conv2d_w8 / fgq_conv2d_dfp /
+    fgq_gemm_dfp_ws)."""
+    layers, tot = [], dict(fp=0.0, paper=0.0, ops=0.0, roof=0.0)
+    gen = torch.Generator(device="cuda")
+    for li, L in enumerate(fi.alexnet_layers(batch)):
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        st, pd = L["stride"], L["pad"]
+        fc = H == 1 and W == 1 and R == 1 and S == 1
+        w = fi.he_weights(O, C, R, S, "alexnet-bench", L["name"])
+        if L["name"] == "conv1":
+            w[:, 3:] = 0.0
+        codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
+        K = R * S * C
+        prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+        prep_dfp = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, G, 8)
+        prep_w8 = fgq.fgq_prepare_weights_w8(torch.from_numpy(w).cuda()) if L["name"] == "conv1" else None
+        Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
+        M = B * Ho * Wo
+        ws = torch.empty(max(fgq.fgq_gemm_ws_bytes(M, K, O, G), 4), dtype=torch.uint8, device="cuda")
+        wsd = torch.empty(max(fgq.fgq_gemm_ws_bytes(M, K, O, G, True), 4), dtype=torch.uint8, device="cuda")
+        gen.manual_seed(fi.SEED + 7000 + li)
+        sets = []
+        for _ in range(nsets):
+            x = torch.randn(B * H * W * C, generator=gen, device="cuda").clamp_(min=0.0)
+            if L["name"] == "conv1":
+                x.view(B, H, W, C)[..., 3:] = 0.0
+            q, sx = fgq.fgq_quantize_act(x, bits)
+            y = torch.empty((M, O), dtype=torch.float32, device="cuda")
+            qo = torch.empty(M * O, dtype=torch.uint8, device="cuda")
+            sets.append((q, sx, y, qo))
+        out_scale = torch.ones(1, dtype=torch.float32, device="cuda")
+
+        def plain(i):
+            q, sx, y, qo = sets[i]
+            if fc:
+                fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep, out=y, ws=ws)
+            else:
+                fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, G, prepared=prep,
+                               y=y.view(B, Ho, Wo, O))
+
+        def paper(i):
+            q, sx, y, qo = sets[i]
+            if prep_w8 is not None:
+                fgq.fgq_conv2d_w8(q, bits, sx, (B, H, W, C), prep_w8, O, R, S, st, pd, 8, out_scale, out=qo)
+            elif fc:
+                fgq.fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prep_dfp, O, G, 8, out_scale, out=qo, ws=wsd)
+            else:
+                fgq.fgq_conv2d_dfp(q, bits, sx, (B, H, W, C), codes, prep_dfp, O, R, S, st, pd, G, 8, out_scale,
+                                   out=qo)
+
+        for i in range(nsets):
+            plain(i)
+        out_scale.fill_(float(sets[0][2].max()) / 255)
+        times = []
+        for fn in (plain, paper):
+            for i in range(nsets):
+                fn(i)
+            torch.cuda.synchronize()
+            gr = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(gr):
+                for i in range(nsets):
+                    fn(i)
+            gr.replay()
+            _, ms = time_graphs(torch, [(gr, reps)])
+            times.append(ms * 1e3 / (reps * nsets))
+        k_true = R * S * (3 if L["name"] == "conv1" else C)
+        ops = 2.0 * M * O * k_true
+        nbytes = B * H * W * C + O * K // 4 + 4 * O * K // G + 4 * M * O
+        roof_us = max(ops / (INT8_PEAK_TOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+        layers.append([L["name"], round(times[0], 2), round(roof_us / times[0], 3), round(times[1], 2)])
+        tot["fp"] += times[0]
+        tot["paper"] += times[1]
+        tot["ops"] += ops
+        tot["roof"] += roof_us
+        del sets, prep, prep_dfp, prep_w8, ws, wsd, codes, alpha
+        torch.cuda.empty_cache()
+    return {"workload": f"AlexNet-shaped layers, batch {batch}, G={G}, u{bits} (conv1 channels padded to 4; "
+                        "fully-connected layers as GEMMs with split K)",
+            "sum_us": round(tot["fp"], 1), "effective_tops": round(tot["ops"] / (tot["fp"] * 1e-6) / 1e12, 1),
+            "sum_roofline_us": round(tot["roof"], 1), "roofline_frac": round(tot["roof"] / tot["fp"], 4),
+            "sum_paper_pipeline_us": round(tot["paper"], 1),
+            "effective_tops_paper_pipeline": round(tot["ops"] / (tot["paper"] * 1e-6) / 1e12, 1),
+            "per_layer_columns": ["layer", "us", "roofline_frac", "paper_pipeline_us"],
+            "per_layer": layers}
+
+
 def gemm_measure(torch, fgq, fi, M=64, K=256, O=128, G=4, bits=8, nsets=8, reps=50):
     """Latency of the single FGQ GEMM (M=64, K=256, O=128, W ~ N(0, 0.05^2),
     G=4, uint8): a launch-latency-bound size, reported in microseconds."""
@@ -619,6 +711,11 @@ def main():
             log(f"[bench] ResNet-{depth} stack, G={G}, u{sbits}")
             out["stacks"][f"resnet{depth}_b64_g{G}_u{sbits}"] = stack_measure(torch, fgq, fi, depth, G, sbits)
             log(f"[bench] ResNet-{depth}: sum conv {out['stacks'][f'resnet{depth}_b64_g{G}_u{sbits}']['sum_conv_us']} us")
+    if not args.no_stacks:
+        log("[bench] AlexNet-shaped layers, batch 64, G=4, u8")
+        out["alexnet_b64_g4_u8"] = alexnet_measure(torch, fgq, fi)
+        log(f"[bench] AlexNet: sum {out['alexnet_b64_g4_u8']['sum_us']} us, "
+            f"paper pipeline {out['alexnet_b64_g4_u8']['sum_paper_pipeline_us']} us")
     if not args.no_cpu:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(fi, LAYER, 4, bits)

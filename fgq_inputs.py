@@ -86,3 +86,19 @@ def resnet_convs(depth, batch):
             H = Ho
     layers.append(dict(name="fc", B=batch, H=1, W=1, C=2048, O=1000, R=1, S=1, stride=1, pad=0))
     return layers
+
+
+def alexnet_layers(batch):
+    """AlexNet shapes (single tower, 227x227 input; the 3 image channels
+    zero-padded to 4; pooling between layers is not part of the FGQ layer).
+    The fully-connected layers are GEMMs with M = batch."""
+    return [
+        dict(name="conv1", B=batch, H=227, W=227, C=4, O=96, R=11, S=11, stride=4, pad=0),
+        dict(name="conv2", B=batch, H=27, W=27, C=96, O=256, R=5, S=5, stride=1, pad=2),
+        dict(name="conv3", B=batch, H=13, W=13, C=256, O=384, R=3, S=3, stride=1, pad=1),
+        dict(name="conv4", B=batch, H=13, W=13, C=384, O=384, R=3, S=3, stride=1, pad=1),
+        dict(name="conv5", B=batch, H=13, W=13, C=384, O=256, R=3, S=3, stride=1, pad=1),
+        dict(name="fc6", B=batch, H=1, W=1, C=9216, O=4096, R=1, S=1, stride=1, pad=0),
+        dict(name="fc7", B=batch, H=1, W=1, C=4096, O=4096, R=1, S=1, stride=1, pad=0),
+        dict(name="fc8", B=batch, H=1, W=1, C=4096, O=1000, R=1, S=1, stride=1, pad=0),
+    ]

@@ -296,6 +296,39 @@ fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx,
                         void* stream);
 
 /*
+ * GEMMs with split K, for fully-connected layers at small batch (few rows,
+ * long K: the rows and channels alone would occupy few compute units).
+ *
+ * fgq_gemm_ws / fgq_gemm_dfp_ws -- the same results as fgq_gemm (or
+ * fgq_gemm_q, by out_bits) and fgq_gemm_dfp, bit for bit: when the
+ * matrix-core kernel runs (prepared given, shape as for fgq_gemm, and for
+ * fgq_gemm_ws the folded layout, i.e. G != 64 or K/64 > 160), the K steps
+ * are divided among workgroups that write their int32 sums to `ws`, and a
+ * second kernel adds them in a fixed order and applies the usual epilogue.
+ *   out_bits / out_scale / out  as for fgq_conv2d_dfp
+ *   ws        [tmp] device buffer of fgq_gemm_ws_bytes(M, K, O, G,
+ *                   fixed_point) bytes (4-byte aligned; fixed_point = 1
+ *                   for fgq_gemm_dfp_ws), not kept between calls; may be
+ *                   NULL when that size is 0 (K is then not split).
+ * FGQ_ERR_WORKSPACE if a needed workspace is missing or too small.  The
+ * split depends on the device's compute-unit count: query the size on the
+ * device that runs the call.
+ */
+size_t fgq_gemm_ws_bytes(int64_t M, int64_t K, int64_t O, int32_t G,
+                         int32_t fixed_point);
+fgq_status fgq_gemm_ws(const uint8_t* q, int32_t bits, const float* sx,
+                       int64_t M, int64_t K, const uint8_t* codes,
+                       const float* alpha, const void* prepared, int64_t O,
+                       int32_t G, int32_t out_bits, const float* out_scale,
+                       void* out, void* ws, size_t ws_bytes, void* stream);
+fgq_status fgq_gemm_dfp_ws(const uint8_t* q, int32_t bits, const float* sx,
+                           int64_t M, int64_t K, const uint8_t* codes,
+                           const void* prepared, int64_t O, int32_t G,
+                           int32_t out_bits, const float* out_scale,
+                           void* out, void* ws, size_t ws_bytes,
+                           void* stream);
+
+/*
  * First layer at 8-bit weights (Sec. 4 keeps the first layer at 8w-8a).
  *
  * fgq_prepare_weights_w8 -- the weights w (fp32 [O][C][R][S]) as a signed

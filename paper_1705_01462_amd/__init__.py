@@ -60,6 +60,9 @@ _SIGS = {
     "fgq_conv2d_dfp": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _I64, _I32, _I32, _I32,
                         _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
     "fgq_gemm_dfp": ([_P, _I32, _P, _I64, _I64, _P, _P, _I64, _I32, _I32, _P, _P, _P], _I32),
+    "fgq_gemm_ws_bytes": ([_I64, _I64, _I64, _I32, _I32], _SZ),
+    "fgq_gemm_ws": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
+    "fgq_gemm_dfp_ws": ([_P, _I32, _P, _I64, _I64, _P, _P, _I64, _I32, _I32, _P, _P, _P, _SZ, _P], _I32),
     "fgq_prepared_bytes_w8": ([_I64, _I64, _I32, _I32], _SZ),
     "fgq_prepare_weights_w8": ([_P, _I64, _I64, _I32, _I32, _P, _SZ, _P], _I32),
     "fgq_conv2d_w8": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _I64, _I32, _I32, _I32, _I32,
@@ -299,6 +302,47 @@ def fgq_gemm_dfp(q, bits, sx, M, K, codes, prepared, O, G, out_bits=0, out_scale
                             None if out_scale is None else _dev(out_scale, torch.float32, "out_scale"),
                             ctypes.c_void_p(out.data_ptr()), _stream())
     _check(rc, "fgq_gemm_dfp")
+    return out
+
+
+def fgq_gemm_ws_bytes(M, K, O, G, fixed_point=False):
+    return int(lib().fgq_gemm_ws_bytes(M, K, O, G, 1 if fixed_point else 0))
+
+
+def _ws_for(M, K, O, G, fixed_point, device, ws):
+    nb = fgq_gemm_ws_bytes(M, K, O, G, fixed_point)
+    if ws is None and nb:
+        ws = torch.empty(nb, dtype=torch.uint8, device=device)
+    return ws, nb
+
+
+def fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=None, out_bits=0, out_scale=None, out=None,
+                ws=None):
+    """fgq_gemm / fgq_gemm_q with K split over workgroups when that helps."""
+    out = _dfp_out((M,), O, out_bits, q.device, out)
+    ws, nb = _ws_for(M, K, O, G, False, q.device, ws)
+    rc = lib().fgq_gemm_ws(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), M, K,
+                           _dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                           None if prepared is None else _dev(prepared, torch.uint8, "prepared"), O, G, out_bits,
+                           None if out_scale is None else _dev(out_scale, torch.float32, "out_scale"),
+                           ctypes.c_void_p(out.data_ptr()),
+                           None if ws is None else ctypes.c_void_p(ws.data_ptr()),
+                           ws.numel() if ws is not None else 0, _stream())
+    _check(rc, "fgq_gemm_ws")
+    return out
+
+
+def fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prepared, O, G, out_bits=0, out_scale=None, out=None, ws=None):
+    """fgq_gemm_dfp with K split over workgroups when that helps."""
+    out = _dfp_out((M,), O, out_bits, q.device, out)
+    ws, nb = _ws_for(M, K, O, G, True, q.device, ws)
+    rc = lib().fgq_gemm_dfp_ws(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), M, K,
+                               _dev(codes, torch.uint8, "codes"), _dev(prepared, torch.uint8, "prepared"), O, G,
+                               out_bits, None if out_scale is None else _dev(out_scale, torch.float32, "out_scale"),
+                               ctypes.c_void_p(out.data_ptr()),
+                               None if ws is None else ctypes.c_void_p(ws.data_ptr()),
+                               ws.numel() if ws is not None else 0, _stream())
+    _check(rc, "fgq_gemm_dfp_ws")
     return out
 
 

@@ -312,6 +312,63 @@ fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx, int64_t
   return run_layer_dfp(q, sx, codes, prepared, g, lo, stream);
 }
 
+size_t fgq_gemm_ws_bytes(int64_t M, int64_t K, int64_t O, int32_t G, int32_t fixed_point) {
+  if (M < 1 || K < 1 || O < 1 || G < 1 || K % G != 0 || K > kFoldMaxK) return 0;
+  if (!fixed_point && prepared_layout(O, K, G).kind != kPrepFold) return 0;
+  int32_t sps = 0;
+  const int32_t splits = splitk_splits(M, K, O, &sps);
+  if (splits <= 1) return 0;
+  return static_cast<size_t>(splits) * (fixed_point ? 1 : 3) * static_cast<size_t>(M * O) * 4;
+}
+
+fgq_status fgq_gemm_ws(const uint8_t* q, int32_t bits, const float* sx, int64_t M, int64_t K,
+                       const uint8_t* codes, const float* alpha, const void* prepared, int64_t O,
+                       int32_t G, int32_t out_bits, const float* out_scale, void* out, void* ws,
+                       size_t ws_bytes, void* stream) {
+  if (!q || !sx || !codes || !alpha || !out) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(1, M, 1, K, O, 1, 1, 1, 1, 0, 0, G, bits, &g, &err)) return err;
+  LayerOut lo;
+  if (!layer_out(out_bits, out_scale, out, O, &lo, &err)) return err;
+  if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  if (prepared && prepared_layout(O, K, G).kind == kPrepFold && fold_supported(g, q)) {
+    int32_t sps = 0;
+    const int32_t splits = splitk_splits(M, K, O, &sps);
+    if (splits > 1) {
+      if (!ws || reinterpret_cast<uintptr_t>(ws) % 4 != 0 || ws_bytes < fgq_gemm_ws_bytes(M, K, O, G, 0))
+        return FGQ_ERR_WORKSPACE;
+      return launch_fold_splitk(q, sx, prepared, g, lo, splits, sps, static_cast<int32_t*>(ws),
+                                as_stream(stream));
+    }
+  }
+  return run_layer(q, sx, codes, alpha, prepared, g, lo, stream);
+}
+
+fgq_status fgq_gemm_dfp_ws(const uint8_t* q, int32_t bits, const float* sx, int64_t M, int64_t K,
+                           const uint8_t* codes, const void* prepared, int64_t O, int32_t G,
+                           int32_t out_bits, const float* out_scale, void* out, void* ws,
+                           size_t ws_bytes, void* stream) {
+  if (!q || !sx || !codes || !prepared || !out) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(1, M, 1, K, O, 1, 1, 1, 1, 0, 0, G, bits, &g, &err)) return err;
+  LayerOut lo;
+  if (!layer_out(out_bits, out_scale, out, O, &lo, &err)) return err;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  if (fold_dfp_supported(g, q)) {
+    int32_t sps = 0;
+    const int32_t splits = splitk_splits(M, K, O, &sps);
+    if (splits > 1) {
+      if (!ws || reinterpret_cast<uintptr_t>(ws) % 4 != 0 || ws_bytes < fgq_gemm_ws_bytes(M, K, O, G, 1))
+        return FGQ_ERR_WORKSPACE;
+      return launch_fold_dfp_splitk(q, sx, prepared, g, lo, splits, sps, static_cast<int32_t*>(ws),
+                                    as_stream(stream));
+    }
+  }
+  return run_layer_dfp(q, sx, codes, prepared, g, lo, stream);
+}
+
 size_t fgq_prepared_bytes_w8(int64_t O, int64_t C, int32_t R, int32_t S) {
   if (O < 1 || C < 1 || R < 1 || S < 1) return 0;
   return static_cast<size_t>(prepared_layout_dfp(O, C * R * S, static_cast<int32_t>(C)).total);

@@ -122,6 +122,19 @@ bool fold_dfp_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_fold_dfp_conv(const uint8_t* q, const float* sx,
                                 const void* prepared, const ConvGeom& g, const LayerOut& out,
                                 hipStream_t st);
+// Split K for the folded kernels (splitk.hip): the number of splits for an
+// M x K x O product (1: none) and its steps per split; the split launches
+// write int32 sums to ws [splits][planes][M][O] and reduce them into `out`.
+int32_t splitk_splits(int64_t M, int64_t K, int64_t O, int32_t* steps_per_split);
+fgq_status launch_fold_splitk(const uint8_t* q, const float* sx, const void* prepared, const ConvGeom& g,
+                              const LayerOut& out, int32_t splits, int32_t steps_per_split, int32_t* ws,
+                              hipStream_t st);
+fgq_status launch_fold_dfp_splitk(const uint8_t* q, const float* sx, const void* prepared, const ConvGeom& g,
+                                  const LayerOut& out, int32_t splits, int32_t steps_per_split, int32_t* ws,
+                                  hipStream_t st);
+fgq_status launch_splitk_reduce(const int32_t* part, int32_t splits, bool dfp, int64_t M, int64_t O,
+                                const float* sx, const float* scale, const int32_t* fl, const LayerOut& out,
+                                hipStream_t st);
 // Per-group int8 MFMA kernel with an fp32 alpha epilogue (G = 64).
 bool group_supported(const ConvGeom& g, const uint8_t* q);
 fgq_status launch_group_conv(const uint8_t* q, const float* sx,

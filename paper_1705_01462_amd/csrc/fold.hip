@@ -24,6 +24,9 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.qo = out.q;
   a.oscale = out.scale;
   a.fl = nullptr;
+  a.part = nullptr;
+  a.splits = 1;
+  a.steps_per_split = 1 << 30;
   a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
@@ -35,5 +38,31 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
 }
 
 fgq_status launch_fold_out_f32(const FoldArgs& a, int bits, hipStream_t st) { return launch_out<0>(a, bits, st); }
+
+fgq_status launch_fold_splitk(const uint8_t* q, const float* sx, const void* prepared, const ConvGeom& g,
+                              const LayerOut& out, int32_t splits, int32_t steps_per_split, int32_t* ws,
+                              hipStream_t st) {
+  const PreparedLayout L = prepared_layout(g.O, g.K, g.G);
+  const char* base = static_cast<const char*>(prepared);
+  FoldArgs a;
+  ig::fill_act_args(g, q, &a.x);
+  a.sx = sx;
+  a.planes = reinterpret_cast<const int8_t*>(base + L.planes_off);
+  a.bias = reinterpret_cast<const int32_t*>(base + L.bias_off);
+  a.scale = reinterpret_cast<const float*>(base + L.scale_off);
+  a.y = nullptr;
+  a.qo = nullptr;
+  a.oscale = nullptr;
+  a.fl = nullptr;
+  a.part = ws;
+  a.splits = splits;
+  a.steps_per_split = steps_per_split;
+  a.staged = 0;
+  a.nks = static_cast<int32_t>(L.nks);
+  a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
+  fgq_status rc = launch_fold_part(a, g.bits, st);
+  if (rc != FGQ_OK) return rc;
+  return launch_splitk_reduce(ws, splits, /*dfp=*/false, g.M, g.O, sx, a.scale, nullptr, out, st);
+}
 
 }  // namespace fgq

@@ -64,6 +64,8 @@ struct FoldArgs {
   uint8_t* qo;           // output codes (kOut 8 or 4)
   const float* oscale;   // their scale
   const int32_t* fl;     // fixed-point scales: fractional length (prepared header)
+  int32_t* part;         // split K (kOut 1): int32 sums [splits][planes][M][O]
+  int32_t splits, steps_per_split;  // K steps [split*sps, min(nk, (split+1)*sps)) per workgroup
   int32_t staged;        // epilogue through LDS (epi_staged)
   int32_t nks, planes_bytes;
 };
@@ -75,6 +77,8 @@ fgq_status launch_fold_out_q4(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_f32(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q4(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_part(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_dfp_part(const FoldArgs& a, int bits, hipStream_t st);
 
 namespace {
 
@@ -94,7 +98,10 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   const int tid = threadIdx.x;
   const int lane = tid % 64, wave = tid / 64;
   const int wo = wave % kNWO, wm = wave / kNWO;
-  const int tile = xcd_swizzle(blockIdx.x, a.x.n_otiles * a.x.n_mtiles);
+  // Workgroups of one K split are numbered together (they share activations).
+  const int ntiles = a.x.n_otiles * a.x.n_mtiles;
+  const int tsplit = xcd_swizzle(blockIdx.x, ntiles * a.splits);
+  const int split = tsplit / ntiles, tile = tsplit % ntiles;
   const int o0 = (tile % a.x.n_otiles) * kTO + 32 * wo;  // this wave's first channel
   const int m0 = (tile / a.x.n_otiles) * kTM;             // workgroup's first row
 
@@ -108,9 +115,11 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   constexpr int kTileB = kPlanes * 2 * 1024;   // bytes of one channel tile, one 64-wide K block
   const int wbase = (o0 / 32) * a.nks * kTileB + 16 * lane;
 
-  const int nk = (a.x.K + kKT - 1) / kKT;
+  const int nk_all = (a.x.K + kKT - 1) / kKT;
+  const int ks0 = split * a.steps_per_split;  // this workgroup's K steps [ks0, nk)
+  const int nk = ks0 + a.steps_per_split < nk_all ? ks0 + a.steps_per_split : nk_all;
   Stager xs;
-  xs.init(a.x, m0, tid);
+  xs.init(a.x, m0, tid, ks0);
 
   // A step covers two 64-wide fragment blocks (K quarters hq = 2*blk + h).
   // The step is the scalar offset, which the buffer range check does not
@@ -139,7 +148,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
     const int oc = o0 + lane % 32;
 #pragma unroll
     for (int j = 0; j < kPlanes; ++j) {
-      const int bj = (kBits == 8 && oc < a.x.O) ? a.bias[j * a.x.O + oc] : 0;
+      const int bj = (kBits == 8 && oc < a.x.O && ks0 == 0) ? a.bias[j * a.x.O + oc] : 0;
       v16i init;
 #pragma unroll
       for (int r = 0; r < 16; ++r) init[r] = bj;
@@ -227,11 +236,11 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   };
   using I0 = std::integral_constant<int, 0>;
   using I1 = std::integral_constant<int, 1>;
-  load_w(I0{}, 0);
+  load_w(I0{}, ks0);
   xs.load(a.x);
   xs.store(lds, 0x80808080u);
   __syncthreads();
-  int ks = 0;
+  int ks = ks0;
   for (; ks + 2 <= nk; ks += 2) {
     step(I0{}, ks);
     step(I1{}, ks + 1);
@@ -240,33 +249,49 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 
   // ---- epilogue: lane holds rows m of channel o.
   const int o = o0 + lane % 32;
-  const float sx = *a.sx;
-  // locals: a byte store may alias anything, including the argument block
-  const OutPtrs out{a.y, a.qo, a.x.M, a.x.O};
-  const bool staged = a.staged != 0;
-  auto emit = [&](auto val) {
-    with_out_scale<kOut>(a.oscale, [&](const QScale& qs, auto rcp) {
-      constexpr bool kR = decltype(rcp)::value;
-      if (staged)
-        store_staged<kOut, kNWO, kNB, kR>(lds, out, qs, m0, o0 - 32 * wo, wm, wo, tid, val);
-      else
-        store_direct<kOut, kNB, kR>(out, qs, m0 + wm * kNB * 32, o, lane, val);
-    });
-  };
-  if constexpr (kDfp) {
-    // y = fp32(double(S) * (double(s_x) * 2^-fl)); the scale is exact.
-    const int32_t fl = *a.fl;  // INT32_MIN marks rejected scales (never negated)
-    const double cd = fl > -2048 && fl < 2048 ? static_cast<double>(sx) * ldexp(1.0, -fl) : 0.0;
-    emit([&](int c, int r) { return static_cast<float>(static_cast<double>(acc[0][c][r]) * cd); });
+  if constexpr (kOut == 1) {
+    // split K: this split's raw integer sums, [split][plane][m][o]
+    int32_t* const part = a.part;
+    const int M = a.x.M, O = a.x.O;
+    if (o >= O) return;
+#pragma unroll
+    for (int j = 0; j < kPlanes; ++j)
+#pragma unroll
+      for (int c = 0; c < kNB; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + wm * kNB * 32 + 32 * c + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
+          if (m < M) part[(static_cast<int64_t>(split * kPlanes + j) * M + m) * O + o] = acc[j][c][r];
+        }
   } else {
-    const float c0 = o < a.x.O ? sx * a.scale[o] : 0.0f;
-    const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
-    emit([&](int c, int r) {
-      const float f2 = static_cast<float>(acc[2 % kPlanes][c][r]);
-      const float f1 = static_cast<float>(acc[1 % kPlanes][c][r]);
-      const float f0 = static_cast<float>(acc[0][c][r]);
-      return fmaf(f2, c2, fmaf(f1, c1, f0 * c0));
-    });
+    const float sx = *a.sx;
+    // locals: a byte store may alias anything, including the argument block
+    const OutPtrs out{a.y, a.qo, a.x.M, a.x.O};
+    const bool staged = a.staged != 0;
+    auto emit = [&](auto val) {
+      with_out_scale<kOut>(a.oscale, [&](const QScale& qs, auto rcp) {
+        constexpr bool kR = decltype(rcp)::value;
+        if (staged)
+          store_staged<kOut, kNWO, kNB, kR>(lds, out, qs, m0, o0 - 32 * wo, wm, wo, tid, val);
+        else
+          store_direct<kOut, kNB, kR>(out, qs, m0 + wm * kNB * 32, o, lane, val);
+      });
+    };
+    if constexpr (kDfp) {
+      // y = fp32(double(S) * (double(s_x) * 2^-fl)); the scale is exact.
+      const int32_t fl = *a.fl;  // INT32_MIN marks rejected scales (never negated)
+      const double cd = fl > -2048 && fl < 2048 ? static_cast<double>(sx) * ldexp(1.0, -fl) : 0.0;
+      emit([&](int c, int r) { return static_cast<float>(static_cast<double>(acc[0][c][r]) * cd); });
+    } else {
+      const float c0 = o < a.x.O ? sx * a.scale[o] : 0.0f;
+      const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
+      emit([&](int c, int r) {
+        const float f2 = static_cast<float>(acc[2 % kPlanes][c][r]);
+        const float f1 = static_cast<float>(acc[1 % kPlanes][c][r]);
+        const float f0 = static_cast<float>(acc[0][c][r]);
+        return fmaf(f2, c2, fmaf(f1, c1, f0 * c0));
+      });
+    }
   }
 }
 
@@ -276,7 +301,7 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   FoldArgs a = a0;
   a.x.n_otiles = (a.x.O + kTO - 1) / kTO;
   a.x.n_mtiles = (a.x.M + kTM - 1) / kTM;
-  const int64_t n = static_cast<int64_t>(a.x.n_otiles) * a.x.n_mtiles;
+  const int64_t n = static_cast<int64_t>(a.x.n_otiles) * a.x.n_mtiles * a.splits;
   if (n > 0x7fffffffLL) return FGQ_ERR_SHAPE;
   const dim3 grid(static_cast<uint32_t>(n));
   switch (c_mode(a.x.C)) {

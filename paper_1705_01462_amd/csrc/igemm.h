@@ -89,8 +89,9 @@ struct ActStager {
   __amdgpu_buffer_rsrc_t rs;
 
   // Piece p = tid + 256*i is row p/kSlots of the tile, k-slot
-  // 16*(p%kSlots) = 16*(tid%kSlots) of every step.
-  __device__ void init(const ActArgs& a, int m0, int tid) {
+  // 16*(p%kSlots) = 16*(tid%kSlots) of every step; the tap state starts at
+  // step ks0.
+  __device__ void init(const ActArgs& a, int m0, int tid, int ks0 = 0) {
     rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
 #pragma unroll
     for (int i = 0; i < kXP; ++i) {
@@ -107,7 +108,7 @@ struct ActStager {
       rowbase[i] = (b * a.H + hi0[i]) * a.W + wi0[i];
       xlds[i] = lds_off(p / kSlots, p % kSlots);
     }
-    tk = 16 * (tid % kSlots);
+    tk = 16 * (tid % kSlots) + ks0 * kKT;
     const int rsi = tk / a.C;
     tc = tk - rsi * a.C;
     ts = rsi % a.S;
@@ -189,7 +190,7 @@ struct ActStagerTinyC {
   uint32_t part[kXP][kSub][kC * kBits / 32 > 0 ? kC * kBits / 32 : 1];
   __amdgpu_buffer_rsrc_t rs;
 
-  __device__ void init(const ActArgs& a, int m0, int tid) {
+  __device__ void init(const ActArgs& a, int m0, int tid, int ks0 = 0) {
     rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
 #pragma unroll
     for (int i = 0; i < kXP; ++i) {
@@ -206,7 +207,7 @@ struct ActStagerTinyC {
       rowbase[i] = (b * a.H + hi0[i]) * a.W + wi0[i];
       xlds[i] = lds_off(p / kSlots, p % kSlots);
     }
-    tk = 16 * (tid % kSlots);
+    tk = 16 * (tid % kSlots) + ks0 * kKT;
   }
 
   __device__ void advance(const ActArgs&) { tk += kKT; }

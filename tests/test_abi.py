@@ -29,7 +29,7 @@ def test_library_exports_every_declared_symbol():
     for n in ("fgq_ternarize", "fgq_quantize_act", "fgq_prepare_weights", "fgq_conv2d",
               "fgq_gemm", "fgq_group_sums", "fgq_conv2d_q", "fgq_gemm_q", "fgq_dfp_alpha",
               "fgq_prepare_weights_dfp", "fgq_conv2d_dfp", "fgq_gemm_dfp",
-              "fgq_prepare_weights_w8", "fgq_conv2d_w8"):
+              "fgq_prepare_weights_w8", "fgq_conv2d_w8", "fgq_gemm_ws", "fgq_gemm_dfp_ws"):
         assert callable(getattr(fgq, n))
 
 
@@ -120,6 +120,19 @@ def test_dfp_validation():
     assert conv(0, 16, None, None) == 1                            # prepared required
     assert conv(0, 16, None, ctypes.c_void_p(0x1001)) == 8         # prepared alignment
     assert L.fgq_gemm_dfp(P, 8, P, 4, 16, P, P, 16, 5, 0, None, P, None) == 3
+
+
+def test_gemm_ws_bytes():
+    L = fgq.lib()
+    # no device here: 256 compute units assumed.  fc6 at batch 64: 32 channel
+    # tiles of 128; splits capped so the int32 sums stay within a quarter of
+    # the weight bytes: min(512/32, 72/2, 9216/(16*64)) = 9 -> 8 steps each, 9 splits
+    assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 4, 0) == 9 * 3 * 64 * 4096 * 4
+    assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 4, 1) == 9 * 1 * 64 * 4096 * 4
+    assert L.fgq_gemm_ws_bytes(64, 256, 128, 4, 0) == 0          # too few steps
+    assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 64, 0) == 0        # per-group layout: no split
+    assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 64, 1) > 0
+    assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 5, 0) == 0         # G does not divide K
 
 
 def test_prepared_bytes_w8():

@@ -95,3 +95,73 @@ def test_stack_layer_sampled_rows(depth, G, bits, L):
                                prepared=prep)
     q_two, _ = fgq.fgq_quantize_act(y_dev, bits, scale_in=s_out)
     assert torch.equal(q_fused.reshape(-1), q_two), "fused quantization differs from conv + quantize"
+
+
+# ---------------------------------------------------------------------------
+# AlexNet-shaped layers (batch 64, G = 4, uint8): conv layers on sampled row
+# ranges, fully-connected layers (M = 64 GEMMs with split K) on every row;
+# ternary weights with fp32 scales within the layer tolerance, and the
+# paper's pipeline (conv1 at 8-bit weights, fixed-point scales elsewhere)
+# bit-exact.
+# ---------------------------------------------------------------------------
+
+ALEX = fi.alexnet_layers(64)
+
+
+@pytest.mark.parametrize("L", ALEX, ids=[L["name"] for L in ALEX])
+def test_alexnet_layer(L):
+    B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+    st, pd, G, bits = L["stride"], L["pad"], 4, 8
+    fc = H == 1 and W == 1
+    print(f"[alexnet] {L['name']} B={B} {H}x{W} C={C} O={O} {R}x{S}/{st}", flush=True)
+    w = fi.he_weights(O, C, R, S, "alexnet", L["name"])
+    x = fi.relu_gauss((B, H, W, C), "alexnet", L["name"])
+    if L["name"] == "conv1":
+        w[:, 3:] = 0.0
+        x[..., 3:] = 0.0
+    codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
+    q, sx = fgq.fgq_quantize_act(torch.from_numpy(x).cuda(), bits)
+    K = R * S * C
+    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+    Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
+    M = B * Ho * Wo
+    if fc:
+        y = fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep)
+    else:
+        y = fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, G, prepared=prep)
+    yh = y.cpu().numpy().reshape(-1, O)
+
+    t, a, _ = oracle.ternarize(w, G)
+    codes_ref = oracle.pack_codes(t)
+    q_ref, s_ref = oracle.quantize_act(x, bits)
+    n = min(ROWS, M)
+    ranges = [(0, M)] if fc else sorted({(0, n), (M // 2 - n // 2, n), (M - n, n)})
+    for row0, nr in ranges:
+        y_ref = oracle.conv2d(q_ref, bits, s_ref, x.shape, codes_ref, a, O, R, S, (st, st), (pd, pd), G,
+                              rows=(row0, nr))[row0:row0 + nr]
+        P = oracle.group_sums_conv(q_ref, bits, x.shape, codes_ref, O, R, S, (st, st), (pd, pd), G,
+                                   row0, nr).astype(np.float64)
+        mag = float(s_ref) * np.einsum("mog,og->mo", np.abs(P), a.astype(np.float64))
+        err = np.abs(yh[row0:row0 + nr].astype(np.float64) - y_ref.astype(np.float64))
+        assert not (err > TOL * mag).any(), f"{L['name']}: rows [{row0}, {row0 + nr}) beyond tolerance"
+
+    # the paper's pipeline: bit-exact with the oracle
+    if L["name"] == "conv1":
+        prep8 = fgq.fgq_prepare_weights_w8(torch.from_numpy(w).cuda())
+        yp = fgq.fgq_conv2d_w8(q, bits, sx, (B, H, W, C), prep8, O, R, S, st, pd)
+        W8, fl = oracle.w8_quantize(w)
+        ref = lambda r0, nr: oracle.conv2d_w8(q_ref, bits, s_ref, x.shape, W8, fl, O, R, S, (st, st), (pd, pd),
+                                              rows=(r0, nr))
+    else:
+        prepd = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, G, 8)
+        if fc:
+            yp = fgq.fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prepd, O, G)
+        else:
+            yp = fgq.fgq_conv2d_dfp(q, bits, sx, (B, H, W, C), codes, prepd, O, R, S, st, pd, G)
+        A, fl = oracle.dfp_alpha(a, 8)
+        ref = lambda r0, nr: oracle.conv2d_dfp(q_ref, bits, s_ref, x.shape, codes_ref, A, fl, O, R, S, (st, st),
+                                               (pd, pd), G, rows=(r0, nr))
+    yp = yp.cpu().numpy().reshape(-1, O)
+    for row0, nr in ranges:
+        np.testing.assert_array_equal(yp[row0:row0 + nr].view(np.uint32),
+                                      ref(row0, nr)[row0:row0 + nr].view(np.uint32))
