@@ -313,28 +313,14 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   return last_launch();
 }
 
-// Rows per wave (kNB blocks of 32): the busiest compute unit does
-// ceil(tiles / CUs) workgroups of kNB blocks per SIMD; among equal costs
-// the smaller kNB wins (kNB = 2 runs two workgroups per compute unit).
+// Rows per wave: two 32-row blocks (kNB = 2) for every shape.  Measured on
+// the benchmark and network layers, 32-row tiles (more weight traffic per
+// matrix instruction) and 128-row tiles (one workgroup per compute unit,
+// and register spills in the per-group kernel) were slower, and a tile
+// count balance of ceil(tiles / CUs) * kNB never prefers kNB = 4 over 2.
 template <int kOut, bool kDfp, int kBits, int kNWO>
 fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
-  constexpr int kNWM = 4 / kNWO;
-  const int64_t otiles = ceil_div(a.x.O, 32 * kNWO);
-  int best = 2;
-  int64_t best_cost = -1;
-  for (int nb = 2; nb <= 4; ++nb) {
-    const int64_t tiles = otiles * ceil_div(a.x.M, kNWM * nb * 32);
-    const int64_t cost = ceil_div(tiles, device_cus()) * nb;
-    if (best_cost < 0 || cost < best_cost) {
-      best_cost = cost;
-      best = nb;
-    }
-  }
-  switch (best) {
-    case 2: return launch_cfg<kOut, kDfp, kBits, kNWO, 2>(a, st);
-    case 3: return launch_cfg<kOut, kDfp, kBits, kNWO, 3>(a, st);
-    default: return launch_cfg<kOut, kDfp, kBits, kNWO, 4>(a, st);
-  }
+  return launch_cfg<kOut, kDfp, kBits, kNWO, 2>(a, st);
 }
 
 template <int kOut, bool kDfp, int kBits>

@@ -317,17 +317,6 @@ inline int device_cus() {
   return cached[dev];
 }
 
-// Dynamic LDS to request so that a grid of `blocks` workgroups, each with
-// `static_lds` bytes of LDS, runs one workgroup per compute unit when it
-// fits in one round: two co-resident workgroups would share every SIMD and
-// both run at half speed while other compute units idle.
-inline size_t spread_lds(int64_t blocks, size_t static_lds) {
-  constexpr size_t kLdsPerCu = 160 * 1024;
-  if (blocks > device_cus()) return 0;
-  const size_t want = kLdsPerCu / 2 + 1024;
-  return want > static_lds ? want - static_lds : 0;
-}
-
 inline int c_mode(int64_t C) { return C % 16 == 0 ? (C >= kKT ? 0 : 1) : static_cast<int>(C); }
 
 }  // namespace ig
