@@ -256,8 +256,8 @@ fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx,
  *
  * fgq_prepare_weights_dfp -- the constants of the layer with those scales:
  * the int8 weights A[o][g(k)] * t[o][k] (one plane, the folded kernel's
- * operand order), their uint8 offset term, fl, and the dequantized scales.
- * 1 byte per weight plus 4 per group.  prepared: device buffer of
+ * operand order), their uint8 offset term, fl, the dequantized scales and
+ * the codes A.  1 byte per weight plus 5 per group.  prepared: device buffer of
  * fgq_prepared_bytes_dfp(O, K, G) bytes, 256-byte aligned, opaque.
  * Synchronizes `stream`; FGQ_ERR_NONFINITE as for fgq_dfp_alpha.
  *
@@ -305,6 +305,8 @@ fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx,
  * fgq_gemm_ws the folded layout, i.e. G != 64 or K/64 > 160), the K steps
  * are divided among workgroups that write their int32 sums to `ws`, and a
  * second kernel adds them in a fixed order and applies the usual epilogue.
+ * fgq_gemm_dfp_ws with G in {4, 8, 16, 32, 64, 128} reads the weights as
+ * the 2-bit codes and the scale codes A and expands them in registers.
  *   out_bits / out_scale / out  as for fgq_conv2d_dfp
  *   ws        [tmp] device buffer of fgq_gemm_ws_bytes(M, K, O, G,
  *                   fixed_point) bytes (4-byte aligned; fixed_point = 1

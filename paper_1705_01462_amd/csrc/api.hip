@@ -3,6 +3,7 @@
 // stream.  No allocation, no hidden device state.
 #include <stdlib.h>
 
+#include <algorithm>
 #include <vector>
 
 #include "fgq_internal.h"
@@ -316,8 +317,9 @@ size_t fgq_gemm_ws_bytes(int64_t M, int64_t K, int64_t O, int32_t G, int32_t fix
   if (M < 1 || K < 1 || O < 1 || G < 1 || K % G != 0 || K > kFoldMaxK) return 0;
   if (!fixed_point && prepared_layout(O, K, G).kind != kPrepFold) return 0;
   int32_t sps = 0;
-  const int32_t splits = splitk_splits(M, K, O, &sps);
-  if (splits <= 1) return 0;
+  int32_t splits = splitk_splits(M, K, O, &sps);
+  if (splits <= 1) splits = 0;
+  if (fixed_point && dfpx_shape_ok(M, K, O, G)) splits = std::max(splits, dfpx_splits(M, K, O, G, &sps));
   return static_cast<size_t>(splits) * (fixed_point ? 1 : 3) * static_cast<size_t>(M * O) * 4;
 }
 
@@ -356,12 +358,16 @@ fgq_status fgq_gemm_dfp_ws(const uint8_t* q, int32_t bits, const float* sx, int6
   LayerOut lo;
   if (!layer_out(out_bits, out_scale, out, O, &lo, &err)) return err;
   if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  const bool ws_ok = ws && reinterpret_cast<uintptr_t>(ws) % 4 == 0 && ws_bytes >= fgq_gemm_ws_bytes(M, K, O, G, 1);
+  if (dfpx_supported(g, q)) {  // weights read as codes + scale codes
+    if (!ws_ok) return FGQ_ERR_WORKSPACE;
+    return launch_dfpx_splitk(q, sx, codes, prepared, g, lo, static_cast<int32_t*>(ws), as_stream(stream));
+  }
   if (fold_dfp_supported(g, q)) {
     int32_t sps = 0;
     const int32_t splits = splitk_splits(M, K, O, &sps);
     if (splits > 1) {
-      if (!ws || reinterpret_cast<uintptr_t>(ws) % 4 != 0 || ws_bytes < fgq_gemm_ws_bytes(M, K, O, G, 1))
-        return FGQ_ERR_WORKSPACE;
+      if (!ws_ok) return FGQ_ERR_WORKSPACE;
       return launch_fold_dfp_splitk(q, sx, prepared, g, lo, splits, sps, static_cast<int32_t*>(ws),
                                     as_stream(stream));
     }

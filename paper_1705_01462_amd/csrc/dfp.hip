@@ -38,7 +38,8 @@ PreparedLayout prepared_layout_dfp(int64_t O, int64_t K, int32_t G) {
   L.planes_off = kDfpHeaderBytes;
   L.bias_off = round_up(L.planes_off + L.O32 * L.Kp, 256);
   L.alpha_off = round_up(L.bias_off + 4 * O, 256);
-  L.total = round_up(L.alpha_off + 4 * O * (K / G), 256);
+  L.acodes_off = round_up(L.alpha_off + 4 * O * (K / G), 256);
+  L.total = round_up(L.acodes_off + O * (K / G), 256);
   L.scale_off = L.total;
   return L;
 }
@@ -119,7 +120,7 @@ __device__ inline int64_t frag_offset1(int64_t nks, int64_t o, int64_t k) {
 __global__ __launch_bounds__(kThreads) void prepare_dfp_kernel(
     const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O, int64_t K,
     int32_t G, int32_t bits, int64_t Kp, const int32_t* __restrict__ flp, int8_t* __restrict__ planes,
-    int32_t* __restrict__ bias, float* __restrict__ alpha_q) {
+    int32_t* __restrict__ bias, float* __restrict__ alpha_q, int8_t* __restrict__ acodes) {
   __shared__ int64_t red[kThreads / 64];
   const int64_t o = blockIdx.x;
   const int64_t nks = Kp / kFoldKStep;
@@ -130,9 +131,11 @@ __global__ __launch_bounds__(kThreads) void prepare_dfp_kernel(
   }
   const int64_t ng = K / G;
   const int64_t rb = ceil_div(K, 4);
-  for (int64_t gi = threadIdx.x; gi < ng; gi += kThreads)
-    alpha_q[o * ng + gi] =
-        static_cast<float>(ldexp(static_cast<double>(dfp_code(alpha[o * ng + gi], fl, bits)), -fl));
+  for (int64_t gi = threadIdx.x; gi < ng; gi += kThreads) {
+    const int A = dfp_code(alpha[o * ng + gi], fl, bits);
+    alpha_q[o * ng + gi] = static_cast<float>(ldexp(static_cast<double>(A), -fl));
+    acodes[o * ng + gi] = static_cast<int8_t>(A);
+  }
   int64_t s = 0;
   for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
     int v = 0;
@@ -232,7 +235,8 @@ fgq_status launch_prepare_dfp(const uint8_t* codes, const float* alpha, int64_t 
                      codes, alpha, O, K, G, alpha_bits, L.Kp, fl,
                      reinterpret_cast<int8_t*>(base + L.planes_off),
                      reinterpret_cast<int32_t*>(base + L.bias_off),
-                     reinterpret_cast<float*>(base + L.alpha_off));
+                     reinterpret_cast<float*>(base + L.alpha_off),
+                     reinterpret_cast<int8_t*>(base + L.acodes_off));
   return last_launch();
 }
 

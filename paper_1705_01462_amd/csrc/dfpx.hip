@@ -1,0 +1,305 @@
+// dfpx.hip -- the GEMM with fixed-point group scales (Sec. 4) for few rows
+// and long K (fully-connected layers at small batch), reading the weights
+// as stored: 2-bit codes and one int8 scale code A per group, expanded to
+// the int8 weights A*t in registers instead of the one-byte-per-weight
+// plane of the prepared layout (0.25 + 1/G bytes per weight).
+//
+// Work split: a workgroup owns 128 channels (a wave each 32), kNB 32-row
+// blocks and up to kSteps 128-wide K steps (split K: int32 sums per split,
+// reduced by splitk_reduce_kernel with the fixed-point epilogue).  Its
+// activation slice (kNB*32 rows x kSteps*128 k) is loaded once and stays in
+// LDS, and every code and scale-code load of the split is issued up front,
+// after the activation loads: the memory counter completes in order, so the
+// publish of the slice waits for the activations only, and step s then
+// waits for its own weights only.  Nothing in the K loop waits for a later
+// load, so the whole split's traffic is in flight at once.
+//
+// Operand order.  Lane l (channel 32*wave + l%32, half hf = l/32) holds, in
+// step s and K quarter h, the 16 weights k = 128*s + 64*hf + 16*h + [0, 16);
+// the activation fragment of the same lane reads the same 16 k of its row
+// from LDS.  So a lane's codes of one step are 16 consecutive bytes of its
+// channel's code row (one load), and its scale codes 64/G consecutive bytes.
+//
+// Expansion of 16 weights (32 bits of codes, weight 4i+b in bits 2b of byte
+// i): per group a byte table [0, A, 0, -A] (-A formed four bytes at a time
+// as (0x80808080 - a) ^ 0x80808080, exact because 0 <= A <= 127), then one
+// byte permute per 4 weights with the four 2-bit codes spread to selector
+// bytes.  Code 2 is never written; its table byte is 0.
+//
+// K tail (K % 128 == 64): activations at k >= K are stored as int8 zero, so
+// whatever the weight loads there return (the next channel's codes, or
+// zeros past the buffer end) adds nothing.  The uint8 offset term covers
+// k < K only, as the 128 * sum of the weights in the prepared bias.
+#include <algorithm>
+
+#include "fgq_internal.h"
+#include "igemm.h"
+
+namespace fgq {
+namespace {
+
+using namespace ig;
+
+constexpr int kSteps = 8;  // K steps per split at most (LDS: kNB * 32 KB)
+
+struct DfpxArgs {
+  const uint8_t* q;       // activations [M][K] (uint8) or [M][K/2] (uint4)
+  const uint8_t* codes;   // [O][K/4]
+  const int8_t* acodes;   // [O][K/G]
+  const int32_t* bias;    // [O]   128 * sum_k A*t (uint8 offset term)
+  int32_t* part;          // [splits][M][O]
+  int32_t M, K, O, n_otiles, n_mtiles, splits, sps, rb, ng;
+  int32_t q_bytes, codes_bytes, acodes_bytes;
+};
+
+template <int kG>
+__device__ inline v4i expand16(uint32_t c32, uint32_t a) {
+  const uint32_t na = (0x80808080u - a) ^ 0x80808080u;  // per byte: -A
+  v4i w;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t j = kG == 4 ? i : (kG == 8 ? i / 2 : 0);  // the A byte of weights 4i..4i+3
+    // table bytes [0, A_j, 0, -A_j]; selector 12 gives a zero byte
+    const uint32_t T = __builtin_amdgcn_perm(na, a, 0x0Cu | (j << 8) | (0x0Cu << 16) | ((4u + j) << 24));
+    const uint32_t c8 = (c32 >> (8 * i)) & 0xFFu;
+    uint32_t s = c8 | (c8 << 6);
+    s = (s | (s << 12)) & 0x03030303u;  // byte b: the code of weight 4i+b
+    w[i] = static_cast<int>(__builtin_amdgcn_perm(0u, T, s));
+  }
+  return w;
+}
+
+// Scale-code bytes of one lane and step: 64/G of them (one for G >= 64).
+template <int kG>
+struct ACodes {
+  static constexpr int kBytes = kG >= 64 ? 1 : 64 / kG;
+  static constexpr int kWords = kBytes >= 4 ? kBytes / 4 : 1;
+  uint32_t w[kWords];
+
+  __device__ void load(__amdgpu_buffer_rsrc_t rs, int off) {
+    if constexpr (kBytes == 16) {
+      const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+      for (int i = 0; i < 4; ++i) w[i] = static_cast<uint32_t>(v[i]);
+    } else if constexpr (kBytes == 8) {
+      const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
+      w[0] = static_cast<uint32_t>(v.x);
+      w[1] = static_cast<uint32_t>(v.y);
+    } else if constexpr (kBytes == 4) {
+      w[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
+    } else if constexpr (kBytes == 2) {
+      w[0] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
+    } else {
+      w[0] = __builtin_amdgcn_raw_buffer_load_b8(rs, off, 0, 0);
+    }
+  }
+  // The A bytes of quarter h (16 weights), placed where expand16<kG> reads
+  // them: four (G = 4), two (G = 8) or one (byte 0).
+  __device__ uint32_t quarter(int h) const {
+    if constexpr (kG == 4) return w[h];
+    else if constexpr (kG == 8) return w[h / 2] >> (16 * (h % 2));
+    else if constexpr (kG == 16) return w[0] >> (8 * h);
+    else if constexpr (kG == 32) return w[0] >> (8 * (h / 2));
+    else return w[0];
+  }
+};
+
+template <int kBits, int kG, int kNB>
+__global__ __launch_bounds__(kThreads, 2) void dfpx_gemm_kernel(DfpxArgs a) {
+  constexpr int kRows = 32 * kNB;
+  constexpr int kStageB = kRows * kRowB;                  // one step's activations
+  constexpr int kXP = kRows * kSteps * kSlots / kThreads;  // 16-k pieces per thread
+  __shared__ __attribute__((aligned(16))) unsigned char lds[kSteps * kStageB];
+
+  const int tid = threadIdx.x;
+  const int lane = tid % 64, wo = tid / 64, hf = lane / 32;
+  const int ntiles = a.n_otiles * a.n_mtiles;
+  const int tsplit = xcd_swizzle(blockIdx.x, ntiles * a.splits);
+  const int split = tsplit / ntiles, tile = tsplit % ntiles;
+  const int oc = (tile % a.n_otiles) * 128 + 32 * wo + lane % 32;  // the lane's channel
+  const int m0 = (tile / a.n_otiles) * kRows;
+  const int nk_all = (a.K + kKT - 1) / kKT;
+  const int ks0 = split * a.sps;
+  const int nsteps = ks0 + a.sps < nk_all ? a.sps : nk_all - ks0;  // 1..kSteps
+  const int k0 = ks0 * kKT;
+
+  // The uint8 offset term of the lane's channel (split 0 only), requested
+  // first so that no wait for it follows the weight loads.
+  const bool ocok = oc < a.O;
+  int bj = 0;
+  if constexpr (kBits == 8) {
+    const __amdgpu_buffer_rsrc_t brs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.bias), 0, 4 * a.O, kBufFlags);
+    bj = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(brs, ocok && ks0 == 0 ? 4 * oc : kOutOfRange, 0, 0));
+  }
+
+  // ---- activation slice: piece p = tid + 256*i is row p / (8*kSteps),
+  // 16-k slot p % (8*kSteps) (a row's slots are consecutive threads, so a
+  // wave reads one contiguous kilobyte of a row).  Rows >= M and steps past
+  // the split read nothing.
+  const __amdgpu_buffer_rsrc_t qrs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
+  typedef typename std::conditional<kBits == 8, v4i, v2i>::type raw_t;
+  raw_t xraw[kXP];
+#pragma unroll
+  for (int i = 0; i < kXP; ++i) {
+    const int p = tid + kThreads * i;
+    const int row = p / (kSlots * kSteps), ksl = p % (kSlots * kSteps);
+    const int m = m0 + row, k = k0 + 16 * ksl;
+    const bool ok = (m < a.M) & (ksl < kSlots * nsteps) & (k < a.K);
+    const uint32_t e = static_cast<uint32_t>(m) * static_cast<uint32_t>(a.K) + static_cast<uint32_t>(k);
+    if constexpr (kBits == 8)
+      xraw[i] = __builtin_amdgcn_raw_buffer_load_b128(qrs, ok ? e : kOutOfRange, 0, 0);
+    else
+      xraw[i] = __builtin_amdgcn_raw_buffer_load_b64(qrs, ok ? e >> 1 : kOutOfRange, 0, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- every weight load of the split.  Steps past the split re-read the
+  // split's last step (in range; never used).  Channels >= O read nothing.
+  const __amdgpu_buffer_rsrc_t crs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.codes), 0, a.codes_bytes, kBufFlags);
+  const __amdgpu_buffer_rsrc_t ars =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.acodes), 0, a.acodes_bytes, kBufFlags);
+  const int cbase = ocok ? oc * a.rb + k0 / 4 + 16 * hf : static_cast<int>(kOutOfRange);
+  const int abase = ocok ? oc * a.ng + (k0 + 64 * hf) / kG : static_cast<int>(kOutOfRange);
+  v4i cw[kSteps];
+  ACodes<kG> aw[kSteps];
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+    const int ss = s < nsteps ? s : nsteps - 1;
+    cw[s] = __builtin_amdgcn_raw_buffer_load_b128(crs, cbase + 32 * ss, 0, 0);
+    aw[s].load(ars, abase + (kKT * ss) / kG);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- publish the slice: uint8 as q - 128 (k >= K as 0), uint4 unpacked
+#pragma unroll
+  for (int i = 0; i < kXP; ++i) {
+    const int p = tid + kThreads * i;
+    const int row = p / (kSlots * kSteps), ksl = p % (kSlots * kSteps);
+    unsigned char* dst = lds + (ksl / kSlots) * kStageB + lds_off(row, ksl % kSlots);
+    v4i v;
+    if constexpr (kBits == 8) {
+      const int x = k0 + 16 * ksl < a.K ? static_cast<int>(0x80808080u) : 0;
+      v = xraw[i];
+      v.x ^= x; v.y ^= x; v.z ^= x; v.w ^= x;
+    } else {
+      v = unpack_u4x16(static_cast<uint32_t>(xraw[i].x), static_cast<uint32_t>(xraw[i].y));
+    }
+    *reinterpret_cast<v4i*>(dst) = v;
+  }
+  __syncthreads();
+
+  v16i acc[kNB];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) acc[c][r] = bj;
+  int afrag[kNB][4];
+#pragma unroll
+  for (int c = 0; c < kNB; ++c)
+#pragma unroll
+    for (int h = 0; h < 4; ++h) afrag[c][h] = lds_off(32 * c + lane % 32, 4 * hf + h);
+
+#pragma unroll
+  for (int s = 0; s < kSteps; ++s) {
+    if (s >= nsteps) break;
+    const unsigned char* base = lds + s * kStageB;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      const v4i wf = expand16<kG>(static_cast<uint32_t>(cw[s][h]), aw[s].quarter(h));
+#pragma unroll
+      for (int c = 0; c < kNB; ++c) {
+        const v4i xf = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+        acc[c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf, wf, acc[c], 0, 0, 0);
+      }
+    }
+  }
+
+  // this split's raw sums, [split][m][o]
+  if (!ocok) return;
+  int32_t* const part = a.part;
+#pragma unroll
+  for (int c = 0; c < kNB; ++c)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
+      if (m < a.M) part[(static_cast<int64_t>(split) * a.M + m) * a.O + oc] = acc[c][r];
+    }
+}
+
+template <int kBits, int kNB>
+fgq_status launch_g(const DfpxArgs& a, int G, hipStream_t st) {
+  const dim3 grid(static_cast<uint32_t>(a.n_otiles * a.n_mtiles * a.splits));
+  switch (G) {
+    case 4: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 4, kNB>), grid, dim3(kThreads), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 8, kNB>), grid, dim3(kThreads), 0, st, a); break;
+    case 16: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 16, kNB>), grid, dim3(kThreads), 0, st, a); break;
+    case 32: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 32, kNB>), grid, dim3(kThreads), 0, st, a); break;
+    case 64: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 64, kNB>), grid, dim3(kThreads), 0, st, a); break;
+    default: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 128, kNB>), grid, dim3(kThreads), 0, st, a); break;
+  }
+  return last_launch();
+}
+
+}  // namespace
+
+bool dfpx_shape_ok(int64_t M, int64_t K, int64_t O, int32_t G) {
+  const bool pow2g = G == 4 || G == 8 || G == 16 || G == 32 || G == 64 || G == 128;
+  return pow2g && M <= kDfpxMaxM && K % 64 == 0 && K <= kFoldMaxK && O * (K / 4) < (1LL << 31) &&
+         M * K < (1LL << 31) && M * O < (1LL << 31);
+}
+
+bool dfpx_supported(const ConvGeom& g, const uint8_t* q) {
+  const uintptr_t align = g.bits == 8 ? 16 : 8;
+  // a 1x1 convolution at stride 1 without padding is the GEMM on [M][K]
+  return g.R == 1 && g.S == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0 &&
+         reinterpret_cast<uintptr_t>(q) % align == 0 &&
+         dfpx_shape_ok(g.M, g.K, g.O, g.G);
+}
+
+int32_t dfpx_splits(int64_t M, int64_t K, int64_t O, int32_t G, int32_t* steps_per_split) {
+  (void)M;
+  (void)O;
+  (void)G;
+  // As many steps per split as the LDS slice holds: a workgroup's loads are
+  // all in flight at once, so its time is about one memory round trip plus
+  // its bytes, and fewer splits mean fewer int32 sums to write and reduce.
+  const int64_t nk = ceil_div(K, 128);
+  const int64_t splits = ceil_div(nk, kSteps);
+  const int64_t sps = ceil_div(nk, splits);
+  *steps_per_split = static_cast<int32_t>(sps);
+  return static_cast<int32_t>(ceil_div(nk, sps));
+}
+
+fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const uint8_t* codes, const void* prepared,
+                              const ConvGeom& g, const LayerOut& out, int32_t* ws, hipStream_t st) {
+  const PreparedLayout L = prepared_layout_dfp(g.O, g.K, g.G);
+  const char* base = static_cast<const char*>(prepared);
+  const int nb = g.M <= 32 ? 1 : 2;
+  DfpxArgs a;
+  a.q = q;
+  a.codes = codes;
+  a.acodes = reinterpret_cast<const int8_t*>(base + L.acodes_off);
+  a.bias = reinterpret_cast<const int32_t*>(base + L.bias_off);
+  a.part = ws;
+  a.M = static_cast<int32_t>(g.M);
+  a.K = static_cast<int32_t>(g.K);
+  a.O = static_cast<int32_t>(g.O);
+  a.n_otiles = static_cast<int32_t>(ceil_div(g.O, 128));
+  a.n_mtiles = static_cast<int32_t>(ceil_div(g.M, 32 * nb));
+  a.splits = dfpx_splits(g.M, g.K, g.O, g.G, &a.sps);
+  a.rb = static_cast<int32_t>(g.K / 4);
+  a.ng = static_cast<int32_t>(g.K / g.G);
+  a.q_bytes = static_cast<int32_t>(g.bits == 8 ? g.M * g.K : g.M * g.K / 2);
+  a.codes_bytes = static_cast<int32_t>(g.O * a.rb);
+  a.acodes_bytes = static_cast<int32_t>(g.O * a.ng);
+  if (static_cast<int64_t>(a.n_otiles) * a.n_mtiles * a.splits > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  fgq_status rc = g.bits == 8 ? (nb == 1 ? launch_g<8, 1>(a, g.G, st) : launch_g<8, 2>(a, g.G, st))
+                              : (nb == 1 ? launch_g<4, 1>(a, g.G, st) : launch_g<4, 2>(a, g.G, st));
+  if (rc != FGQ_OK) return rc;
+  return launch_splitk_reduce(ws, a.splits, /*dfp=*/true, g.M, g.O, sx, nullptr,
+                              reinterpret_cast<const int32_t*>(base), out, st);
+}
+
+}  // namespace fgq

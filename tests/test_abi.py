@@ -92,15 +92,17 @@ def test_fused_layer_validation():
 
 def test_prepared_bytes_dfp():
     L = fgq.lib()
-    # header 256, one int8 plane O32*Kp, bias 4*O, dequantized scales 4*O*K/G
+    # header 256, one int8 plane O32*Kp, bias 4*O, dequantized scales 4*O*K/G,
+    # scale codes O*K/G (each region 256-byte aligned)
     plane = 128 * 1152
     bias_off = 256 + plane
     alpha_off = bias_off + 512
-    assert L.fgq_prepared_bytes_dfp(128, 1152, 4) == alpha_off + 4 * 128 * 288
+    acodes_off = alpha_off + 4 * 128 * 288
+    assert L.fgq_prepared_bytes_dfp(128, 1152, 4) == acodes_off + 128 * 288
     assert L.fgq_prepared_bytes_dfp(128, 1152, 5) == 0
     # O padded to 32, K to 128
     assert L.fgq_prepared_bytes_dfp(33, 100, 4) % 256 == 0
-    assert L.fgq_prepared_bytes_dfp(33, 100, 4) >= 256 + 64 * 128 + 4 * 33 + 4 * 33 * 25
+    assert L.fgq_prepared_bytes_dfp(33, 100, 4) >= 256 + 64 * 128 + 4 * 33 + 5 * 33 * 25
 
 
 @no_device

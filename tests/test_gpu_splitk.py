@@ -81,6 +81,42 @@ def test_gemm_dfp_ws_bit_exact(case):
     np.testing.assert_array_equal(got, oracle.quantize_act(y_ref.ravel(), 8, s_out)[0])
 
 
+# Shapes of the codes-expanding kernel (M <= 64, K % 64 == 0, G a power of
+# two in 4..128): one or two 32-row blocks, every scale-code width, a K tail
+# of half a step, channels that do not fill the last 128-wide tile, 4-bit
+# activations, and long K (many splits of up to 8 steps).
+DFPX_CASES = [
+    # M, K, O, G, bits
+    (64, 9216, 256, 4, 8),
+    (1, 9216, 384, 4, 8),
+    (32, 2048, 200, 8, 8),
+    (33, 4160, 128, 16, 8),       # K % 128 == 64
+    (7, 4096, 160, 32, 4),
+    (40, 4160, 96, 64, 4),        # K % 128 == 64, 4-bit
+    (64, 4096, 130, 128, 8),
+    (2, 1024, 64, 4, 4),
+]
+
+
+@pytest.mark.parametrize("case", DFPX_CASES)
+def test_gemm_dfp_ws_codes_path(case):
+    M, K, O, G, bits = case
+    w, x, codes, alpha, q, sx = setup(*case, tag=("dfpx", case))
+    prep = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, G, 8)
+    t, a, _ = oracle.ternarize(w, G)
+    qr, sr = oracle.quantize_act(x, bits)
+    A, fl = oracle.dfp_alpha(a, 8)
+    y_ref = oracle.gemm_dfp(qr, bits, sr, M, K, oracle.pack_codes(t), A, fl, O, G)
+    y = host(fgq.fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prep, O, G))
+    np.testing.assert_array_equal(y.view(np.uint32), y_ref.view(np.uint32))
+    for out_bits in (8, 4):
+        s_out = np.float32(0.8 * float(np.abs(y_ref).max()) / (2 ** out_bits - 1))
+        got = host(fgq.fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prep, O, G, out_bits=out_bits,
+                                       out_scale=dev(np.array([s_out], np.float32)))).ravel()
+        ref = oracle.quantize_act(y_ref.ravel(), out_bits, s_out)[0]
+        np.testing.assert_array_equal(got, ref)
+
+
 def test_gemm_ws_missing_workspace_and_no_split():
     M, K, O, G, bits = CASES[0]
     w, x, codes, alpha, q, sx = setup(M, K, O, G, bits, "ws")
