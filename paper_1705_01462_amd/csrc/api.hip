@@ -361,7 +361,7 @@ fgq_status fgq_gemm_dfp_ws(const uint8_t* q, int32_t bits, const float* sx, int6
   const bool ws_ok = ws && reinterpret_cast<uintptr_t>(ws) % 4 == 0 && ws_bytes >= fgq_gemm_ws_bytes(M, K, O, G, 1);
   if (dfpx_supported(g, q)) {  // weights read as codes + scale codes
     if (!ws_ok) return FGQ_ERR_WORKSPACE;
-    return launch_dfpx_splitk(q, sx, codes, prepared, g, lo, static_cast<int32_t*>(ws), as_stream(stream));
+    return launch_dfpx_splitk(q, sx, prepared, g, lo, static_cast<int32_t*>(ws), as_stream(stream));
   }
   if (fold_dfp_supported(g, q)) {
     int32_t sps = 0;

@@ -38,8 +38,11 @@ PreparedLayout prepared_layout_dfp(int64_t O, int64_t K, int32_t G) {
   L.planes_off = kDfpHeaderBytes;
   L.bias_off = round_up(L.planes_off + L.O32 * L.Kp, 256);
   L.alpha_off = round_up(L.bias_off + 4 * O, 256);
-  L.acodes_off = round_up(L.alpha_off + 4 * O * (K / G), 256);
-  L.total = round_up(L.acodes_off + O * (K / G), 256);
+  const int64_t xnb = dfpx_acode_bytes(G);
+  const int64_t O128 = round_up(O, 128);
+  L.xcodes_off = round_up(L.alpha_off + 4 * O * (K / G), 256);
+  L.xacodes_off = round_up(L.xcodes_off + (xnb > 0 ? O128 * L.Kp / 4 : 0), 256);
+  L.total = round_up(L.xacodes_off + O128 * (L.Kp / 64) * xnb, 256);
   L.scale_off = L.total;
   return L;
 }
@@ -116,34 +119,66 @@ __device__ inline int64_t frag_offset1(int64_t nks, int64_t o, int64_t k) {
   return ((tile * nks + ks) * 2 + half) * 1024 + lane * 16 + (kk % 16);
 }
 
-// One block per channel of the padded channel range.
+// Offset of lane (channel o, half hf) of 128-wide K step ks in the
+// expanding GEMM's order: [O/128][Kp/128][4 waves][64 lanes][per-lane bytes].
+__device__ inline int64_t xfrag_lane(int64_t nk, int64_t o, int64_t ks, int hf) {
+  return ((o / 128 * nk + ks) * 4 + (o % 128) / 32) * 64 + o % 32 + 32 * hf;
+}
+
+// One block per channel of the padded channel range (O32 for the plane,
+// O128 for the expanding GEMM's regions when xnb > 0).
 __global__ __launch_bounds__(kThreads) void prepare_dfp_kernel(
     const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O, int64_t K,
     int32_t G, int32_t bits, int64_t Kp, const int32_t* __restrict__ flp, int8_t* __restrict__ planes,
-    int32_t* __restrict__ bias, float* __restrict__ alpha_q, int8_t* __restrict__ acodes) {
+    int32_t* __restrict__ bias, float* __restrict__ alpha_q, uint8_t* __restrict__ xcodes,
+    int8_t* __restrict__ xacodes, int32_t xnb) {
   __shared__ int64_t red[kThreads / 64];
   const int64_t o = blockIdx.x;
   const int64_t nks = Kp / kFoldKStep;
+  const int64_t O32 = round_up(O, 32);
   const int32_t fl = *flp;
-  if (o >= O || fl == INT_MIN) {  // padding channel (or rejected scales)
+  const bool live = o < O && fl != INT_MIN;  // else a padding channel (or rejected scales): zeros
+  const int64_t ng = K / G;
+  const int64_t rb = ceil_div(K, 4);
+  auto code = [&](int64_t k) -> uint32_t { return k < K ? (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u : 0u; };
+
+  // Expanding GEMM order.  Codes: lane (o, hf) of step ks holds k = 128*ks +
+  // 64*hf + [0, 64) in 16 bytes; byte 4h+b holds, at bits 2i, the code of
+  // k = 128*ks + 64*hf + 16h + 4i + b.  Scale codes: xnb bytes per lane, byte
+  // j the code A of the group of k = 128*ks + 64*hf + G*j (G = 128: of 128*ks).
+  if (xnb > 0) {
+    const int64_t nk = Kp / 128;
+    for (int64_t e = threadIdx.x; e < nk * 32; e += kThreads) {
+      const int64_t ks = e / 32;
+      const int hf = static_cast<int>((e % 32) / 16), B = static_cast<int>(e % 16);
+      const int64_t k0 = 128 * ks + 64 * hf + 16 * (B / 4) + B % 4;
+      uint32_t v = 0;
+      if (live)
+        for (int i = 0; i < 4; ++i) v |= code(k0 + 4 * i) << (2 * i);
+      xcodes[xfrag_lane(nk, o, ks, hf) * 16 + B] = static_cast<uint8_t>(v);
+    }
+    for (int64_t e = threadIdx.x; e < nk * 2 * xnb; e += kThreads) {
+      const int64_t ks = e / (2 * xnb);
+      const int hf = static_cast<int>((e / xnb) % 2), j = static_cast<int>(e % xnb);
+      const int64_t k = G >= 128 ? 128 * ks : 128 * ks + 64 * hf + static_cast<int64_t>(G) * j;
+      const int A = (live && k < K) ? dfp_code(alpha[o * ng + k / G], fl, bits) : 0;
+      xacodes[xfrag_lane(nk, o, ks, hf) * xnb + j] = static_cast<int8_t>(A);
+    }
+  }
+  if (o >= O32) return;
+  if (!live) {
     for (int64_t k = threadIdx.x; k < Kp; k += kThreads) planes[frag_offset1(nks, o, k)] = 0;
     return;
   }
-  const int64_t ng = K / G;
-  const int64_t rb = ceil_div(K, 4);
   for (int64_t gi = threadIdx.x; gi < ng; gi += kThreads) {
     const int A = dfp_code(alpha[o * ng + gi], fl, bits);
     alpha_q[o * ng + gi] = static_cast<float>(ldexp(static_cast<double>(A), -fl));
-    acodes[o * ng + gi] = static_cast<int8_t>(A);
   }
   int64_t s = 0;
   for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
-    int v = 0;
-    if (k < K) {
-      const uint32_t c = (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u;
-      const int t = c == 1 ? 1 : (c == 3 ? -1 : 0);
-      v = t * dfp_code(alpha[o * ng + k / G], fl, bits);
-    }
+    const uint32_t c = code(k);
+    const int t = c == 1 ? 1 : (c == 3 ? -1 : 0);
+    const int v = t * (k < K ? dfp_code(alpha[o * ng + k / G], fl, bits) : 0);
     planes[frag_offset1(nks, o, k)] = static_cast<int8_t>(v);
     s += v;
   }
@@ -231,12 +266,15 @@ fgq_status launch_prepare_dfp(const uint8_t* codes, const float* alpha, int64_t 
   fgq_status rc = launch_dfp_alpha(alpha, O * (K / G), alpha_bits, nullptr, fl, st);
   if (rc != FGQ_OK) return rc;
   if (L.O32 > 0x7fffffffLL) return FGQ_ERR_SHAPE;
-  hipLaunchKernelGGL(prepare_dfp_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0, st,
+  const int32_t xnb = static_cast<int32_t>(dfpx_acode_bytes(G));
+  const int64_t nblk = xnb > 0 ? round_up(O, 128) : L.O32;
+  hipLaunchKernelGGL(prepare_dfp_kernel, dim3(static_cast<uint32_t>(nblk)), dim3(kThreads), 0, st,
                      codes, alpha, O, K, G, alpha_bits, L.Kp, fl,
                      reinterpret_cast<int8_t*>(base + L.planes_off),
                      reinterpret_cast<int32_t*>(base + L.bias_off),
                      reinterpret_cast<float*>(base + L.alpha_off),
-                     reinterpret_cast<int8_t*>(base + L.acodes_off));
+                     reinterpret_cast<uint8_t*>(base + L.xcodes_off),
+                     reinterpret_cast<int8_t*>(base + L.xacodes_off), xnb);
   return last_launch();
 }
 

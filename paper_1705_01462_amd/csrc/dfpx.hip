@@ -4,9 +4,13 @@
 // the int8 weights A*t in registers instead of the one-byte-per-weight
 // plane of the prepared layout (0.25 + 1/G bytes per weight).
 //
-// Work split: a workgroup owns 128 channels (a wave each 32), kNB 32-row
-// blocks and up to kSteps 128-wide K steps (split K: int32 sums per split,
-// reduced by splitk_reduce_kernel with the fixed-point epilogue).  Its
+// Work split: a workgroup owns 128 channels, kNB 32-row blocks and up to
+// kSteps 128-wide K steps (split K: int32 sums per split, reduced by
+// splitk_reduce_kernel with the fixed-point epilogue).  Its waves are,
+// with two 32-row blocks, two sets of four (a wave per 32 channels), each
+// set taking half of the steps, so that two waves share every SIMD and one's
+// code expansion overlaps the other's matrix instructions (the sets' sums
+// meet in LDS); with one block, one set of four.  Its
 // activation slice (kNB*32 rows x kSteps*128 k) is loaded once and stays in
 // LDS, and every code and scale-code load of the split is issued up front,
 // after the activation loads: the memory counter completes in order, so the
@@ -17,19 +21,23 @@
 // Operand order.  Lane l (channel 32*wave + l%32, half hf = l/32) holds, in
 // step s and K quarter h, the 16 weights k = 128*s + 64*hf + 16*h + [0, 16);
 // the activation fragment of the same lane reads the same 16 k of its row
-// from LDS.  So a lane's codes of one step are 16 consecutive bytes of its
-// channel's code row (one load), and its scale codes 64/G consecutive bytes.
+// from LDS.  The prepared layout stores the codes and the scale codes in
+// exactly this order ([O/128][K/128][4 waves][64 lanes][16 code bytes, or
+// 64/G scale-code bytes]), so every weight load of a wave reads one
+// contiguous block (a kilobyte of codes), and within a quarter's 32 bits of
+// codes byte b holds, at bits 2i, the code of weight 4i+b: the selector
+// bytes of weights 4i..4i+3 are (codes >> 2i) & 0x03030303.
 //
-// Expansion of 16 weights (32 bits of codes, weight 4i+b in bits 2b of byte
-// i): per group a byte table [0, A, 0, -A] (-A formed four bytes at a time
-// as (0x80808080 - a) ^ 0x80808080, exact because 0 <= A <= 127), then one
-// byte permute per 4 weights with the four 2-bit codes spread to selector
-// bytes.  Code 2 is never written; its table byte is 0.
+// Expansion of 4 weights of one group: a byte table [0, A, 0, -A] (-A
+// formed four bytes at a time as (0x80808080 - a) ^ 0x80808080, exact
+// because 0 <= A <= 127) indexed by those selectors with one byte permute.
+// Code 2 is never written; its table byte is 0.
 //
-// K tail (K % 128 == 64): activations at k >= K are stored as int8 zero, so
-// whatever the weight loads there return (the next channel's codes, or
-// zeros past the buffer end) adds nothing.  The uint8 offset term covers
-// k < K only, as the 128 * sum of the weights in the prepared bias.
+// Padding: codes and scale codes past K and past O are zero in the prepared
+// layout, so padded activations (past K, or rows past M) meet zero weights;
+// the uint8 offset term covers k < K only, as the 128 * sum of the weights
+// in the prepared bias.  Partial sums go out through LDS as 16-byte row
+// pieces when O % 4 == 0 and the workspace is 16-byte aligned.
 #include <algorithm>
 
 #include "fgq_internal.h"
@@ -44,12 +52,12 @@ constexpr int kSteps = 8;  // K steps per split at most (LDS: kNB * 32 KB)
 
 struct DfpxArgs {
   const uint8_t* q;       // activations [M][K] (uint8) or [M][K/2] (uint4)
-  const uint8_t* codes;   // [O][K/4]
-  const int8_t* acodes;   // [O][K/G]
+  const uint8_t* xcodes;  // codes, expanding-GEMM order
+  const int8_t* xacodes;  // scale codes, same order
   const int32_t* bias;    // [O]   128 * sum_k A*t (uint8 offset term)
   int32_t* part;          // [splits][M][O]
-  int32_t M, K, O, n_otiles, n_mtiles, splits, sps, rb, ng;
-  int32_t q_bytes, codes_bytes, acodes_bytes;
+  int32_t M, K, O, n_otiles, n_mtiles, splits, sps, nk, staged;
+  int32_t q_bytes, xcodes_bytes, xacodes_bytes;
 };
 
 template <int kG>
@@ -61,9 +69,7 @@ __device__ inline v4i expand16(uint32_t c32, uint32_t a) {
     const uint32_t j = kG == 4 ? i : (kG == 8 ? i / 2 : 0);  // the A byte of weights 4i..4i+3
     // table bytes [0, A_j, 0, -A_j]; selector 12 gives a zero byte
     const uint32_t T = __builtin_amdgcn_perm(na, a, 0x0Cu | (j << 8) | (0x0Cu << 16) | ((4u + j) << 24));
-    const uint32_t c8 = (c32 >> (8 * i)) & 0xFFu;
-    uint32_t s = c8 | (c8 << 6);
-    s = (s | (s << 12)) & 0x03030303u;  // byte b: the code of weight 4i+b
+    const uint32_t s = (c32 >> (2 * i)) & 0x03030303u;  // byte b: the code of weight 4i+b
     w[i] = static_cast<int>(__builtin_amdgcn_perm(0u, T, s));
   }
   return w;
@@ -103,15 +109,21 @@ struct ACodes {
   }
 };
 
+template <int kNB>
+constexpr int wg_threads() { return kNB == 2 ? 512 : 256; }
+
 template <int kBits, int kG, int kNB>
-__global__ __launch_bounds__(kThreads, 2) void dfpx_gemm_kernel(DfpxArgs a) {
+__global__ __launch_bounds__(wg_threads<kNB>(), 2) void dfpx_gemm_kernel(DfpxArgs a) {
+  constexpr int kWG = wg_threads<kNB>();
+  constexpr int kSets = kWG / 256;                    // wave sets sharing the steps
   constexpr int kRows = 32 * kNB;
-  constexpr int kStageB = kRows * kRowB;                  // one step's activations
-  constexpr int kXP = kRows * kSteps * kSlots / kThreads;  // 16-k pieces per thread
+  constexpr int kStageB = kRows * kRowB;              // one step's activations
+  constexpr int kXP = kRows * kSteps * kSlots / kWG;  // 16-k pieces per thread
+  constexpr int kHalf = kSteps / kSets;               // steps per wave
   __shared__ __attribute__((aligned(16))) unsigned char lds[kSteps * kStageB];
 
   const int tid = threadIdx.x;
-  const int lane = tid % 64, wo = tid / 64, hf = lane / 32;
+  const int lane = tid % 64, wo = (tid / 64) % 4, sh = tid / 256, hf = lane / 32;
   const int ntiles = a.n_otiles * a.n_mtiles;
   const int tsplit = xcd_swizzle(blockIdx.x, ntiles * a.splits);
   const int split = tsplit / ntiles, tile = tsplit % ntiles;
@@ -122,17 +134,18 @@ __global__ __launch_bounds__(kThreads, 2) void dfpx_gemm_kernel(DfpxArgs a) {
   const int nsteps = ks0 + a.sps < nk_all ? a.sps : nk_all - ks0;  // 1..kSteps
   const int k0 = ks0 * kKT;
 
-  // The uint8 offset term of the lane's channel (split 0 only), requested
-  // first so that no wait for it follows the weight loads.
+  // The uint8 offset term of the lane's channel (split 0, first half only),
+  // requested first so that no wait for it follows the weight loads.
   const bool ocok = oc < a.O;
   int bj = 0;
   if constexpr (kBits == 8) {
     const __amdgpu_buffer_rsrc_t brs =
         __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.bias), 0, 4 * a.O, kBufFlags);
-    bj = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(brs, ocok && ks0 == 0 ? 4 * oc : kOutOfRange, 0, 0));
+    bj = static_cast<int>(
+        __builtin_amdgcn_raw_buffer_load_b32(brs, ocok && ks0 == 0 && sh == 0 ? 4 * oc : kOutOfRange, 0, 0));
   }
 
-  // ---- activation slice: piece p = tid + 256*i is row p / (8*kSteps),
+  // ---- activation slice: piece p = tid + 512*i is row p / (8*kSteps),
   // 16-k slot p % (8*kSteps) (a row's slots are consecutive threads, so a
   // wave reads one contiguous kilobyte of a row).  Rows >= M and steps past
   // the split read nothing.
@@ -142,7 +155,7 @@ __global__ __launch_bounds__(kThreads, 2) void dfpx_gemm_kernel(DfpxArgs a) {
   raw_t xraw[kXP];
 #pragma unroll
   for (int i = 0; i < kXP; ++i) {
-    const int p = tid + kThreads * i;
+    const int p = tid + kWG * i;
     const int row = p / (kSlots * kSteps), ksl = p % (kSlots * kSteps);
     const int m = m0 + row, k = k0 + 16 * ksl;
     const bool ok = (m < a.M) & (ksl < kSlots * nsteps) & (k < a.K);
@@ -154,33 +167,35 @@ __global__ __launch_bounds__(kThreads, 2) void dfpx_gemm_kernel(DfpxArgs a) {
   }
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- every weight load of the split.  Steps past the split re-read the
-  // split's last step (in range; never used).  Channels >= O read nothing.
+  // ---- every weight load of the wave's steps (kHalf*sh + s), in the
+  // prepared order.  Steps past the split re-read the split's last step (in
+  // range; never used).
   const __amdgpu_buffer_rsrc_t crs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.codes), 0, a.codes_bytes, kBufFlags);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.xcodes), 0, a.xcodes_bytes, kBufFlags);
   const __amdgpu_buffer_rsrc_t ars =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.acodes), 0, a.acodes_bytes, kBufFlags);
-  const int cbase = ocok ? oc * a.rb + k0 / 4 + 16 * hf : static_cast<int>(kOutOfRange);
-  const int abase = ocok ? oc * a.ng + (k0 + 64 * hf) / kG : static_cast<int>(kOutOfRange);
-  v4i cw[kSteps];
-  ACodes<kG> aw[kSteps];
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.xacodes), 0, a.xacodes_bytes, kBufFlags);
+  const int lane0 = ((tile % a.n_otiles) * a.nk + ks0) * 256 + 64 * wo + lane;  // lane index of step ks0
+  constexpr int kAB = ACodes<kG>::kBytes;
+  v4i cw[kHalf];
+  ACodes<kG> aw[kHalf];
 #pragma unroll
-  for (int s = 0; s < kSteps; ++s) {
-    const int ss = s < nsteps ? s : nsteps - 1;
-    cw[s] = __builtin_amdgcn_raw_buffer_load_b128(crs, cbase + 32 * ss, 0, 0);
-    aw[s].load(ars, abase + (kKT * ss) / kG);
+  for (int s = 0; s < kHalf; ++s) {
+    const int st = kHalf * sh + s;
+    const int ln = lane0 + 256 * (st < nsteps ? st : nsteps - 1);
+    cw[s] = __builtin_amdgcn_raw_buffer_load_b128(crs, 16 * ln, 0, 0);
+    aw[s].load(ars, kAB * ln);
   }
   __builtin_amdgcn_sched_barrier(0);
 
-  // ---- publish the slice: uint8 as q - 128 (k >= K as 0), uint4 unpacked
+  // ---- publish the slice: uint8 as q - 128, uint4 unpacked
 #pragma unroll
   for (int i = 0; i < kXP; ++i) {
-    const int p = tid + kThreads * i;
+    const int p = tid + kWG * i;
     const int row = p / (kSlots * kSteps), ksl = p % (kSlots * kSteps);
     unsigned char* dst = lds + (ksl / kSlots) * kStageB + lds_off(row, ksl % kSlots);
     v4i v;
     if constexpr (kBits == 8) {
-      const int x = k0 + 16 * ksl < a.K ? static_cast<int>(0x80808080u) : 0;
+      const int x = static_cast<int>(0x80808080u);
       v = xraw[i];
       v.x ^= x; v.y ^= x; v.z ^= x; v.w ^= x;
     } else {
@@ -202,9 +217,10 @@ __global__ __launch_bounds__(kThreads, 2) void dfpx_gemm_kernel(DfpxArgs a) {
     for (int h = 0; h < 4; ++h) afrag[c][h] = lds_off(32 * c + lane % 32, 4 * hf + h);
 
 #pragma unroll
-  for (int s = 0; s < kSteps; ++s) {
-    if (s >= nsteps) break;
-    const unsigned char* base = lds + s * kStageB;
+  for (int s = 0; s < kHalf; ++s) {
+    const int st = kHalf * sh + s;
+    if (st >= nsteps) break;
+    const unsigned char* base = lds + st * kStageB;
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       const v4i wf = expand16<kG>(static_cast<uint32_t>(cw[s][h]), aw[s].quarter(h));
@@ -216,28 +232,80 @@ __global__ __launch_bounds__(kThreads, 2) void dfpx_gemm_kernel(DfpxArgs a) {
     }
   }
 
-  // this split's raw sums, [split][m][o]
-  if (!ocok) return;
-  int32_t* const part = a.part;
+  // ---- the sums into a kRows x 128-channel int32 tile in LDS (the slice
+  // is dead once every wave is past the K loop); a second wave set adds its
+  // own with LDS atomic adds (integer, so the order does not matter)
+  constexpr int kPitch = 128 * 4 + 32;  // the two rows of a write are 32 banks apart
+  static_assert(kRows * kPitch <= kSteps * kStageB, "partial tile fits the slice");
+  auto at = [&](int c, int r) -> int* {
+    const int row = 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
+    return reinterpret_cast<int*>(lds + row * kPitch + 4 * (32 * wo + lane % 32));
+  };
+  int32_t* const part = a.part + static_cast<int64_t>(split) * a.M * a.O;
+  if (kSets == 1 && !a.staged) {
+    if (!ocok) return;
 #pragma unroll
-  for (int c = 0; c < kNB; ++c)
+    for (int c = 0; c < kNB; ++c)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
-      if (m < a.M) part[(static_cast<int64_t>(split) * a.M + m) * a.O + oc] = acc[c][r];
+      for (int r = 0; r < 16; ++r) {
+        const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
+        if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = acc[c][r];
+      }
+    return;
+  }
+  __syncthreads();
+  if (sh == 0) {
+#pragma unroll
+    for (int c = 0; c < kNB; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) *at(c, r) = acc[c][r];
+  }
+  if constexpr (kSets == 2) {
+    __syncthreads();
+    if (sh == 1) {
+#pragma unroll
+      for (int c = 0; c < kNB; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r)
+          __hip_atomic_fetch_add(at(c, r), acc[c][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
     }
+    if (!a.staged) {
+      __syncthreads();
+      if (sh != 0 || !ocok) return;
+#pragma unroll
+      for (int c = 0; c < kNB; ++c)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
+          if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = *at(c, r);
+        }
+      return;
+    }
+  }
+  // this split's raw sums, [split][m][o], as 16-byte pieces of rows
+  __syncthreads();
+  const int o0 = (tile % a.n_otiles) * 128;
+#pragma unroll
+  for (int t = tid; t < kRows * 32; t += kWG) {
+    const int row = t / 32, ch = o0 + 4 * (t % 32);
+    const int m = m0 + row;
+    if (m < a.M && ch < a.O)
+      *reinterpret_cast<v4i*>(part + static_cast<int64_t>(m) * a.O + ch) =
+          *reinterpret_cast<const v4i*>(lds + row * kPitch + 16 * (t % 32));
+  }
 }
 
 template <int kBits, int kNB>
 fgq_status launch_g(const DfpxArgs& a, int G, hipStream_t st) {
   const dim3 grid(static_cast<uint32_t>(a.n_otiles * a.n_mtiles * a.splits));
+  constexpr int kWG = wg_threads<kNB>();
   switch (G) {
-    case 4: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 4, kNB>), grid, dim3(kThreads), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 8, kNB>), grid, dim3(kThreads), 0, st, a); break;
-    case 16: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 16, kNB>), grid, dim3(kThreads), 0, st, a); break;
-    case 32: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 32, kNB>), grid, dim3(kThreads), 0, st, a); break;
-    case 64: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 64, kNB>), grid, dim3(kThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 128, kNB>), grid, dim3(kThreads), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 4, kNB>), grid, dim3(kWG), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 8, kNB>), grid, dim3(kWG), 0, st, a); break;
+    case 16: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 16, kNB>), grid, dim3(kWG), 0, st, a); break;
+    case 32: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 32, kNB>), grid, dim3(kWG), 0, st, a); break;
+    case 64: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 64, kNB>), grid, dim3(kWG), 0, st, a); break;
+    default: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 128, kNB>), grid, dim3(kWG), 0, st, a); break;
   }
   return last_launch();
 }
@@ -245,17 +313,16 @@ fgq_status launch_g(const DfpxArgs& a, int G, hipStream_t st) {
 }  // namespace
 
 bool dfpx_shape_ok(int64_t M, int64_t K, int64_t O, int32_t G) {
-  const bool pow2g = G == 4 || G == 8 || G == 16 || G == 32 || G == 64 || G == 128;
-  return pow2g && M <= kDfpxMaxM && K % 64 == 0 && K <= kFoldMaxK && O * (K / 4) < (1LL << 31) &&
-         M * K < (1LL << 31) && M * O < (1LL << 31);
+  const int64_t O128 = round_up(O, 128), Kp = round_up(K, 128);
+  return dfpx_acode_bytes(G) > 0 && M <= kDfpxMaxM && K % 16 == 0 && K <= kFoldMaxK &&
+         O128 * Kp / 4 < (1LL << 31) && M * K < (1LL << 31) && M * O < (1LL << 31);
 }
 
 bool dfpx_supported(const ConvGeom& g, const uint8_t* q) {
   const uintptr_t align = g.bits == 8 ? 16 : 8;
   // a 1x1 convolution at stride 1 without padding is the GEMM on [M][K]
   return g.R == 1 && g.S == 1 && g.sh == 1 && g.sw == 1 && g.ph == 0 && g.pw == 0 &&
-         reinterpret_cast<uintptr_t>(q) % align == 0 &&
-         dfpx_shape_ok(g.M, g.K, g.O, g.G);
+         reinterpret_cast<uintptr_t>(q) % align == 0 && dfpx_shape_ok(g.M, g.K, g.O, g.G);
 }
 
 int32_t dfpx_splits(int64_t M, int64_t K, int64_t O, int32_t G, int32_t* steps_per_split) {
@@ -272,15 +339,15 @@ int32_t dfpx_splits(int64_t M, int64_t K, int64_t O, int32_t G, int32_t* steps_p
   return static_cast<int32_t>(ceil_div(nk, sps));
 }
 
-fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const uint8_t* codes, const void* prepared,
+fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const void* prepared,
                               const ConvGeom& g, const LayerOut& out, int32_t* ws, hipStream_t st) {
   const PreparedLayout L = prepared_layout_dfp(g.O, g.K, g.G);
   const char* base = static_cast<const char*>(prepared);
   const int nb = g.M <= 32 ? 1 : 2;
   DfpxArgs a;
   a.q = q;
-  a.codes = codes;
-  a.acodes = reinterpret_cast<const int8_t*>(base + L.acodes_off);
+  a.xcodes = reinterpret_cast<const uint8_t*>(base + L.xcodes_off);
+  a.xacodes = reinterpret_cast<const int8_t*>(base + L.xacodes_off);
   a.bias = reinterpret_cast<const int32_t*>(base + L.bias_off);
   a.part = ws;
   a.M = static_cast<int32_t>(g.M);
@@ -289,11 +356,11 @@ fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const uint8_t* 
   a.n_otiles = static_cast<int32_t>(ceil_div(g.O, 128));
   a.n_mtiles = static_cast<int32_t>(ceil_div(g.M, 32 * nb));
   a.splits = dfpx_splits(g.M, g.K, g.O, g.G, &a.sps);
-  a.rb = static_cast<int32_t>(g.K / 4);
-  a.ng = static_cast<int32_t>(g.K / g.G);
+  a.nk = static_cast<int32_t>(L.Kp / 128);
+  a.staged = g.O % 4 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0;
   a.q_bytes = static_cast<int32_t>(g.bits == 8 ? g.M * g.K : g.M * g.K / 2);
-  a.codes_bytes = static_cast<int32_t>(g.O * a.rb);
-  a.acodes_bytes = static_cast<int32_t>(g.O * a.ng);
+  a.xcodes_bytes = static_cast<int32_t>(L.xacodes_off - L.xcodes_off);
+  a.xacodes_bytes = static_cast<int32_t>(L.total - L.xacodes_off);
   if (static_cast<int64_t>(a.n_otiles) * a.n_mtiles * a.splits > 0x7fffffffLL) return FGQ_ERR_SHAPE;
   fgq_status rc = g.bits == 8 ? (nb == 1 ? launch_g<8, 1>(a, g.G, st) : launch_g<8, 2>(a, g.G, st))
                               : (nb == 1 ? launch_g<4, 1>(a, g.G, st) : launch_g<4, 2>(a, g.G, st));

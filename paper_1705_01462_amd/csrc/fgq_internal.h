@@ -61,8 +61,9 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 //               [O32/32][Kp/64][1 plane][2 K halves][64 lanes][16 bytes]
 //      bias   : int32 [O]     128 * sum_k plane[o][k]
 //      alpha  : fp32 [O][K/G] the dequantized scales A * 2^-fl (direct path)
-//      acodes : int8 [O][K/G] the codes A themselves (GEMMs that expand the
-//               2-bit weight codes in registers, dfpx.hip)
+//      xcodes, xacodes (G a power of two in 4..128): the 2-bit codes and the
+//               scale codes A in the order of the GEMM that expands them in
+//               registers (dfpx.hip; layout there)
 // In the fragment order, lane l of (channel tile, 64-wide K block, plane,
 // half) holds channel 32*tile + l%32, k = 64*block + 32*half + 16*(l/32) +
 // [0, 16), so each wave-wide 16-byte load is one contiguous kilobyte.
@@ -70,7 +71,7 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 enum PrepKind { kPrepFold = 0, kPrepGroup = 1, kPrepDfp = 2 };
 struct PreparedLayout {
   int kind;
-  int64_t O32, Kp, nks, planes_off, bias_off, scale_off, alpha_off, acodes_off, total;
+  int64_t O32, Kp, nks, planes_off, bias_off, scale_off, alpha_off, xcodes_off, xacodes_off, total;
 };
 constexpr int64_t kFoldKStep = 64;
 constexpr int64_t kFoldTileBytes = 3 * 2 * 64 * 16;  // one channel tile, one K block
@@ -138,10 +139,15 @@ fgq_status launch_fold_dfp_splitk(const uint8_t* q, const float* sx, const void*
 // the 2-bit codes and the scale codes in registers (dfpx.hip): its own K
 // split (dfpx_splits), int32 sums in ws [splits][M][O], the same reduction.
 constexpr int64_t kDfpxMaxM = 64;
+// Scale-code bytes per lane and 128-wide K step in that order (0: no such
+// regions for this G).
+inline int64_t dfpx_acode_bytes(int32_t G) {
+  return (G == 4 || G == 8 || G == 16 || G == 32 || G == 64) ? 64 / G : (G == 128 ? 1 : 0);
+}
 bool dfpx_shape_ok(int64_t M, int64_t K, int64_t O, int32_t G);
 bool dfpx_supported(const ConvGeom& g, const uint8_t* q);
 int32_t dfpx_splits(int64_t M, int64_t K, int64_t O, int32_t G, int32_t* steps_per_split);
-fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const uint8_t* codes, const void* prepared,
+fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const void* prepared,
                               const ConvGeom& g, const LayerOut& out, int32_t* ws, hipStream_t st);
 fgq_status launch_splitk_reduce(const int32_t* part, int32_t splits, bool dfp, int64_t M, int64_t O,
                                 const float* sx, const float* scale, const int32_t* fl, const LayerOut& out,

@@ -38,13 +38,13 @@ PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G) {
     L.alpha_off = round_up(L.O32 * L.Kp, 256);
     L.total = round_up(L.alpha_off + 4 * L.nks * L.O32, 256);
     L.bias_off = L.scale_off = L.total;
-    L.acodes_off = L.total;
+    L.xcodes_off = L.xacodes_off = L.total;
   } else {
     L.kind = kPrepFold;
     L.bias_off = round_up(3 * L.O32 * L.Kp, 256);
     L.scale_off = round_up(L.bias_off + 12 * O, 256);
     L.total = round_up(L.scale_off + 4 * O, 256);
-    L.alpha_off = L.acodes_off = L.total;
+    L.alpha_off = L.xcodes_off = L.xacodes_off = L.total;
   }
   return L;
 }

@@ -93,12 +93,18 @@ def test_fused_layer_validation():
 def test_prepared_bytes_dfp():
     L = fgq.lib()
     # header 256, one int8 plane O32*Kp, bias 4*O, dequantized scales 4*O*K/G,
-    # scale codes O*K/G (each region 256-byte aligned)
+    # then for the codes-expanding GEMM the 2-bit codes (O128*Kp/4) and the
+    # scale codes (O128*Kp/64 * 64/G) in its operand order (each region
+    # 256-byte aligned)
     plane = 128 * 1152
     bias_off = 256 + plane
     alpha_off = bias_off + 512
-    acodes_off = alpha_off + 4 * 128 * 288
-    assert L.fgq_prepared_bytes_dfp(128, 1152, 4) == acodes_off + 128 * 288
+    xcodes_off = alpha_off + 4 * 128 * 288
+    xacodes_off = xcodes_off + 128 * 1152 // 4
+    assert L.fgq_prepared_bytes_dfp(128, 1152, 4) == xacodes_off + 128 * 1152 // 4
+    # G = 64: one scale-code byte per lane and 128-wide step
+    assert L.fgq_prepared_bytes_dfp(128, 1152, 64) == (alpha_off + 4 * 128 * 18 + 255) // 256 * 256 \
+        + 128 * 1152 // 4 + 128 * 1152 // 64
     assert L.fgq_prepared_bytes_dfp(128, 1152, 5) == 0
     # O padded to 32, K to 128
     assert L.fgq_prepared_bytes_dfp(33, 100, 4) % 256 == 0
