@@ -52,47 +52,59 @@ namespace {
 constexpr int kThreads = 256;
 constexpr int kExpThreads = 1024;
 
-// One workgroup: the largest alpha (kSigned: the largest |w|), then fl
-// (INT32_MIN if a value is NaN or Inf, or, for scales, negative).
+// The shared exponent in three launches, accumulated in *fl itself: zero
+// it, fold every value into it with an unsigned atomic maximum (a finite
+// non-negative float orders as its bit pattern; NaN, Inf or a negative scale
+// becomes 0xFFFFFFFF, above every such pattern), then turn the largest value
+// into fl (INT32_MIN if any value was rejected).  kSigned: |w| of weights.
+__global__ void dfp_exponent_init_kernel(int32_t* __restrict__ fl) { fl[0] = 0; }
+
 template <bool kSigned>
 __global__ __launch_bounds__(kExpThreads) void dfp_exponent_kernel(const float* __restrict__ alpha,
-                                                                   int64_t n, int32_t bits,
-                                                                   int32_t* __restrict__ fl) {
-  __shared__ float red[kExpThreads / 64];
-  __shared__ int badw[kExpThreads / 64];
-  float amax = 0.0f;
-  int bad = 0;
-  for (int64_t i = threadIdx.x; i < n; i += kExpThreads) {
+                                                                   int64_t n, int32_t* __restrict__ fl) {
+  __shared__ uint32_t red[kExpThreads / 64];
+  uint32_t vmax = 0;
+  for (int64_t i = static_cast<int64_t>(blockIdx.x) * kExpThreads + threadIdx.x; i < n;
+       i += static_cast<int64_t>(gridDim.x) * kExpThreads) {
     const float a = kSigned ? fabsf(alpha[i]) : alpha[i];
-    bad |= !(a >= 0.0f && a < __builtin_huge_valf());  // NaN, Inf or (scales) negative
-    amax = fmaxf(amax, a);
+    const bool ok = a >= 0.0f && a < __builtin_huge_valf();
+    const uint32_t v = ok ? __float_as_uint(a + 0.0f) : 0xFFFFFFFFu;  // + 0: -0 becomes +0
+    vmax = v > vmax ? v : vmax;
   }
   for (int off = 32; off > 0; off >>= 1) {
-    amax = fmaxf(amax, __shfl_xor(amax, off));
-    bad |= __shfl_xor(bad, off);
+    const uint32_t o = static_cast<uint32_t>(__shfl_xor(static_cast<int>(vmax), off));
+    vmax = o > vmax ? o : vmax;
   }
-  const int lane = threadIdx.x % 64, wid = threadIdx.x / 64;
-  if (lane == 0) {
-    red[wid] = amax;
-    badw[wid] = bad;
-  }
+  if (threadIdx.x % 64 == 0) red[threadIdx.x / 64] = vmax;
   __syncthreads();
   if (threadIdx.x == 0) {
-    for (int i = 1; i < kExpThreads / 64; ++i) {
-      amax = fmaxf(amax, red[i]);
-      bad |= badw[i];
-    }
-    amax = fmaxf(amax, red[0]);
-    bad |= badw[0];
-    int32_t f = 0;
-    if (amax > 0.0f) {
-      int e;
-      const float m = frexpf(amax, &e);  // amax = m 2^e, m in [0.5, 1)
-      const int ceil_log2 = m == 0.5f ? e - 1 : e;
-      f = bits - (ceil_log2 + 1);
-    }
-    fl[0] = bad ? INT_MIN : f;
+    for (int i = 0; i < kExpThreads / 64; ++i) vmax = red[i] > vmax ? red[i] : vmax;
+    atomicMax(reinterpret_cast<unsigned int*>(fl), vmax);
   }
+}
+
+__global__ void dfp_exponent_final_kernel(int32_t bits, int32_t* __restrict__ fl) {
+  const uint32_t v = static_cast<uint32_t>(fl[0]);
+  int32_t f = 0;
+  const float amax = __uint_as_float(v);
+  if (v != 0xFFFFFFFFu && amax > 0.0f) {
+    int e;
+    const float m = frexpf(amax, &e);  // amax = m 2^e, m in [0.5, 1)
+    const int ceil_log2 = m == 0.5f ? e - 1 : e;
+    f = bits - (ceil_log2 + 1);
+  }
+  fl[0] = v == 0xFFFFFFFFu ? INT_MIN : f;
+}
+
+template <bool kSigned>
+fgq_status launch_exponent(const float* x, int64_t n, int32_t bits, int32_t* fl, hipStream_t st) {
+  const int64_t blocks = ceil_div(n, 4 * kExpThreads) < 1024 ? ceil_div(n, 4 * kExpThreads) : 1024;
+  hipLaunchKernelGGL(dfp_exponent_init_kernel, dim3(1), dim3(1), 0, st, fl);
+  if (n > 0)
+    hipLaunchKernelGGL(dfp_exponent_kernel<kSigned>, dim3(static_cast<uint32_t>(blocks)), dim3(kExpThreads), 0, st,
+                       x, n, fl);
+  hipLaunchKernelGGL(dfp_exponent_final_kernel, dim3(1), dim3(1), 0, st, bits, fl);
+  return last_launch();
 }
 
 __device__ inline int dfp_code(float alpha, int32_t fl, int32_t bits) {
@@ -237,8 +249,7 @@ fgq_status launch_prepare_w8(const float* w, int64_t O, int64_t C, int32_t R, in
   const PreparedLayout L = prepared_layout_dfp(O, K, static_cast<int32_t>(C));
   char* base = static_cast<char*>(prepared);
   int32_t* fl = reinterpret_cast<int32_t*>(base);
-  hipLaunchKernelGGL(dfp_exponent_kernel<true>, dim3(1), dim3(kExpThreads), 0, st, w, O * K, 8, fl);
-  if (hipGetLastError() != hipSuccess) return FGQ_ERR_HIP;
+  if (launch_exponent<true>(w, O * K, 8, fl, st) != FGQ_OK) return FGQ_ERR_HIP;
   if (L.O32 > 0x7fffffffLL) return FGQ_ERR_SHAPE;
   hipLaunchKernelGGL(prepare_w8_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0, st, w, O,
                      C, R, S, L.Kp, fl, reinterpret_cast<int8_t*>(base + L.planes_off),
@@ -248,8 +259,7 @@ fgq_status launch_prepare_w8(const float* w, int64_t O, int64_t C, int32_t R, in
 
 fgq_status launch_dfp_alpha(const float* alpha, int64_t n, int32_t bits, int8_t* A, int32_t* fl,
                             hipStream_t st) {
-  hipLaunchKernelGGL(dfp_exponent_kernel<false>, dim3(1), dim3(kExpThreads), 0, st, alpha, n, bits, fl);
-  if (hipGetLastError() != hipSuccess) return FGQ_ERR_HIP;
+  if (launch_exponent<false>(alpha, n, bits, fl, st) != FGQ_OK) return FGQ_ERR_HIP;
   if (A && n > 0) {
     const int64_t blocks = ceil_div(n, kThreads) < 4096 ? ceil_div(n, kThreads) : 4096;
     hipLaunchKernelGGL(dfp_codes_kernel, dim3(static_cast<uint32_t>(blocks)), dim3(kThreads), 0, st,
