@@ -14,6 +14,8 @@ from . import build as _build
 
 EXACT = 0       # Eq. (5) solved by exhaustive threshold search
 EXP_LEMMA = 1   # Lemma 1: Delta = mean |W|
+GAUSS = 3       # Gaussian-optimal threshold 0.612 * rms(W)
+KS = 4          # per layer: EXP_LEMMA or GAUSS, by the K-S test (Sec. 3.1)
 
 _lib = None
 
@@ -55,10 +57,16 @@ def lib():
                                     _c_i64, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i64,
                                     _c_i64, _c_i32, _c_p]
         L.orc_max_threads.argtypes = []
+        L.orc_ternarize_group_asym.argtypes = [_c_p, _c_i64, _c_i64, _c_p, _c_i64, _c_p, _c_p, _c_p]
+        L.orc_ternarize_asym.argtypes = [_c_p, _c_i64, _c_i64, _c_i32, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p]
+        L.orc_ks_distances.argtypes = [_c_p, _c_i64, _c_p]
+        L.orc_gauss_u.argtypes = []
+        L.orc_gauss_u.restype = ctypes.c_double
         for f in ("orc_ternarize_group", "orc_ternarize", "orc_quantize_act",
                   "orc_group_sums_conv", "orc_conv2d", "orc_gemm", "orc_dfp_alpha",
                   "orc_conv2d_dfp", "orc_gemm_dfp", "orc_w8_quantize", "orc_conv2d_w8",
-                  "orc_max_threads"):
+                  "orc_max_threads", "orc_ternarize_group_asym", "orc_ternarize_asym",
+                  "orc_ks_distances"):
             getattr(L, f).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -104,6 +112,45 @@ def ternarize(w, G, method=EXACT):
     d = np.zeros_like(a)
     _check(lib().orc_ternarize(_ptr(w), O, C, R, S, G, method, _ptr(t), _ptr(a), _ptr(d)))
     return t, a, d
+
+
+def ternarize_group_asym(w):
+    """One group, Eq. (3)-(4): returns (t int8[n], alpha, delta_p, delta_n)."""
+    w = np.ascontiguousarray(w, dtype=np.float32).ravel()
+    t = np.zeros(w.size, np.int8)
+    a, dp, dn = (np.zeros(1, np.float32) for _ in range(3))
+    _check(lib().orc_ternarize_group_asym(_ptr(w), w.size, 1, _ptr(t), 1, _ptr(a), _ptr(dp), _ptr(dn)))
+    return t, a[0], dp[0], dn[0]
+
+
+def ternarize_asym(w, G):
+    """Layer weights as for ternarize; returns t, alpha, delta_p, delta_n."""
+    w = np.ascontiguousarray(w, dtype=np.float32)
+    if w.ndim == 2:
+        w = w.reshape(w.shape[0], w.shape[1], 1, 1)
+    O, C, R, S = w.shape
+    K = C * R * S
+    t = np.zeros((O, K), np.int8)
+    a = np.zeros((O, K // G if G > 0 and K % G == 0 else 1), np.float32)
+    dp, dn = np.zeros_like(a), np.zeros_like(a)
+    _check(lib().orc_ternarize_asym(_ptr(w), O, C, R, S, G, _ptr(t), _ptr(a), _ptr(dp), _ptr(dn)))
+    return t, a, dp, dn
+
+
+def ks_distances(w):
+    """K-S distances of |w| (storage order) to the fitted half-normal and
+    exponential laws: returns (d_gauss, d_exp)."""
+    w = np.ascontiguousarray(w, dtype=np.float32).ravel()
+    d = np.zeros(2, np.float64)
+    _check(lib().orc_ks_distances(_ptr(w), w.size, _ptr(d)))
+    return float(d[0]), float(d[1])
+
+
+def gauss_u():
+    return float(lib().orc_gauss_u())
+
+
+KS_SAMPLE = 16384
 
 
 def pack_codes(t):

@@ -107,6 +107,42 @@ static int ternarize_lemma(const float* w, int64_t n, int64_t stride, int8_t* t,
   return ORC_OK;
 }
 
+/*
+ * Gaussian reference (Sec. 3.1, the distribution the K-S test may select):
+ * for w ~ N(0, sigma) and a threshold u*sigma, the expected objective of
+ * Eq. (5), E[|w|; |w| > u sigma]^2 / P(|w| > u sigma), is proportional to
+ * phi(u)^2 / (1 - Phi(u)); its stationary point satisfies
+ * 2u (1 - Phi(u)) = phi(u), whose root is ORC_GAUSS_U = 0.61200318...  With
+ * sigma estimated by maximum likelihood, rms(w) (Sec. 3.1):
+ * Delta = fp32(ORC_GAUSS_U * sqrt(sum w^2 / n)) (fp64 sum in index order),
+ * kept set {i : |w_i| > Delta} in fp32, alpha = fp32(mean of the kept
+ * magnitudes) as in Eq. (5).
+ */
+static int ternarize_gauss(const float* w, int64_t n, int64_t stride, int8_t* t,
+                           int64_t tstride, float* alpha, float* delta) {
+  double Q = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    const double v = (double)w[i * stride];
+    Q = Q + v * v;
+  }
+  float d = (float)(ORC_GAUSS_U * sqrt(Q / (double)n));
+  double K = 0.0;
+  int64_t cnt = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    float a = fabsf(w[i * stride]);
+    if (a > d) {
+      K = K + (double)a;
+      cnt += 1;
+      t[i * tstride] = (int8_t)sign_of(w[i * stride]);
+    } else {
+      t[i * tstride] = 0;
+    }
+  }
+  *alpha = cnt > 0 ? (float)(K / (double)cnt) : 0.0f;
+  *delta = d;
+  return ORC_OK;
+}
+
 int orc_ternarize_group(const float* w, int64_t n, int64_t stride, int method,
                         int8_t* t, int64_t tstride, float* alpha, float* delta) {
   if (!w || !t || !alpha || !delta) return ORC_ERR_NULL;
@@ -117,7 +153,128 @@ int orc_ternarize_group(const float* w, int64_t n, int64_t stride, int method,
     return ternarize_exact(w, n, stride, t, tstride, alpha, delta);
   if (method == ORC_TERN_EXP_LEMMA)
     return ternarize_lemma(w, n, stride, t, tstride, alpha, delta);
+  if (method == ORC_TERN_GAUSS)
+    return ternarize_gauss(w, n, stride, t, tstride, alpha, delta);
   return ORC_ERR_SHAPE;
+}
+
+/*
+ * Eq. (3)-(4): one threshold for the positive weights, I+ = {i : w_i > Dp},
+ * one for the negative ones, I- = {i : w_i < -Dn}, and one scale.  Eq. (4)
+ * gives alpha = (sum_{I+}|w| + sum_{I-}|w|) / (|I+| + |I-|) and the
+ * thresholds maximising the square of that sum over |I+| + |I-|.  Every
+ * distinct pair of kept sets is a pair of prefixes of the positive and of
+ * the negative magnitudes, each sorted in decreasing order (ties by
+ * position), so the exhaustive search visits every pair (a, b), 0 <= a <= n+,
+ * 0 <= b <= n-, a + b >= 1: P_a and N_b are fp64 prefix sums in sorted
+ * order, T = P_a + N_b, f = T*T / (a + b), and the first maximum in the
+ * order (a, then b) with a strict > is kept.  alpha = fp32(T / (a + b));
+ * Dp = the (a+1)-th positive magnitude (0 if all positives are kept), Dn
+ * likewise; t = +1 on the a largest positives, -1 on the b largest negatives.
+ * Zeros are in neither set.  No group has a zero f maximum unless it is all
+ * zeros (then alpha = Dp = Dn = 0, all codes 0).
+ */
+int orc_ternarize_group_asym(const float* w, int64_t n, int64_t stride, int8_t* t,
+                             int64_t tstride, float* alpha, float* delta_p, float* delta_n) {
+  if (!w || !t || !alpha || !delta_p || !delta_n) return ORC_ERR_NULL;
+  if (n < 1) return ORC_ERR_SHAPE;
+  for (int64_t i = 0; i < n; ++i)
+    if (!isfinite(w[i * stride])) return ORC_ERR_NONFINITE;
+  mag_t* pos = (mag_t*)malloc(sizeof(mag_t) * (size_t)n);
+  mag_t* neg = (mag_t*)malloc(sizeof(mag_t) * (size_t)n);
+  double* P = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+  double* N = (double*)malloc(sizeof(double) * (size_t)(n + 1));
+  if (!pos || !neg || !P || !N) {
+    free(pos); free(neg); free(P); free(N);
+    return ORC_ERR_SHAPE;
+  }
+  int64_t np = 0, nn = 0;
+  for (int64_t i = 0; i < n; ++i) {
+    const float v = w[i * stride];
+    if (v > 0.0f) { pos[np].a = v; pos[np].idx = i; ++np; }
+    if (v < 0.0f) { neg[nn].a = -v; neg[nn].idx = i; ++nn; }
+  }
+  qsort(pos, (size_t)np, sizeof(mag_t), cmp_mag);
+  qsort(neg, (size_t)nn, sizeof(mag_t), cmp_mag);
+  P[0] = 0.0;
+  for (int64_t a = 1; a <= np; ++a) P[a] = P[a - 1] + (double)pos[a - 1].a;
+  N[0] = 0.0;
+  for (int64_t b = 1; b <= nn; ++b) N[b] = N[b - 1] + (double)neg[b - 1].a;
+  double bestf = 0.0, bestT = 0.0;
+  int64_t ba = 0, bb = 0;
+  for (int64_t a = 0; a <= np; ++a)
+    for (int64_t b = 0; b <= nn; ++b) {
+      if (a + b == 0) continue;
+      const double T = P[a] + N[b];
+      const double f = (T * T) / (double)(a + b);
+      if (f > bestf) {
+        bestf = f;
+        bestT = T;
+        ba = a;
+        bb = b;
+      }
+    }
+  *alpha = ba + bb > 0 ? (float)(bestT / (double)(ba + bb)) : 0.0f;
+  *delta_p = ba < np ? pos[ba].a : 0.0f;
+  *delta_n = bb < nn ? neg[bb].a : 0.0f;
+  for (int64_t i = 0; i < n; ++i) t[i * tstride] = 0;
+  for (int64_t a = 0; a < ba; ++a) t[pos[a].idx * tstride] = 1;
+  for (int64_t b = 0; b < bb; ++b) t[neg[b].idx * tstride] = -1;
+  free(pos); free(neg); free(P); free(N);
+  return ORC_OK;
+}
+
+static int cmp_float_up(const void* pa, const void* pb) {
+  const float x = *(const float*)pa, y = *(const float*)pb;
+  return x < y ? -1 : (x > y ? 1 : 0);
+}
+
+/*
+ * Sec. 3.1: the Kolmogorov-Smirnov distance of the weight magnitudes to the
+ * two reference laws, each fitted by maximum likelihood: the half-normal law
+ * of N(0, sigma), sigma = rms(W), CDF erf(x / (sigma sqrt 2)); and the
+ * exponential law of scale mu = mean|W| (the 1/lambda of Lemma 1), CDF
+ * 1 - exp(-x / mu).  Computed on at most ORC_KS_SAMPLE magnitudes: every s-th
+ * weight in storage order, s = ceil(n / ORC_KS_SAMPLE).  With the sample
+ * sorted ascending, m_(1) <= ... <= m_(ns): sigma^2 = sum m^2 / ns and
+ * mu = sum m / ns (fp64, ascending order), and
+ * D = max_i max(i/ns - F(m_(i)), F(m_(i)) - (i-1)/ns).  A sample of zeros
+ * gives D = 0 for both.  d[0] = D for the half-normal law, d[1] for the
+ * exponential one.
+ */
+int orc_ks_distances(const float* w, int64_t n, double* d) {
+  if (!w || !d) return ORC_ERR_NULL;
+  if (n < 1) return ORC_ERR_SHAPE;
+  for (int64_t i = 0; i < n; ++i)
+    if (!isfinite(w[i])) return ORC_ERR_NONFINITE;
+  const int64_t step = (n + ORC_KS_SAMPLE - 1) / ORC_KS_SAMPLE;
+  const int64_t ns = (n + step - 1) / step;
+  float* m = (float*)malloc(sizeof(float) * (size_t)ns);
+  if (!m) return ORC_ERR_SHAPE;
+  for (int64_t j = 0; j < ns; ++j) m[j] = fabsf(w[j * step]);
+  qsort(m, (size_t)ns, sizeof(float), cmp_float_up);
+  double Q = 0.0, S = 0.0;
+  for (int64_t j = 0; j < ns; ++j) {
+    const double v = (double)m[j];
+    Q = Q + v * v;
+    S = S + v;
+  }
+  const double sigma = sqrt(Q / (double)ns), mu = S / (double)ns;
+  double dg = 0.0, de = 0.0;
+  if (mu > 0.0) {
+    for (int64_t j = 0; j < ns; ++j) {
+      const double x = (double)m[j];
+      const double hi = (double)(j + 1) / (double)ns, lo = (double)j / (double)ns;
+      const double fg = erf(x / (sigma * sqrt(2.0)));
+      const double fe = 1.0 - exp(-x / mu);
+      dg = fmax(dg, fmax(hi - fg, fg - lo));
+      de = fmax(de, fmax(hi - fe, fe - lo));
+    }
+  }
+  d[0] = dg;
+  d[1] = de;
+  free(m);
+  return ORC_OK;
 }
 
 /*
@@ -135,6 +292,15 @@ int orc_ternarize(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
   const int64_t ng = K / G;
   for (int64_t i = 0; i < O * K; ++i)
     if (!isfinite(w[i])) return ORC_ERR_NONFINITE;
+  if (method == ORC_TERN_KS) {
+    /* Sec. 3.1: the K-S test picks the reference law of the layer, and each
+     * group takes that law's threshold: exponential -> Lemma 1, Gaussian ->
+     * ORC_GAUSS_U * rms (the exponential law only when strictly closer). */
+    double d[2];
+    int rc = orc_ks_distances(w, O * K, d);
+    if (rc != ORC_OK) return rc;
+    method = d[1] < d[0] ? ORC_TERN_EXP_LEMMA : ORC_TERN_GAUSS;
+  }
   for (int64_t o = 0; o < O; ++o)
     for (int32_t r = 0; r < R; ++r)
       for (int32_t s = 0; s < S; ++s)
@@ -526,3 +692,30 @@ int orc_conv2d_w8(const uint8_t* q, int32_t bits, float sx, int64_t B,
 }
 
 int orc_max_threads(void) { return omp_get_max_threads(); }
+
+double orc_gauss_u(void) { return ORC_GAUSS_U; }
+
+/*
+ * Eq. (3)-(4) per group over a layer, grouped as orc_ternarize does.
+ */
+int orc_ternarize_asym(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
+                       int32_t G, int8_t* t, float* alpha, float* delta_p, float* delta_n) {
+  if (!w || !t || !alpha || !delta_p || !delta_n) return ORC_ERR_NULL;
+  if (O < 1 || C < 1 || R < 1 || S < 1) return ORC_ERR_SHAPE;
+  if (G < 1 || C % G != 0) return ORC_ERR_GROUP;
+  const int64_t K = (int64_t)R * S * C;
+  const int64_t ng = K / G;
+  for (int64_t o = 0; o < O; ++o)
+    for (int32_t r = 0; r < R; ++r)
+      for (int32_t s = 0; s < S; ++s)
+        for (int64_t cb = 0; cb < C / G; ++cb) {
+          const float* src = w + ((o * C + cb * G) * R + r) * S + s;
+          const int64_t k0 = ((int64_t)r * S + s) * C + cb * G;
+          const int64_t g = k0 / G;
+          int rc = orc_ternarize_group_asym(src, G, (int64_t)R * S, t + o * K + k0, 1,
+                                            alpha + o * ng + g, delta_p + o * ng + g,
+                                            delta_n + o * ng + g);
+          if (rc != ORC_OK) return rc;
+        }
+  return ORC_OK;
+}

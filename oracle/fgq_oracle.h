@@ -14,7 +14,12 @@
  *                     of Eq. (5) by exhaustive search over the thresholds
  *                     (the "brute-force" solve of Sec. 3.1 / Sec. 4); groups
  *                     are N consecutive input channels at a fixed filter tap
- *                     (Sec. 3.2, Fig. 2).  Method 1 is Lemma 1 (Delta = mean|W|).
+ *                     (Sec. 3.2, Fig. 2).  Method 1 is Lemma 1 (Delta = mean|W|);
+ *                     method 3 the Gaussian-optimal threshold 0.612 rms(W);
+ *                     method 4 picks 1 or 3 per layer by the K-S test (Sec. 3.1).
+ *   orc_ternarize_asym  Eq. (3)-(4): positive and negative thresholds, one
+ *                     scale, solved exhaustively.
+ *   orc_ks_distances  the K-S distances behind method 4.
  *   orc_pack_codes    2-bit storage of ternary codes (4 per byte).
  *   orc_quantize_act  activations quantized to 8 or 4 bits with one scale per
  *                     tensor (Sec. 4, experimental setup).
@@ -34,7 +39,10 @@
  *
  * Parity status: ternarize, quantize, group sums, conv2d and gemm are pinned
  * by the tests (brute-force enumeration, Lemma 1 statistics, closed forms,
- * reduction to a library convolution); see tests/test_oracle_*.py.
+ * reduction to a library convolution); the variants (asymmetric thresholds,
+ * Gaussian threshold, K-S distances and choice) by enumeration, the Eq. (5)
+ * optimum, a root found by scipy, scipy's K-S statistic and large-sample
+ * limits; see tests/test_oracle_*.py.
  *
  * Conventions (shared with the library only by specification, not by code):
  *   weights   fp32 [O][C][R][S]
@@ -65,7 +73,13 @@ enum {
   ORC_ERR_NONFINITE = 5
 };
 
-enum { ORC_TERN_EXACT = 0, ORC_TERN_EXP_LEMMA = 1 };
+enum { ORC_TERN_EXACT = 0, ORC_TERN_EXP_LEMMA = 1, ORC_TERN_GAUSS = 3, ORC_TERN_KS = 4 };
+
+/* Root of 2u(1 - Phi(u)) = phi(u): the Gaussian-optimal threshold of Eq. (5)
+ * in units of sigma (see orc_ternarize_group, method ORC_TERN_GAUSS). */
+#define ORC_GAUSS_U 0.61200318096248076
+/* Sample size of the K-S distances (orc_ks_distances). */
+#define ORC_KS_SAMPLE 16384
 
 /* One group of n weights read at w[i*stride].  Writes t[i*tstride] in
  * {-1,0,1}, *alpha, *delta.  Returns ORC_ERR_NONFINITE on NaN/Inf. */
@@ -73,6 +87,17 @@ int orc_ternarize_group(const float* w, int64_t n, int64_t stride, int method,
                         int8_t* t, int64_t tstride, float* alpha, float* delta);
 
 /* Whole layer.  t is [O][R][S][C] (unpacked codes), alpha/delta [O][K/G]. */
+/* Eq. (3)-(4): asymmetric thresholds Dp, Dn with one alpha, exhaustive over
+ * pairs of prefixes; t in {-1,0,1}.  Returns ORC_ERR_NONFINITE on NaN/Inf. */
+int orc_ternarize_group_asym(const float* w, int64_t n, int64_t stride, int8_t* t,
+                             int64_t tstride, float* alpha, float* delta_p, float* delta_n);
+int orc_ternarize_asym(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
+                       int32_t G, int8_t* t, float* alpha, float* delta_p, float* delta_n);
+/* Sec. 3.1 K-S goodness of fit of |w| (n values, storage order) against the
+ * half-normal (d[0]) and exponential (d[1]) laws fitted by maximum likelihood. */
+int orc_ks_distances(const float* w, int64_t n, double* d);
+/* ORC_GAUSS_U, for the tests. */
+double orc_gauss_u(void);
 int orc_ternarize(const float* w, int64_t O, int64_t C, int32_t R, int32_t S,
                   int32_t G, int32_t method, int8_t* t, float* alpha,
                   float* delta);
