@@ -75,7 +75,14 @@ enum {
 enum {
   FGQ_TERN_EXACT = 0,     /* Eq. (5) solved exactly by exhaustive threshold
                              search (the brute-force solve of Sec. 3.1/4) */
-  FGQ_TERN_EXP_LEMMA = 1  /* Lemma 1: Delta = mean |w| of the group */
+  FGQ_TERN_EXP_LEMMA = 1, /* Lemma 1: Delta = mean |w| of the group */
+  /* 2: the asymmetric thresholds of Eq. (3)-(4), see fgq_ternarize_asym */
+  FGQ_TERN_GAUSS = 3,     /* Delta = 0.612... rms(w) of the group: the
+                             threshold that maximises Eq. (5) in expectation
+                             for Gaussian weights (Sec. 3.1) */
+  FGQ_TERN_KS = 4         /* per layer, FGQ_TERN_EXP_LEMMA or FGQ_TERN_GAUSS,
+                             whichever reference law the Kolmogorov-Smirnov
+                             test finds closer (Sec. 3.1; fgq_ks_distances) */
 };
 
 /* Human-readable name of a status code (static string, never NULL). */
@@ -105,6 +112,13 @@ int64_t fgq_group_count(int64_t O, int64_t K, int32_t G);
  * the J largest and 0 elsewhere.  An all-zero group gets alpha = Delta = 0.
  * Method FGQ_TERN_EXP_LEMMA: Delta = fp32(mean |w|), kept iff |w| > Delta,
  * alpha = fp32(mean of the kept magnitudes) (0 if none).
+ * Method FGQ_TERN_GAUSS: the same with Delta = fp32(u * sqrt(sum w^2 / G))
+ * (fp64, index order), u = 0.61200318096248076, the root of
+ * 2u (1 - Phi(u)) = phi(u) (for w ~ N(0, sigma) the expected objective of
+ * Eq. (5) at the threshold u*sigma is proportional to phi(u)^2/(1 - Phi(u))).
+ * Method FGQ_TERN_KS: FGQ_TERN_EXP_LEMMA for every group if the layer's
+ * exponential K-S distance (fgq_ks_distances over all O*C*R*S weights) is
+ * strictly smaller than the half-normal one, else FGQ_TERN_GAUSS.
  *
  * w      [in]  fp32 [O][C][R][S]
  * codes  [out] fgq_codes_bytes(O, R*S*C) bytes, layout above
@@ -116,6 +130,46 @@ int64_t fgq_group_count(int64_t O, int64_t K, int32_t G);
 fgq_status fgq_ternarize(const float* w, int64_t O, int64_t C, int32_t R,
                          int32_t S, int32_t G, int32_t method, uint8_t* codes,
                          float* alpha, float* delta, void* stream);
+
+/*
+ * fgq_ternarize_asym -- Eq. (3)-(4): per group, one threshold Dp for the
+ * positive weights (kept iff w > Dp) and one Dn for the negative ones (kept
+ * iff w < -Dn), with one scale alpha = (sum of kept |w|) / (number kept),
+ * the thresholds maximising (sum of kept |w|)^2 / (number kept).  Solved
+ * exhaustively: the positive and the negative magnitudes each in decreasing
+ * order (ties by channel), P_a and N_b their fp64 prefix sums, every pair
+ * (a, b) with a + b >= 1 scored f = (P_a + N_b)^2 / (a + b), the first
+ * maximum in the order (a, then b) kept; alpha = fp32((P_a + N_b)/(a + b)),
+ * Dp = the (a+1)-th positive magnitude (0 if all are kept), Dn likewise.  The
+ * maximum equals that of Eq. (5) (for a given count the largest kept sum is
+ * the largest magnitudes, whatever their signs), so codes match
+ * FGQ_TERN_EXACT except where magnitudes tie.
+ *
+ * w, codes, alpha  as for fgq_ternarize
+ * delta_p, delta_n [out] fp32 [O][R*S*C/G] each, or NULL if not wanted
+ * Synchronizes `stream`; FGQ_ERR_NONFINITE on NaN or Inf weights.  Costs
+ * (G/2)^2 steps per group on one lane: meant for groups of up to a few
+ * hundred weights.
+ */
+fgq_status fgq_ternarize_asym(const float* w, int64_t O, int64_t C, int32_t R,
+                              int32_t S, int32_t G, uint8_t* codes, float* alpha,
+                              float* delta_p, float* delta_n, void* stream);
+
+/*
+ * fgq_ks_distances -- Sec. 3.1: the Kolmogorov-Smirnov distance of the weight
+ * magnitudes |w| (n values, any order) to the half-normal law of N(0, sigma),
+ * sigma = rms(w), CDF erf(x / (sigma sqrt 2)), and to the exponential law of
+ * scale mu = mean |w| (the 1/lambda of Lemma 1), CDF 1 - exp(-x / mu), both
+ * fitted by maximum likelihood.  Computed on at most 16384 magnitudes, every
+ * s-th value with s = ceil(n / 16384), sorted ascending m_(1..ns):
+ * sigma^2 = sum m^2 / ns, mu = sum m / ns (fp64, ascending order) and
+ * D = max_i max(i/ns - F(m_(i)), F(m_(i)) - (i-1)/ns).  A sample of zeros
+ * gives 0 for both.
+ *
+ * d [out] device fp64 [2]: D for the half-normal law, then the exponential.
+ * Enqueued on `stream`.  Non-finite weights give unspecified distances.
+ */
+fgq_status fgq_ks_distances(const float* w, int64_t n, double* d, void* stream);
 
 /*
  * fgq_quantize_act -- activations to unsigned `bits` (8 or 4) with one scale

@@ -17,6 +17,8 @@ LIB_PATH = os.path.join(_HERE, "libfgq.so")
 
 FGQ_TERN_EXACT = 0
 FGQ_TERN_EXP_LEMMA = 1
+FGQ_TERN_GAUSS = 3
+FGQ_TERN_KS = 4
 
 _STATUS = {0: "FGQ_OK", 1: "FGQ_ERR_NULL", 2: "FGQ_ERR_SHAPE", 3: "FGQ_ERR_GROUP",
            4: "FGQ_ERR_BITS", 5: "FGQ_ERR_NONFINITE", 6: "FGQ_ERR_HIP",
@@ -42,6 +44,8 @@ _SIGS = {
     "fgq_codes_bytes": ([_I64, _I64], _SZ),
     "fgq_group_count": ([_I64, _I64, _I32], _I64),
     "fgq_ternarize": ([_P, _I64, _I64, _I32, _I32, _I32, _I32, _P, _P, _P, _P], _I32),
+    "fgq_ternarize_asym": ([_P, _I64, _I64, _I32, _I32, _I32, _P, _P, _P, _P, _P], _I32),
+    "fgq_ks_distances": ([_P, _I64, _P, _P], _I32),
     "fgq_quantize_ws_bytes": ([_I64], _SZ),
     "fgq_quantize_act": ([_P, _I64, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
     "fgq_prepared_bytes": ([_I64, _I64, _I32], _SZ),
@@ -130,6 +134,31 @@ def fgq_ternarize(w, G, method=FGQ_TERN_EXACT, want_delta=True):
                              delta.data_ptr() if delta is not None else None, _stream())
     _check(rc, "fgq_ternarize")
     return codes, alpha, delta
+
+
+def fgq_ternarize_asym(w, G):
+    """Eq. (3)-(4) per group.  Returns (codes, alpha, delta_p, delta_n)."""
+    w4 = w if w.dim() == 4 else w.reshape(w.shape[0], w.shape[1], 1, 1)
+    O, C, R, S = w4.shape
+    K = C * R * S
+    pw = _dev(w4, torch.float32, "w")
+    codes = torch.empty((O, (K + 3) // 4), dtype=torch.uint8, device=w.device)
+    ng = K // G if G > 0 and K % G == 0 else 1
+    alpha = torch.empty((O, ng), dtype=torch.float32, device=w.device)
+    dp, dn = torch.empty_like(alpha), torch.empty_like(alpha)
+    rc = lib().fgq_ternarize_asym(pw, O, C, R, S, G, codes.data_ptr(), alpha.data_ptr(), dp.data_ptr(),
+                                  dn.data_ptr(), _stream())
+    _check(rc, "fgq_ternarize_asym")
+    return codes, alpha, dp, dn
+
+
+def fgq_ks_distances(w):
+    """K-S distances of |w| to the fitted half-normal and exponential laws:
+    a device fp64 tensor [D_gauss, D_exp]."""
+    pw = _dev(w, torch.float32, "w")
+    d = torch.empty(2, dtype=torch.float64, device=w.device)
+    _check(lib().fgq_ks_distances(pw, w.numel(), d.data_ptr(), _stream()), "fgq_ks_distances")
+    return d
 
 
 def fgq_quantize_ws_bytes(n):

@@ -134,26 +134,63 @@ int64_t fgq_group_count(int64_t O, int64_t K, int32_t G) {
   return O * (K / G);
 }
 
-fgq_status fgq_ternarize(const float* w, int64_t O, int64_t C, int32_t R, int32_t S, int32_t G,
-                         int32_t method, uint8_t* codes, float* alpha, float* delta,
-                         void* stream) {
-  if (!w || !codes || !alpha) return FGQ_ERR_NULL;
-  if (O < 1 || C < 1 || R < 1 || S < 1) return FGQ_ERR_SHAPE;
-  if (G < 1 || C % G != 0) return FGQ_ERR_GROUP;
-  if (method != FGQ_TERN_EXACT && method != FGQ_TERN_EXP_LEMMA) return FGQ_ERR_UNSUPPORTED;
-  const int64_t K = static_cast<int64_t>(R) * S * C;
-  hipStream_t st = as_stream(stream);
-  fgq_status rc = launch_ternarize(w, O, C, R, S, G, method, codes, alpha, delta, st);
-  if (rc != FGQ_OK) return rc;
-  // Offline step: wait, then report non-finite weights (their groups carry
-  // alpha = NaN).
-  const int64_t ng = O * (K / G);
+namespace {
+
+// Wait for the offline step, then report non-finite weights (their groups
+// carry alpha = NaN).
+fgq_status ternarize_finish(const float* alpha, int64_t ng, hipStream_t st) {
   std::vector<float> host(static_cast<size_t>(ng));
   FGQ_TRY_HIP(hipMemcpyAsync(host.data(), alpha, sizeof(float) * ng, hipMemcpyDeviceToHost, st));
   FGQ_TRY_HIP(hipStreamSynchronize(st));
   for (int64_t i = 0; i < ng; ++i)
     if (host[i] != host[i]) return FGQ_ERR_NONFINITE;
   return FGQ_OK;
+}
+
+}  // namespace
+
+fgq_status fgq_ternarize(const float* w, int64_t O, int64_t C, int32_t R, int32_t S, int32_t G,
+                         int32_t method, uint8_t* codes, float* alpha, float* delta,
+                         void* stream) {
+  if (!w || !codes || !alpha) return FGQ_ERR_NULL;
+  if (O < 1 || C < 1 || R < 1 || S < 1) return FGQ_ERR_SHAPE;
+  if (G < 1 || C % G != 0) return FGQ_ERR_GROUP;
+  if (method != FGQ_TERN_EXACT && method != FGQ_TERN_EXP_LEMMA && method != FGQ_TERN_GAUSS &&
+      method != FGQ_TERN_KS)
+    return FGQ_ERR_UNSUPPORTED;
+  const int64_t K = static_cast<int64_t>(R) * S * C;
+  hipStream_t st = as_stream(stream);
+  if (method == FGQ_TERN_KS) {
+    // the layer's rule by the K-S test, passed through alpha[0] (about to be
+    // overwritten) to the host
+    int32_t pick = 0;
+    fgq_status rc = launch_ks(w, O * K, nullptr, reinterpret_cast<int32_t*>(alpha), st);
+    if (rc != FGQ_OK) return rc;
+    FGQ_TRY_HIP(hipMemcpyAsync(&pick, alpha, sizeof(pick), hipMemcpyDeviceToHost, st));
+    FGQ_TRY_HIP(hipStreamSynchronize(st));
+    method = pick;
+  }
+  fgq_status rc = launch_ternarize(w, O, C, R, S, G, method, codes, alpha, delta, nullptr, st);
+  if (rc != FGQ_OK) return rc;
+  return ternarize_finish(alpha, O * (K / G), st);
+}
+
+fgq_status fgq_ternarize_asym(const float* w, int64_t O, int64_t C, int32_t R, int32_t S, int32_t G,
+                              uint8_t* codes, float* alpha, float* delta_p, float* delta_n, void* stream) {
+  if (!w || !codes || !alpha) return FGQ_ERR_NULL;
+  if (O < 1 || C < 1 || R < 1 || S < 1) return FGQ_ERR_SHAPE;
+  if (G < 1 || C % G != 0) return FGQ_ERR_GROUP;
+  const int64_t K = static_cast<int64_t>(R) * S * C;
+  hipStream_t st = as_stream(stream);
+  fgq_status rc = launch_ternarize(w, O, C, R, S, G, kTernAsym, codes, alpha, delta_p, delta_n, st);
+  if (rc != FGQ_OK) return rc;
+  return ternarize_finish(alpha, O * (K / G), st);
+}
+
+fgq_status fgq_ks_distances(const float* w, int64_t n, double* d, void* stream) {
+  if (!w || !d) return FGQ_ERR_NULL;
+  if (n < 1) return FGQ_ERR_SHAPE;
+  return launch_ks(w, n, d, nullptr, as_stream(stream));
 }
 
 size_t fgq_quantize_ws_bytes(int64_t n) {

@@ -86,10 +86,16 @@ PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G);
 PreparedLayout prepared_layout_dfp(int64_t O, int64_t K, int32_t G);
 
 // Launchers (return FGQ_OK or FGQ_ERR_HIP); arguments already validated.
-fgq_status launch_ternarize(const float* w, int64_t O, int64_t C, int32_t R,
-                            int32_t S, int32_t G, int32_t method,
-                            uint8_t* codes, float* alpha, float* delta,
+fgq_status launch_ternarize(const float* w, int64_t O, int64_t C, int32_t R, int32_t S, int32_t G,
+                            int32_t method, uint8_t* codes, float* alpha, float* delta, float* delta_n,
                             hipStream_t st);
+// Eq. (3)-(4) as a ternarize method (fgq_ternarize_asym; delta = Dp,
+// delta_n = Dn).
+constexpr int32_t kTernAsym = 2;
+// K-S distances (d, nullable device [2]) and the rule they pick (pick,
+// nullable device int32), ternarize.hip; the sample size.
+constexpr int kKsSample = 16384;
+fgq_status launch_ks(const float* w, int64_t n, double* d, int32_t* pick, hipStream_t st);
 fgq_status launch_quantize(const float* x, int64_t n, int32_t bits,
                            const float* scale_in, uint8_t* q, float* scale_out,
                            float* partials, int32_t npart, hipStream_t st);

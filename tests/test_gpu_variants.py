@@ -1,0 +1,104 @@
+"""Ternarization variants on the GPU against the oracle, through the C ABI:
+the asymmetric thresholds of Eq. (3)-(4), the Gaussian-optimal threshold, the
+K-S distances and the per-layer K-S choice (Sec. 3.1).  Codes, scales and
+thresholds must match bit for bit; the K-S distances to 1e-12 (the device's
+erf/exp may differ from the host's in the last bit).
+"""
+import numpy as np
+import pytest
+import torch
+
+import fgq_inputs as fi
+import oracle
+
+fgq = pytest.importorskip("paper_1705_01462_amd")
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def weights(kind, shape, tag):
+    rng = fi.rng("variants", kind, *shape, tag)
+    if kind == "gauss":
+        w = rng.standard_normal(shape)
+    elif kind == "laplace":
+        w = rng.laplace(0.0, 1.0, shape)
+    elif kind == "skewed":
+        w = rng.standard_normal(shape) + 0.5
+    else:  # "ties": a coarse grid, so magnitudes tie across and within signs, with zeros
+        w = np.round(rng.standard_normal(shape) * 2.0) / 2.0
+    return (w * 0.05).astype(np.float32)
+
+
+LAYERS = [
+    # kind, (O, C, R, S), G
+    ("gauss", (32, 64, 3, 3), 4),
+    ("laplace", (16, 128, 1, 1), 64),
+    ("skewed", (24, 32, 3, 3), 8),
+    ("ties", (8, 96, 1, 1), 32),
+    ("laplace", (4, 256, 1, 1), 128),
+    ("ties", (16, 16, 3, 3), 4),
+]
+
+
+@pytest.mark.parametrize("kind,shape,G", LAYERS)
+def test_asym_bit_exact(kind, shape, G):
+    w = weights(kind, shape, "asym")
+    codes, alpha, dp, dn = fgq.fgq_ternarize_asym(dev(w), G)
+    t, a, rp, rn = oracle.ternarize_asym(w, G)
+    np.testing.assert_array_equal(host(codes), oracle.pack_codes(t))
+    np.testing.assert_array_equal(host(alpha).view(np.uint32), a.view(np.uint32))
+    np.testing.assert_array_equal(host(dp).view(np.uint32), rp.view(np.uint32))
+    np.testing.assert_array_equal(host(dn).view(np.uint32), rn.view(np.uint32))
+
+
+@pytest.mark.parametrize("kind,shape,G", LAYERS)
+def test_gauss_rule_bit_exact(kind, shape, G):
+    w = weights(kind, shape, "gauss")
+    codes, alpha, delta = fgq.fgq_ternarize(dev(w), G, fgq.FGQ_TERN_GAUSS)
+    t, a, d = oracle.ternarize(w, G, oracle.GAUSS)
+    np.testing.assert_array_equal(host(codes), oracle.pack_codes(t))
+    np.testing.assert_array_equal(host(alpha).view(np.uint32), a.view(np.uint32))
+    np.testing.assert_array_equal(host(delta).view(np.uint32), d.view(np.uint32))
+
+
+@pytest.mark.parametrize("kind,shape", [("gauss", (64, 64, 3, 3)), ("laplace", (64, 64, 3, 3)),
+                                        ("gauss", (10, 100, 1, 1)), ("ties", (7, 33, 1, 1))])
+def test_ks_distances(kind, shape):
+    w = weights(kind, shape, "ks")
+    d = host(fgq.fgq_ks_distances(dev(w)))
+    dg, de = oracle.ks_distances(w)
+    assert abs(d[0] - dg) < 1e-12 and abs(d[1] - de) < 1e-12
+
+
+@pytest.mark.parametrize("kind", ["gauss", "laplace"])
+def test_ks_method_bit_exact(kind):
+    shape = (64, 64, 3, 3)  # more weights than the K-S sample: every 3rd is used
+    w = weights(kind, shape, "ksm")
+    dg, de = oracle.ks_distances(w)
+    assert abs(dg - de) > 1e-9  # the choice is not a near-tie
+    codes, alpha, delta = fgq.fgq_ternarize(dev(w), 4, fgq.FGQ_TERN_KS)
+    t, a, d = oracle.ternarize(w, 4, oracle.KS)
+    np.testing.assert_array_equal(host(codes), oracle.pack_codes(t))
+    np.testing.assert_array_equal(host(alpha).view(np.uint32), a.view(np.uint32))
+    np.testing.assert_array_equal(host(delta).view(np.uint32), d.view(np.uint32))
+
+
+def test_variants_reject_non_finite():
+    w = weights("gauss", (4, 16, 1, 1), "nan")
+    w[2, 5, 0, 0] = np.nan
+    with pytest.raises(RuntimeError):
+        fgq.fgq_ternarize_asym(dev(w), 4)
+    w[2, 5, 0, 0] = np.inf
+    for m in (fgq.FGQ_TERN_GAUSS, fgq.FGQ_TERN_KS):
+        with pytest.raises(RuntimeError):
+            fgq.fgq_ternarize(dev(w), 4, m)
