@@ -8,8 +8,12 @@
 // atomics, no zero-initialised state and no host synchronisation.  Both
 // passes issue all of a thread's loads before using any of them (pass 2
 // also before the partials are reduced), so each costs about one memory
-// round trip plus its bytes.  Each pass-2 thread turns 16 (u8) or 32 (u4)
-// values into one 16-byte store.
+// round trip plus its bytes (a thread requests all of its partials at once:
+// one loop load at a time cost a round trip each).  For uint8 codes from
+// aligned buffers, pass 2 reads one contiguous kilobyte per wave-wide load
+// and stores four codes per lane (quantize8_coalesced_kernel: 6.3 -> 4.9 us
+// on a 12.8 MB input); otherwise each pass-2 thread turns 16 (u8) or 32
+// (u4) consecutive values into one 16-byte store.
 //
 // The codes (qcode.h) use the correctly rounded quotient x/s from the
 // reciprocal and one exact correction rather than the full division
@@ -38,6 +42,23 @@ __device__ inline float block_max(float v, float* red) {
 #pragma unroll
   for (int i = 1; i < kThreads / 64; ++i) m = fmaxf(m, red[i]);
   return m;
+}
+
+// The largest of pass 1's partial maxima: every thread requests its (up to
+// kMaxPartials / kThreads) partials at once through a range-checked buffer
+// (reads past npart return 0, neutral for maxima of non-negative values),
+// so the reduction costs one round trip, then one block reduction.
+__device__ inline float partials_max(const float* partials, int32_t npart, float* red) {
+  const __amdgpu_buffer_rsrc_t rs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(partials), 0, 4 * npart, 0x00020000);
+  float p[kMaxPartials / kThreads];
+#pragma unroll
+  for (int u = 0; u < kMaxPartials / kThreads; ++u)
+    p[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, 4 * (threadIdx.x + kThreads * u), 0, 0));
+  float m = 0.0f;
+#pragma unroll
+  for (int u = 0; u < kMaxPartials / kThreads; ++u) m = fmaxf(m, p[u]);
+  return block_max(m, red);
 }
 
 template <bool kAligned>
@@ -104,9 +125,7 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
   if (scale_in) {
     s = *scale_in;
   } else {
-    float m = 0.0f;
-    for (int i = threadIdx.x; i < npart; i += kThreads) m = fmaxf(m, partials[i]);
-    m = block_max(m, red);
+    const float m = partials_max(partials, npart, red);
     s = m > 0.0f ? m / qmax : 1.0f;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = s;
@@ -156,6 +175,51 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
   });
 }
 
+// Pass 2 for uint8 codes from 16-byte aligned x and q: each wave-wide load
+// is one contiguous kilobyte of x (lane l takes float4 number 256*i + 64*w
+// + l of the block's 1024, i = 0..3), and each code word of four values is
+// stored where it belongs (a contiguous 256 bytes per wave-wide store).
+__global__ __launch_bounds__(kThreads) void quantize8_coalesced_kernel(
+    const float* __restrict__ x, int64_t n, const float* __restrict__ scale_in,
+    const float* __restrict__ partials, int32_t npart, uint8_t* __restrict__ q,
+    float* __restrict__ scale_out) {
+  __shared__ float red[kThreads / 64];
+  constexpr int kVec = 4;  // float4 per thread
+  const int64_t n4 = n / 4;
+  const int64_t f0 = static_cast<int64_t>(blockIdx.x) * kThreads * kVec + threadIdx.x;
+  const v4f* x4 = reinterpret_cast<const v4f*>(x);
+  v4f v[kVec];
+#pragma unroll
+  for (int i = 0; i < kVec; ++i) {
+    const int64_t f = f0 + static_cast<int64_t>(i) * kThreads;
+    v[i] = f < n4 ? __builtin_nontemporal_load(&x4[f]) : v4f{0.0f, 0.0f, 0.0f, 0.0f};
+  }
+  float s;
+  if (scale_in) {
+    s = *scale_in;
+  } else {
+    const float m = partials_max(partials, npart, red);
+    s = m > 0.0f ? m / 255.0f : 1.0f;
+  }
+  if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = s;
+  const QScale qs = make_qscale(s, 8);
+  with_rcp(qs, [&](auto rcp) {
+    auto code = [&](float val) { return qcode<decltype(rcp)::value>(val, qs); };
+    uint32_t* q32 = reinterpret_cast<uint32_t*>(q);
+#pragma unroll
+    for (int i = 0; i < kVec; ++i) {
+      const int64_t f = f0 + static_cast<int64_t>(i) * kThreads;
+      if (f < n4) {
+        const uint32_t word = code(v[i].x) | (code(v[i].y) << 8) | (code(v[i].z) << 16) | (code(v[i].w) << 24);
+        __builtin_nontemporal_store(word, q32 + f);
+      }
+    }
+    // the tail (n % 4 values), one byte per thread of the first block
+    const int64_t done = n4 * 4;
+    if (blockIdx.x == 0 && threadIdx.x < n - done) q[done + threadIdx.x] = static_cast<uint8_t>(code(x[done + threadIdx.x]));
+  });
+}
+
 int64_t pass2_blocks(int64_t n, int32_t bits) {
   const int64_t per = bits == 8 ? 16 : 32;
   int64_t b = ceil_div(n / per, kThreads);
@@ -183,6 +247,14 @@ fgq_status launch_quantize(const float* x, int64_t n, int32_t bits,
     else
       hipLaunchKernelGGL(absmax_partial_kernel<false>, dim3(npart), dim3(kThreads), 0, st, x, n, partials);
     if (last_launch() != FGQ_OK) return FGQ_ERR_HIP;
+  }
+  if (bits == 8 && aligned) {
+    const int64_t b8 = ceil_div(n / 4, static_cast<int64_t>(kThreads) * 4);
+    const dim3 g8(static_cast<uint32_t>(b8 < 1 ? 1 : b8));
+    if (b8 > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+    hipLaunchKernelGGL(quantize8_coalesced_kernel, g8, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q,
+                       scale_out);
+    return last_launch();
   }
   const int64_t blocks = pass2_blocks(n, bits);
   if (blocks > 0x7fffffffLL) return FGQ_ERR_SHAPE;
