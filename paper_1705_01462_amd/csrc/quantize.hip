@@ -11,9 +11,9 @@
 // round trip plus its bytes (a thread requests all of its partials at once:
 // one loop load at a time cost a round trip each).  For uint8 codes from
 // aligned buffers, pass 2 reads one contiguous kilobyte per wave-wide load
-// and stores four codes per lane (quantize8_coalesced_kernel: 6.3 -> 4.9 us
-// on a 12.8 MB input); otherwise each pass-2 thread turns 16 (u8) or 32
-// (u4) consecutive values into one 16-byte store.
+// and stores four codes per lane (quantize_coalesced_kernel: 6.3 -> 4.9 us
+// on a 12.8 MB input to uint8); from unaligned buffers each pass-2 thread
+// turns 16 (u8) or 32 (u4) consecutive values into codes byte by byte.
 //
 // The codes (qcode.h) use the correctly rounded quotient x/s from the
 // reciprocal and one exact correction rather than the full division
@@ -175,11 +175,13 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
   });
 }
 
-// Pass 2 for uint8 codes from 16-byte aligned x and q: each wave-wide load
-// is one contiguous kilobyte of x (lane l takes float4 number 256*i + 64*w
-// + l of the block's 1024, i = 0..3), and each code word of four values is
-// stored where it belongs (a contiguous 256 bytes per wave-wide store).
-__global__ __launch_bounds__(kThreads) void quantize8_coalesced_kernel(
+// Pass 2 from 16-byte aligned x and q: each wave-wide load is one
+// contiguous kilobyte of x (lane l takes float4 number 256*i + 64*w + l of
+// the block's 1024, i = 0..3), and the codes of those four values are
+// stored where they belong (4 bytes for uint8, 2 for uint4: a contiguous
+// 256 or 128 bytes per wave-wide store).
+template <int kBits>
+__global__ __launch_bounds__(kThreads) void quantize_coalesced_kernel(
     const float* __restrict__ x, int64_t n, const float* __restrict__ scale_in,
     const float* __restrict__ partials, int32_t npart, uint8_t* __restrict__ q,
     float* __restrict__ scale_out) {
@@ -199,24 +201,33 @@ __global__ __launch_bounds__(kThreads) void quantize8_coalesced_kernel(
     s = *scale_in;
   } else {
     const float m = partials_max(partials, npart, red);
-    s = m > 0.0f ? m / 255.0f : 1.0f;
+    s = m > 0.0f ? m / (kBits == 8 ? 255.0f : 15.0f) : 1.0f;
   }
   if (blockIdx.x == 0 && threadIdx.x == 0) *scale_out = s;
-  const QScale qs = make_qscale(s, 8);
+  const QScale qs = make_qscale(s, kBits);
   with_rcp(qs, [&](auto rcp) {
     auto code = [&](float val) { return qcode<decltype(rcp)::value>(val, qs); };
-    uint32_t* q32 = reinterpret_cast<uint32_t*>(q);
 #pragma unroll
     for (int i = 0; i < kVec; ++i) {
       const int64_t f = f0 + static_cast<int64_t>(i) * kThreads;
       if (f < n4) {
-        const uint32_t word = code(v[i].x) | (code(v[i].y) << 8) | (code(v[i].z) << 16) | (code(v[i].w) << 24);
-        __builtin_nontemporal_store(word, q32 + f);
+        if constexpr (kBits == 8) {
+          const uint32_t word = code(v[i].x) | (code(v[i].y) << 8) | (code(v[i].z) << 16) | (code(v[i].w) << 24);
+          __builtin_nontemporal_store(word, reinterpret_cast<uint32_t*>(q) + f);
+        } else {
+          const uint32_t half = code(v[i].x) | (code(v[i].y) << 4) | (code(v[i].z) << 8) | (code(v[i].w) << 12);
+          __builtin_nontemporal_store(static_cast<uint16_t>(half), reinterpret_cast<uint16_t*>(q) + f);
+        }
       }
     }
-    // the tail (n % 4 values), one byte per thread of the first block
+    // the tail (n % 4 values; n is even for uint4), by the first block
     const int64_t done = n4 * 4;
-    if (blockIdx.x == 0 && threadIdx.x < n - done) q[done + threadIdx.x] = static_cast<uint8_t>(code(x[done + threadIdx.x]));
+    if (blockIdx.x == 0) {
+      if (kBits == 8 && threadIdx.x < n - done)
+        q[done + threadIdx.x] = static_cast<uint8_t>(code(x[done + threadIdx.x]));
+      if (kBits == 4 && threadIdx.x == 0 && n - done == 2)
+        q[done / 2] = static_cast<uint8_t>(code(x[done]) | (code(x[done + 1]) << 4));
+    }
   });
 }
 
@@ -248,28 +259,27 @@ fgq_status launch_quantize(const float* x, int64_t n, int32_t bits,
       hipLaunchKernelGGL(absmax_partial_kernel<false>, dim3(npart), dim3(kThreads), 0, st, x, n, partials);
     if (last_launch() != FGQ_OK) return FGQ_ERR_HIP;
   }
-  if (bits == 8 && aligned) {
-    const int64_t b8 = ceil_div(n / 4, static_cast<int64_t>(kThreads) * 4);
-    const dim3 g8(static_cast<uint32_t>(b8 < 1 ? 1 : b8));
-    if (b8 > 0x7fffffffLL) return FGQ_ERR_SHAPE;
-    hipLaunchKernelGGL(quantize8_coalesced_kernel, g8, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q,
-                       scale_out);
+  if (aligned) {
+    const int64_t bc = ceil_div(n / 4, static_cast<int64_t>(kThreads) * 4);
+    if (bc > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+    const dim3 gc(static_cast<uint32_t>(bc < 1 ? 1 : bc));
+    if (bits == 8)
+      hipLaunchKernelGGL(quantize_coalesced_kernel<8>, gc, dim3(kThreads), 0, st, x, n, scale_in, partials, npart,
+                         q, scale_out);
+    else
+      hipLaunchKernelGGL(quantize_coalesced_kernel<4>, gc, dim3(kThreads), 0, st, x, n, scale_in, partials, npart,
+                         q, scale_out);
     return last_launch();
   }
   const int64_t blocks = pass2_blocks(n, bits);
   if (blocks > 0x7fffffffLL) return FGQ_ERR_SHAPE;
   const dim3 grid(static_cast<uint32_t>(blocks));
-  if (bits == 8) {
-    if (aligned)
-      hipLaunchKernelGGL((quantize_kernel<8, true>), grid, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q, scale_out);
-    else
-      hipLaunchKernelGGL((quantize_kernel<8, false>), grid, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q, scale_out);
-  } else {
-    if (aligned)
-      hipLaunchKernelGGL((quantize_kernel<4, true>), grid, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q, scale_out);
-    else
-      hipLaunchKernelGGL((quantize_kernel<4, false>), grid, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q, scale_out);
-  }
+  if (bits == 8)
+    hipLaunchKernelGGL((quantize_kernel<8, false>), grid, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q,
+                       scale_out);
+  else
+    hipLaunchKernelGGL((quantize_kernel<4, false>), grid, dim3(kThreads), 0, st, x, n, scale_in, partials, npart, q,
+                       scale_out);
   return last_launch();
 }
 
