@@ -577,6 +577,21 @@ def fused_entry(L, G, bits, r, ops):
             "roofline": roofline(L, G, bits, r["conv_fused_us"], out_bits=bits)}
 
 
+def profile_fc(torch, fgq, fi, M, K, O, G, steps):
+    """For profilers: `steps` eager calls of fgq_gemm_dfp_ws (8-bit scales,
+    uint8 activations, fp32 output) on one prepared M x K x O layer."""
+    w = fi.gauss_weights(O, K, 0.01, "fc", K, O)
+    codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
+    prep = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, G, 8)
+    q, sx = fgq.fgq_quantize_act(torch.from_numpy(fi.relu_gauss((M, K), "fc")).cuda(), 8)
+    y = torch.empty((M, O), dtype=torch.float32, device="cuda")
+    ws = torch.empty(max(fgq.fgq_gemm_ws_bytes(M, K, O, G, True), 4), dtype=torch.uint8, device="cuda")
+    for _ in range(steps):
+        fgq.fgq_gemm_dfp_ws(q, 8, sx, M, K, codes, prep, O, G, out=y, ws=ws)
+    torch.cuda.synchronize()
+    log(f"[bench] profile fc M={M} K={K} O={O} G={G}: {steps} eager calls done")
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -595,6 +610,9 @@ def main():
                     help="layer configurations for --profile-steps")
     ap.add_argument("--profile-fused", action="store_true",
                     help="with --profile-steps: each step also runs fgq_conv2d_q (8-bit output codes)")
+    ap.add_argument("--profile-fc", default="",
+                    help="with --profile-steps: instead of the conv layers, call fgq_gemm_dfp_ws on a "
+                         "fully-connected layer given as M,K,O,G")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); the FGQ layer is "
@@ -614,7 +632,8 @@ def main():
     ops = 2.0 * M * LAYER["O"] * K
 
     if args.profile_steps:
-        for name in args.layers.split(","):
+        fc = [int(v) for v in args.profile_fc.split(",")] if args.profile_fc else None
+        for name in ([] if fc else args.layers.split(",")):
             L, G = CONFIGS[name]
             st = Setup(torch, fgq, fi, L, G, bits, 4, folded=not args.direct)
             if args.profile_fused:
@@ -626,6 +645,8 @@ def main():
             torch.cuda.synchronize()
             log(f"[bench] profile {name} ({layer_key(L, G)}): {args.profile_steps} eager steps done")
             del st
+        if fc:
+            profile_fc(torch, fgq, fi, *fc, args.profile_steps)
         # calibration: one plain device copy of known size (FETCH_SIZE and
         # WRITE_SIZE of this dispatch give the counter-to-bytes factor)
         src = torch.ones(CALIB_COPY_BYTES // 4, dtype=torch.float32, device="cuda")
