@@ -356,7 +356,7 @@ size_t fgq_gemm_ws_bytes(int64_t M, int64_t K, int64_t O, int32_t G, int32_t fix
   int32_t sps = 0;
   int32_t splits = splitk_splits(M, K, O, &sps);
   if (splits <= 1) splits = 0;
-  if (fixed_point && dfpx_shape_ok(M, K, O, G)) splits = std::max(splits, dfpx_splits(M, K, O, G, &sps));
+  if (dfpx_shape_ok(M, K, O, G)) splits = std::max(splits, dfpx_splits(M, K, O, G, &sps));
   return static_cast<size_t>(splits) * (fixed_point ? 1 : 3) * static_cast<size_t>(M * O) * 4;
 }
 
@@ -372,11 +372,15 @@ fgq_status fgq_gemm_ws(const uint8_t* q, int32_t bits, const float* sx, int64_t 
   if (!layer_out(out_bits, out_scale, out, O, &lo, &err)) return err;
   if (prepared && reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
   if (prepared && prepared_layout(O, K, G).kind == kPrepFold && fold_supported(g, q)) {
+    const bool ws_ok = ws && reinterpret_cast<uintptr_t>(ws) % 4 == 0 && ws_bytes >= fgq_gemm_ws_bytes(M, K, O, G, 0);
+    if (dfpx_supported(g, q)) {  // weights read as codes + scale digits
+      if (!ws_ok) return FGQ_ERR_WORKSPACE;
+      return launch_foldx_splitk(q, sx, prepared, g, lo, static_cast<int32_t*>(ws), as_stream(stream));
+    }
     int32_t sps = 0;
     const int32_t splits = splitk_splits(M, K, O, &sps);
     if (splits > 1) {
-      if (!ws || reinterpret_cast<uintptr_t>(ws) % 4 != 0 || ws_bytes < fgq_gemm_ws_bytes(M, K, O, G, 0))
-        return FGQ_ERR_WORKSPACE;
+      if (!ws_ok) return FGQ_ERR_WORKSPACE;
       return launch_fold_splitk(q, sx, prepared, g, lo, splits, sps, static_cast<int32_t*>(ws),
                                 as_stream(stream));
     }

@@ -23,6 +23,7 @@
 #include <limits.h>
 
 #include "fgq_internal.h"
+#include "xlayout.h"
 
 // Every floating-point expression here is evaluated exactly as written.
 #pragma clang fp contract(off)
@@ -131,12 +132,6 @@ __device__ inline int64_t frag_offset1(int64_t nks, int64_t o, int64_t k) {
   return ((tile * nks + ks) * 2 + half) * 1024 + lane * 16 + (kk % 16);
 }
 
-// Offset of lane (channel o, half hf) of 128-wide K step ks in the
-// expanding GEMM's order: [O/128][Kp/128][4 waves][64 lanes][per-lane bytes].
-__device__ inline int64_t xfrag_lane(int64_t nk, int64_t o, int64_t ks, int hf) {
-  return ((o / 128 * nk + ks) * 4 + (o % 128) / 32) * 64 + o % 32 + 32 * hf;
-}
-
 // One block per channel of the padded channel range (O32 for the plane,
 // O128 for the expanding GEMM's regions when xnb > 0).
 __global__ __launch_bounds__(kThreads) void prepare_dfp_kernel(
@@ -154,25 +149,14 @@ __global__ __launch_bounds__(kThreads) void prepare_dfp_kernel(
   const int64_t rb = ceil_div(K, 4);
   auto code = [&](int64_t k) -> uint32_t { return k < K ? (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u : 0u; };
 
-  // Expanding GEMM order.  Codes: lane (o, hf) of step ks holds k = 128*ks +
-  // 64*hf + [0, 64) in 16 bytes; byte 4h+b holds, at bits 2i, the code of
-  // k = 128*ks + 64*hf + 16h + 4i + b.  Scale codes: xnb bytes per lane, byte
-  // j the code A of the group of k = 128*ks + 64*hf + G*j (G = 128: of 128*ks).
+  // The expanding GEMM's order (xlayout.h): the codes, and the scale codes A.
   if (xnb > 0) {
     const int64_t nk = Kp / 128;
-    for (int64_t e = threadIdx.x; e < nk * 32; e += kThreads) {
-      const int64_t ks = e / 32;
-      const int hf = static_cast<int>((e % 32) / 16), B = static_cast<int>(e % 16);
-      const int64_t k0 = 128 * ks + 64 * hf + 16 * (B / 4) + B % 4;
-      uint32_t v = 0;
-      if (live)
-        for (int i = 0; i < 4; ++i) v |= code(k0 + 4 * i) << (2 * i);
-      xcodes[xfrag_lane(nk, o, ks, hf) * 16 + B] = static_cast<uint8_t>(v);
-    }
+    write_xcodes(codes, o, K, Kp, live, xcodes);
     for (int64_t e = threadIdx.x; e < nk * 2 * xnb; e += kThreads) {
       const int64_t ks = e / (2 * xnb);
       const int hf = static_cast<int>((e / xnb) % 2), j = static_cast<int>(e % xnb);
-      const int64_t k = G >= 128 ? 128 * ks : 128 * ks + 64 * hf + static_cast<int64_t>(G) * j;
+      const int64_t k = xscale_k(ks, hf, j, G);
       const int A = (live && k < K) ? dfp_code(alpha[o * ng + k / G], fl, bits) : 0;
       xacodes[xfrag_lane(nk, o, ks, hf) * xnb + j] = static_cast<int8_t>(A);
     }

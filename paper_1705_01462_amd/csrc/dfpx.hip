@@ -53,24 +53,35 @@ constexpr int kSteps = 8;  // K steps per split at most (LDS: kNB * 32 KB)
 struct DfpxArgs {
   const uint8_t* q;       // activations [M][K] (uint8) or [M][K/2] (uint4)
   const uint8_t* xcodes;  // codes, expanding-GEMM order
-  const int8_t* xacodes;  // scale codes, same order
-  const int32_t* bias;    // [O]   128 * sum_k A*t (uint8 offset term)
-  int32_t* part;          // [splits][M][O]
+  const int8_t* xacodes;  // per plane: scale codes (or scale digits), same order
+  const int32_t* bias;    // [planes][O]  128 * sum_k (weight of the plane) (uint8 offset term)
+  int32_t* part;          // [splits][planes][M][O]
   int32_t M, K, O, n_otiles, n_mtiles, splits, sps, nk, staged;
-  int32_t q_bytes, xcodes_bytes, xacodes_bytes;
+  int32_t q_bytes, xcodes_bytes, xacodes_bytes, xplane;  // xplane: bytes between planes
 };
 
+// Permute selectors of a quarter's 16 weights: word i, byte b = the code of
+// weight 4i+b.
+__device__ inline void selectors(uint32_t c32, uint32_t (&s)[4]) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) s[i] = (c32 >> (2 * i)) & 0x03030303u;
+}
+
+// The quarter's int8 weights for scale bytes a (A, or a digit of it, in
+// [-127, 127]): table [0, a, 0, -a] per group, indexed by the selectors.
+// -a is formed four bytes at a time as ((a ^ 0x7F7F7F7F) + 0x01010101) ^
+// 0x80808080 (one's complement of a + 128, plus one, minus 128), with no
+// carry between bytes because no byte is -128.
 template <int kG>
-__device__ inline v4i expand16(uint32_t c32, uint32_t a) {
-  const uint32_t na = (0x80808080u - a) ^ 0x80808080u;  // per byte: -A
+__device__ inline v4i expand16(const uint32_t (&s)[4], uint32_t a) {
+  const uint32_t na = ((a ^ 0x7F7F7F7Fu) + 0x01010101u) ^ 0x80808080u;  // per byte: -a
   v4i w;
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    const uint32_t j = kG == 4 ? i : (kG == 8 ? i / 2 : 0);  // the A byte of weights 4i..4i+3
-    // table bytes [0, A_j, 0, -A_j]; selector 12 gives a zero byte
+    const uint32_t j = kG == 4 ? i : (kG == 8 ? i / 2 : 0);  // the scale byte of weights 4i..4i+3
+    // table bytes [0, a_j, 0, -a_j]; selector 12 gives a zero byte
     const uint32_t T = __builtin_amdgcn_perm(na, a, 0x0Cu | (j << 8) | (0x0Cu << 16) | ((4u + j) << 24));
-    const uint32_t s = (c32 >> (2 * i)) & 0x03030303u;  // byte b: the code of weight 4i+b
-    w[i] = static_cast<int>(__builtin_amdgcn_perm(0u, T, s));
+    w[i] = static_cast<int>(__builtin_amdgcn_perm(0u, T, s[i]));
   }
   return w;
 }
@@ -109,12 +120,12 @@ struct ACodes {
   }
 };
 
-template <int kNB>
-constexpr int wg_threads() { return kNB == 2 ? 512 : 256; }
+template <int kNB, int kPlanes>
+constexpr int wg_threads() { return kNB == 2 || kPlanes == 3 ? 512 : 256; }
 
-template <int kBits, int kG, int kNB>
-__global__ __launch_bounds__(wg_threads<kNB>(), 2) void dfpx_gemm_kernel(DfpxArgs a) {
-  constexpr int kWG = wg_threads<kNB>();
+template <int kBits, int kG, int kNB, int kPlanes>
+__global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_kernel(DfpxArgs a) {
+  constexpr int kWG = wg_threads<kNB, kPlanes>();
   constexpr int kSets = kWG / 256;                    // wave sets sharing the steps
   constexpr int kRows = 32 * kNB;
   constexpr int kStageB = kRows * kRowB;              // one step's activations
@@ -137,12 +148,14 @@ __global__ __launch_bounds__(wg_threads<kNB>(), 2) void dfpx_gemm_kernel(DfpxArg
   // The uint8 offset term of the lane's channel (split 0, first half only),
   // requested first so that no wait for it follows the weight loads.
   const bool ocok = oc < a.O;
-  int bj = 0;
+  int bj[kPlanes] = {};
   if constexpr (kBits == 8) {
     const __amdgpu_buffer_rsrc_t brs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.bias), 0, 4 * a.O, kBufFlags);
-    bj = static_cast<int>(
-        __builtin_amdgcn_raw_buffer_load_b32(brs, ocok && ks0 == 0 && sh == 0 ? 4 * oc : kOutOfRange, 0, 0));
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.bias), 0, 4 * kPlanes * a.O, kBufFlags);
+#pragma unroll
+    for (int j = 0; j < kPlanes; ++j)
+      bj[j] = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(
+          brs, ocok && ks0 == 0 && sh == 0 ? 4 * (j * a.O + oc) : kOutOfRange, 0, 0));
   }
 
   // ---- activation slice: piece p = tid + 512*i is row p / (8*kSteps),
@@ -177,13 +190,14 @@ __global__ __launch_bounds__(wg_threads<kNB>(), 2) void dfpx_gemm_kernel(DfpxArg
   const int lane0 = ((tile % a.n_otiles) * a.nk + ks0) * 256 + 64 * wo + lane;  // lane index of step ks0
   constexpr int kAB = ACodes<kG>::kBytes;
   v4i cw[kHalf];
-  ACodes<kG> aw[kHalf];
+  ACodes<kG> aw[kPlanes][kHalf];
 #pragma unroll
   for (int s = 0; s < kHalf; ++s) {
     const int st = kHalf * sh + s;
     const int ln = lane0 + 256 * (st < nsteps ? st : nsteps - 1);
     cw[s] = __builtin_amdgcn_raw_buffer_load_b128(crs, 16 * ln, 0, 0);
-    aw[s].load(ars, kAB * ln);
+#pragma unroll
+    for (int j = 0; j < kPlanes; ++j) aw[j][s].load(ars, j * a.xplane + kAB * ln);
   }
   __builtin_amdgcn_sched_barrier(0);
 
@@ -205,11 +219,13 @@ __global__ __launch_bounds__(wg_threads<kNB>(), 2) void dfpx_gemm_kernel(DfpxArg
   }
   __syncthreads();
 
-  v16i acc[kNB];
+  v16i acc[kPlanes][kNB];
 #pragma unroll
-  for (int c = 0; c < kNB; ++c)
+  for (int j = 0; j < kPlanes; ++j)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) acc[c][r] = bj;
+    for (int c = 0; c < kNB; ++c)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[j][c][r] = bj[j];
   int afrag[kNB][4];
 #pragma unroll
   for (int c = 0; c < kNB; ++c)
@@ -223,11 +239,16 @@ __global__ __launch_bounds__(wg_threads<kNB>(), 2) void dfpx_gemm_kernel(DfpxArg
     const unsigned char* base = lds + st * kStageB;
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
-      const v4i wf = expand16<kG>(static_cast<uint32_t>(cw[s][h]), aw[s].quarter(h));
+      uint32_t sel[4];
+      selectors(static_cast<uint32_t>(cw[s][h]), sel);
+      v4i xf[kNB];
 #pragma unroll
-      for (int c = 0; c < kNB; ++c) {
-        const v4i xf = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
-        acc[c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf, wf, acc[c], 0, 0, 0);
+      for (int c = 0; c < kNB; ++c) xf[c] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+#pragma unroll
+      for (int j = 0; j < kPlanes; ++j) {
+        const v4i wf = expand16<kG>(sel, aw[j][s].quarter(h));
+#pragma unroll
+        for (int c = 0; c < kNB; ++c) acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], wf, acc[j][c], 0, 0, 0);
       }
     }
   }
@@ -241,73 +262,101 @@ __global__ __launch_bounds__(wg_threads<kNB>(), 2) void dfpx_gemm_kernel(DfpxArg
     const int row = 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
     return reinterpret_cast<int*>(lds + row * kPitch + 4 * (32 * wo + lane % 32));
   };
-  int32_t* const part = a.part + static_cast<int64_t>(split) * a.M * a.O;
-  if (kSets == 1 && !a.staged) {
-    if (!ocok) return;
 #pragma unroll
-    for (int c = 0; c < kNB; ++c)
+  for (int j = 0; j < kPlanes; ++j) {
+    int32_t* const part = a.part + (static_cast<int64_t>(split) * kPlanes + j) * a.M * a.O;
+    if (kSets == 1 && !a.staged) {
+      if (ocok) {
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
-        if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = acc[c][r];
+        for (int c = 0; c < kNB; ++c)
+#pragma unroll
+          for (int r = 0; r < 16; ++r) {
+            const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
+            if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = acc[j][c][r];
+          }
       }
-    return;
-  }
-  __syncthreads();
-  if (sh == 0) {
-#pragma unroll
-    for (int c = 0; c < kNB; ++c)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) *at(c, r) = acc[c][r];
-  }
-  if constexpr (kSets == 2) {
-    __syncthreads();
-    if (sh == 1) {
+      continue;
+    }
+    __syncthreads();  // the slice (or the previous plane's tile) is no longer read
+    if (sh == 0) {
 #pragma unroll
       for (int c = 0; c < kNB; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r)
-          __hip_atomic_fetch_add(at(c, r), acc[c][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+        for (int r = 0; r < 16; ++r) *at(c, r) = acc[j][c][r];
     }
-    if (!a.staged) {
+    if constexpr (kSets == 2) {
       __syncthreads();
-      if (sh != 0 || !ocok) return;
+      if (sh == 1) {
 #pragma unroll
-      for (int c = 0; c < kNB; ++c)
+        for (int c = 0; c < kNB; ++c)
 #pragma unroll
-        for (int r = 0; r < 16; ++r) {
-          const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
-          if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = *at(c, r);
+          for (int r = 0; r < 16; ++r)
+            __hip_atomic_fetch_add(at(c, r), acc[j][c][r], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_WORKGROUP);
+      }
+      if (!a.staged) {
+        __syncthreads();
+        if (sh == 0 && ocok) {
+#pragma unroll
+          for (int c = 0; c < kNB; ++c)
+#pragma unroll
+            for (int r = 0; r < 16; ++r) {
+              const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
+              if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = *at(c, r);
+            }
         }
-      return;
+        continue;
+      }
     }
-  }
-  // this split's raw sums, [split][m][o], as 16-byte pieces of rows
-  __syncthreads();
-  const int o0 = (tile % a.n_otiles) * 128;
+    // this split's raw sums of plane j, [split][j][m][o], as 16-byte pieces of rows
+    __syncthreads();
+    const int o0 = (tile % a.n_otiles) * 128;
 #pragma unroll
-  for (int t = tid; t < kRows * 32; t += kWG) {
-    const int row = t / 32, ch = o0 + 4 * (t % 32);
-    const int m = m0 + row;
-    if (m < a.M && ch < a.O)
-      *reinterpret_cast<v4i*>(part + static_cast<int64_t>(m) * a.O + ch) =
-          *reinterpret_cast<const v4i*>(lds + row * kPitch + 16 * (t % 32));
+    for (int t = tid; t < kRows * 32; t += kWG) {
+      const int row = t / 32, ch = o0 + 4 * (t % 32);
+      const int m = m0 + row;
+      if (m < a.M && ch < a.O)
+        *reinterpret_cast<v4i*>(part + static_cast<int64_t>(m) * a.O + ch) =
+            *reinterpret_cast<const v4i*>(lds + row * kPitch + 16 * (t % 32));
+    }
   }
 }
 
-template <int kBits, int kNB>
+template <int kBits, int kNB, int kPlanes>
 fgq_status launch_g(const DfpxArgs& a, int G, hipStream_t st) {
   const dim3 grid(static_cast<uint32_t>(a.n_otiles * a.n_mtiles * a.splits));
-  constexpr int kWG = wg_threads<kNB>();
+  constexpr int kWG = wg_threads<kNB, kPlanes>();
   switch (G) {
-    case 4: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 4, kNB>), grid, dim3(kWG), 0, st, a); break;
-    case 8: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 8, kNB>), grid, dim3(kWG), 0, st, a); break;
-    case 16: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 16, kNB>), grid, dim3(kWG), 0, st, a); break;
-    case 32: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 32, kNB>), grid, dim3(kWG), 0, st, a); break;
-    case 64: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 64, kNB>), grid, dim3(kWG), 0, st, a); break;
-    default: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 128, kNB>), grid, dim3(kWG), 0, st, a); break;
+    case 4: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 4, kNB, kPlanes>), grid, dim3(kWG), 0, st, a); break;
+    case 8: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 8, kNB, kPlanes>), grid, dim3(kWG), 0, st, a); break;
+    case 16: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 16, kNB, kPlanes>), grid, dim3(kWG), 0, st, a); break;
+    case 32: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 32, kNB, kPlanes>), grid, dim3(kWG), 0, st, a); break;
+    case 64: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 64, kNB, kPlanes>), grid, dim3(kWG), 0, st, a); break;
+    default: hipLaunchKernelGGL((dfpx_gemm_kernel<kBits, 128, kNB, kPlanes>), grid, dim3(kWG), 0, st, a); break;
   }
   return last_launch();
+}
+
+template <int kPlanes>
+fgq_status launch_planes(const DfpxArgs& a, int bits, int nb, int G, hipStream_t st) {
+  return bits == 8 ? (nb == 1 ? launch_g<8, 1, kPlanes>(a, G, st) : launch_g<8, 2, kPlanes>(a, G, st))
+                   : (nb == 1 ? launch_g<4, 1, kPlanes>(a, G, st) : launch_g<4, 2, kPlanes>(a, G, st));
+}
+
+// Arguments shared by the two layouts; the caller fills in the pointers.
+DfpxArgs make_args(const uint8_t* q, const ConvGeom& g, int32_t* ws, int nb) {
+  DfpxArgs a;
+  a.q = q;
+  a.part = ws;
+  a.M = static_cast<int32_t>(g.M);
+  a.K = static_cast<int32_t>(g.K);
+  a.O = static_cast<int32_t>(g.O);
+  a.n_otiles = static_cast<int32_t>(ceil_div(g.O, 128));
+  a.n_mtiles = static_cast<int32_t>(ceil_div(g.M, 32 * nb));
+  a.splits = dfpx_splits(g.M, g.K, g.O, g.G, &a.sps);
+  a.nk = static_cast<int32_t>(round_up(g.K, 128) / 128);
+  a.staged = g.O % 4 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0;
+  a.q_bytes = static_cast<int32_t>(g.bits == 8 ? g.M * g.K : g.M * g.K / 2);
+  return a;
 }
 
 }  // namespace
@@ -344,29 +393,37 @@ fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const void* pre
   const PreparedLayout L = prepared_layout_dfp(g.O, g.K, g.G);
   const char* base = static_cast<const char*>(prepared);
   const int nb = g.M <= 32 ? 1 : 2;
-  DfpxArgs a;
-  a.q = q;
+  DfpxArgs a = make_args(q, g, ws, nb);
   a.xcodes = reinterpret_cast<const uint8_t*>(base + L.xcodes_off);
   a.xacodes = reinterpret_cast<const int8_t*>(base + L.xacodes_off);
   a.bias = reinterpret_cast<const int32_t*>(base + L.bias_off);
-  a.part = ws;
-  a.M = static_cast<int32_t>(g.M);
-  a.K = static_cast<int32_t>(g.K);
-  a.O = static_cast<int32_t>(g.O);
-  a.n_otiles = static_cast<int32_t>(ceil_div(g.O, 128));
-  a.n_mtiles = static_cast<int32_t>(ceil_div(g.M, 32 * nb));
-  a.splits = dfpx_splits(g.M, g.K, g.O, g.G, &a.sps);
-  a.nk = static_cast<int32_t>(L.Kp / 128);
-  a.staged = g.O % 4 == 0 && reinterpret_cast<uintptr_t>(ws) % 16 == 0;
-  a.q_bytes = static_cast<int32_t>(g.bits == 8 ? g.M * g.K : g.M * g.K / 2);
   a.xcodes_bytes = static_cast<int32_t>(L.xacodes_off - L.xcodes_off);
   a.xacodes_bytes = static_cast<int32_t>(L.total - L.xacodes_off);
+  a.xplane = 0;
   if (static_cast<int64_t>(a.n_otiles) * a.n_mtiles * a.splits > 0x7fffffffLL) return FGQ_ERR_SHAPE;
-  fgq_status rc = g.bits == 8 ? (nb == 1 ? launch_g<8, 1>(a, g.G, st) : launch_g<8, 2>(a, g.G, st))
-                              : (nb == 1 ? launch_g<4, 1>(a, g.G, st) : launch_g<4, 2>(a, g.G, st));
+  fgq_status rc = launch_planes<1>(a, g.bits, nb, g.G, st);
   if (rc != FGQ_OK) return rc;
   return launch_splitk_reduce(ws, a.splits, /*dfp=*/true, g.M, g.O, sx, nullptr,
                               reinterpret_cast<const int32_t*>(base), out, st);
+}
+
+fgq_status launch_foldx_splitk(const uint8_t* q, const float* sx, const void* prepared,
+                               const ConvGeom& g, const LayerOut& out, int32_t* ws, hipStream_t st) {
+  const PreparedLayout L = prepared_layout(g.O, g.K, g.G);
+  const char* base = static_cast<const char*>(prepared);
+  const int nb = g.M <= 32 ? 1 : 2;
+  DfpxArgs a = make_args(q, g, ws, nb);
+  a.xcodes = reinterpret_cast<const uint8_t*>(base + L.xcodes_off);
+  a.xacodes = reinterpret_cast<const int8_t*>(base + L.xacodes_off);
+  a.bias = reinterpret_cast<const int32_t*>(base + L.bias_off);
+  a.xcodes_bytes = static_cast<int32_t>(L.xacodes_off - L.xcodes_off);
+  a.xacodes_bytes = static_cast<int32_t>(L.total - L.xacodes_off);
+  a.xplane = static_cast<int32_t>(round_up(g.O, 128) * (L.Kp / 64) * dfpx_acode_bytes(g.G));
+  if (static_cast<int64_t>(a.n_otiles) * a.n_mtiles * a.splits > 0x7fffffffLL) return FGQ_ERR_SHAPE;
+  fgq_status rc = launch_planes<3>(a, g.bits, nb, g.G, st);
+  if (rc != FGQ_OK) return rc;
+  return launch_splitk_reduce(ws, a.splits, /*dfp=*/false, g.M, g.O, sx,
+                              reinterpret_cast<const float*>(base + L.scale_off), nullptr, out, st);
 }
 
 }  // namespace fgq

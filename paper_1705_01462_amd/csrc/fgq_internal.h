@@ -54,6 +54,9 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 //               [O32/32][Kp/64][3 planes][2 K halves][64 lanes][16 bytes]
 //      bias   : int32 [3][O]  128 * sum_k plane_j[o][k] (uint8 offset term)
 //      scale  : fp32  [O]     2^-E_o
+//      xcodes, xacodes (G a power of two in 4..128): the 2-bit codes and the
+//               three digits of each group's scale in the codes-expanding
+//               GEMM's order (xlayout.h; digits plane-major)
 // A third kind is written by fgq_prepare_weights_dfp (any G), for the layer
 // with fixed-point group scales:
 //      header : int32 fl, the fractional length of the layer's scales
@@ -155,6 +158,10 @@ bool dfpx_supported(const ConvGeom& g, const uint8_t* q);
 int32_t dfpx_splits(int64_t M, int64_t K, int64_t O, int32_t G, int32_t* steps_per_split);
 fgq_status launch_dfpx_splitk(const uint8_t* q, const float* sx, const void* prepared,
                               const ConvGeom& g, const LayerOut& out, int32_t* ws, hipStream_t st);
+// The same kernel on the folded layout (fp32 scales as three int8 digit
+// planes), int32 sums in ws [splits][3][M][O], the folded reduction.
+fgq_status launch_foldx_splitk(const uint8_t* q, const float* sx, const void* prepared,
+                               const ConvGeom& g, const LayerOut& out, int32_t* ws, hipStream_t st);
 fgq_status launch_splitk_reduce(const int32_t* part, int32_t splits, bool dfp, int64_t M, int64_t O,
                                 const float* sx, const float* scale, const int32_t* fl, const LayerOut& out,
                                 hipStream_t st);

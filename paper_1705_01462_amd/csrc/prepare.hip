@@ -19,8 +19,12 @@
 //
 // One block per output channel (channels padded to a multiple of 32 get
 // zero planes): max alpha -> E_o, then digits, planes (written in the
-// fragment order of the matrix-core kernel) and the per-plane sums.
+// fragment order of the matrix-core kernel) and the per-plane sums.  For G
+// a power of two in 4..128 the layout also holds the 2-bit codes and each
+// group's three digits in the codes-expanding GEMM's order (xlayout.h;
+// digits plane-major, [3][O128 * Kp/64 * xnb]), for GEMMs at small batch.
 #include "fgq_internal.h"
+#include "xlayout.h"
 
 // Every floating-point expression here is evaluated exactly as written.
 #pragma clang fp contract(off)
@@ -43,8 +47,11 @@ PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G) {
     L.kind = kPrepFold;
     L.bias_off = round_up(3 * L.O32 * L.Kp, 256);
     L.scale_off = round_up(L.bias_off + 12 * O, 256);
-    L.total = round_up(L.scale_off + 4 * O, 256);
-    L.alpha_off = L.xcodes_off = L.xacodes_off = L.total;
+    const int64_t xnb = dfpx_acode_bytes(G), O128 = round_up(O, 128);
+    L.xcodes_off = round_up(L.scale_off + 4 * O, 256);
+    L.xacodes_off = round_up(L.xcodes_off + (xnb > 0 ? O128 * L.Kp / 4 : 0), 256);
+    L.total = round_up(L.xacodes_off + 3 * O128 * (L.Kp / 64) * xnb, 256);
+    L.alpha_off = L.total;
   }
   return L;
 }
@@ -74,14 +81,24 @@ __device__ inline int64_t frag_offset(int64_t nks, int j, int64_t o, int64_t k) 
 __global__ __launch_bounds__(kThreads) void prepare_kernel(
     const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O,
     int64_t K, int32_t G, int64_t Kp, int8_t* __restrict__ planes,
-    int32_t* __restrict__ bias, float* __restrict__ scale) {
+    int32_t* __restrict__ bias, float* __restrict__ scale, uint8_t* __restrict__ xcodes,
+    int8_t* __restrict__ xdigits, int32_t xnb) {
   __shared__ float redf[kThreads / 64];
   __shared__ int64_t redi[3][kThreads / 64];
   const int64_t o = blockIdx.x;
   const int64_t nks = Kp / kFoldKStep;
-  if (o >= O) {  // padding channel of the last 32-channel tile
-    for (int64_t k = threadIdx.x; k < Kp; k += kThreads)
-      for (int j = 0; j < 3; ++j) planes[frag_offset(nks, j, o, k)] = 0;
+  const int64_t nk = Kp / 128, xplane = round_up(O, 128) * nk * 2 * xnb;  // digit plane stride
+  if (o >= O) {  // padding channel of the last 32- (or 128-) channel tile
+    if (o < round_up(O, 32))
+      for (int64_t k = threadIdx.x; k < Kp; k += kThreads)
+        for (int j = 0; j < 3; ++j) planes[frag_offset(nks, j, o, k)] = 0;
+    if (xnb > 0) {
+      write_xcodes(codes, o, K, Kp, false, xcodes);
+      for (int64_t e = threadIdx.x; e < nk * 2 * xnb; e += kThreads) {
+        const int64_t ln = xfrag_lane(nk, o, e / (2 * xnb), static_cast<int>((e / xnb) % 2));
+        for (int j = 0; j < 3; ++j) xdigits[j * xplane + ln * xnb + e % xnb] = 0;
+      }
+    }
     return;
   }
   const int64_t ng = K / G;
@@ -107,6 +124,19 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
     if (E < -126) E = -126;
   }
   const double two_e = ldexp(1.0, E);
+
+  if (xnb > 0) {
+    write_xcodes(codes, o, K, Kp, true, xcodes);
+    for (int64_t e = threadIdx.x; e < nk * 2 * xnb; e += kThreads) {
+      const int64_t ks = e / (2 * xnb);
+      const int hf = static_cast<int>((e / xnb) % 2), jb = static_cast<int>(e % xnb);
+      const int64_t k = xscale_k(ks, hf, jb, G);
+      int d[3] = {0, 0, 0};
+      if (k < K) digits_of(static_cast<int64_t>(rint(static_cast<double>(alpha[o * ng + k / G]) * two_e)), d);
+      const int64_t ln = xfrag_lane(nk, o, ks, hf);
+      for (int j = 0; j < 3; ++j) xdigits[j * xplane + ln * xnb + jb] = static_cast<int8_t>(d[j]);
+    }
+  }
 
   int64_t s[3] = {0, 0, 0};
   for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
@@ -178,10 +208,14 @@ fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O, i
                        reinterpret_cast<float*>(base + L.alpha_off));
     return last_launch();
   }
-  hipLaunchKernelGGL(prepare_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0, st, codes,
+  const int32_t xnb = static_cast<int32_t>(dfpx_acode_bytes(G));
+  const int64_t nblk = xnb > 0 ? round_up(O, 128) : L.O32;
+  hipLaunchKernelGGL(prepare_kernel, dim3(static_cast<uint32_t>(nblk)), dim3(kThreads), 0, st, codes,
                      alpha, O, K, G, L.Kp, reinterpret_cast<int8_t*>(base + L.planes_off),
                      reinterpret_cast<int32_t*>(base + L.bias_off),
-                     reinterpret_cast<float*>(base + L.scale_off));
+                     reinterpret_cast<float*>(base + L.scale_off),
+                     reinterpret_cast<uint8_t*>(base + L.xcodes_off),
+                     reinterpret_cast<int8_t*>(base + L.xacodes_off), xnb);
   return last_launch();
 }
 

@@ -137,7 +137,12 @@ def test_gemm_ws_bytes():
     # the weight bytes: min(512/32, 72/2, 9216/(16*64)) = 9 -> 8 steps each, 9 splits
     assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 4, 0) == 9 * 3 * 64 * 4096 * 4
     assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 4, 1) == 9 * 1 * 64 * 4096 * 4
-    assert L.fgq_gemm_ws_bytes(64, 256, 128, 4, 0) == 0          # too few steps
+    # the codes-expanding GEMM (M <= 64, K % 16 == 0, G a power of two in
+    # 4..128) always writes sums per split: splits of up to 8 steps
+    assert L.fgq_gemm_ws_bytes(64, 256, 128, 4, 0) == 1 * 3 * 64 * 128 * 4
+    assert L.fgq_gemm_ws_bytes(64, 256, 128, 4, 1) == 1 * 1 * 64 * 128 * 4
+    assert L.fgq_gemm_ws_bytes(64, 264, 128, 4, 0) == 0          # K % 16 != 0, too few steps
+    assert L.fgq_gemm_ws_bytes(65, 256, 128, 4, 0) == 0          # M > 64, too few steps
     assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 64, 0) == 0        # per-group layout: no split
     assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 64, 1) > 0
     assert L.fgq_gemm_ws_bytes(64, 9216, 4096, 5, 0) == 0         # G does not divide K

@@ -71,6 +71,9 @@ def test_folded_gemm_at_max_k(extreme):
         assert np.all(qr == 255) and np.all(np.abs(t) == 1)
     mag = summand_mag(qr.reshape(M, K), sr, t, a, G)
     assert np.all(np.abs(y.astype(np.float64) - y_ref) <= 1e-5 * mag)
+    # the codes-expanding kernel (split K) gives the same integer sums
+    y_ws = host(fgq.fgq_gemm_ws(q, 8, sx, M, K, codes, alpha, O, G, prepared=prep))
+    np.testing.assert_array_equal(y_ws.view(np.uint32), y.view(np.uint32))
 
 
 def test_folded_gemm_past_max_k_falls_back_exact():

@@ -117,6 +117,22 @@ def test_gemm_dfp_ws_codes_path(case):
         np.testing.assert_array_equal(got, ref)
 
 
+@pytest.mark.parametrize("case", DFPX_CASES)
+def test_gemm_ws_codes_path_equals_unsplit(case):
+    # fp32 scales: the expanding kernel on the folded layout (three digit
+    # planes) must give the unsplit kernel's integer sums and epilogue
+    M, K, O, G, bits = case
+    w, x, codes, alpha, q, sx = setup(*case, tag=("x3", case))
+    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+    y = host(fgq.fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
+    y_ws = host(fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
+    np.testing.assert_array_equal(y_ws.view(np.uint32), y.view(np.uint32))
+    sc = dev(np.array([np.float32(0.9 * float(np.abs(y).max()) / 255)], np.float32))
+    a = host(fgq.fgq_gemm_q(q, bits, sx, M, K, codes, alpha, O, G, 8, sc, prepared=prep))
+    b = host(fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep, out_bits=8, out_scale=sc))
+    np.testing.assert_array_equal(a.ravel(), b.ravel())
+
+
 def test_gemm_ws_missing_workspace_and_no_split():
     M, K, O, G, bits = CASES[0]
     w, x, codes, alpha, q, sx = setup(M, K, O, G, bits, "ws")
