@@ -359,13 +359,18 @@ fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx,
  * fgq_gemm_ws the folded layout, i.e. G != 64 or K/64 > 160), the K steps
  * are divided among workgroups that write their int32 sums to `ws`, and a
  * second kernel adds them in a fixed order and applies the usual epilogue.
- * fgq_gemm_dfp_ws with G in {4, 8, 16, 32, 64, 128} reads the weights as
- * the 2-bit codes and the scale codes A and expands them in registers.
+ * With M <= 64, K % 16 == 0 and G in {4, 8, 16, 32, 64, 128} (and, for
+ * fgq_gemm_ws, the folded layout) the kernel reads the weights as the 2-bit
+ * codes plus, per group, the scale code A (fgq_gemm_dfp_ws) or the three
+ * digits of the scale (fgq_gemm_ws), all stored by the prepare call in the
+ * kernel's operand order, and expands them to int8 weights in registers;
+ * such shapes always use the workspace.
  *   out_bits / out_scale / out  as for fgq_conv2d_dfp
  *   ws        [tmp] device buffer of fgq_gemm_ws_bytes(M, K, O, G,
- *                   fixed_point) bytes (4-byte aligned; fixed_point = 1
- *                   for fgq_gemm_dfp_ws), not kept between calls; may be
- *                   NULL when that size is 0 (K is then not split).
+ *                   fixed_point) bytes (4-byte aligned, 16-byte aligned
+ *                   for the fastest stores; fixed_point = 1 for
+ *                   fgq_gemm_dfp_ws), not kept between calls; may be NULL
+ *                   when that size is 0 (K is then not split).
  * FGQ_ERR_WORKSPACE if a needed workspace is missing or too small.  The
  * split depends on the device's compute-unit count: query the size on the
  * device that runs the call.
