@@ -61,6 +61,18 @@ def test_asym_bit_exact(kind, shape, G):
     np.testing.assert_array_equal(host(dn).view(np.uint32), rn.view(np.uint32))
 
 
+def test_asym_exact_tie_on_gpu():
+    # the exact objective tie of the oracle's worked example, in every group
+    w = np.tile(np.array([3, -1, -1, -1], np.float32), (8, 4)).reshape(8, 16, 1, 1)
+    codes, alpha, dp, dn = fgq.fgq_ternarize_asym(dev(w), 4)
+    t, a, rp, rn = oracle.ternarize_asym(w, 4)
+    assert np.all(a == 3) and np.all(rn == 1)
+    np.testing.assert_array_equal(host(codes), oracle.pack_codes(t))
+    np.testing.assert_array_equal(host(alpha), a)
+    np.testing.assert_array_equal(host(dp), rp)
+    np.testing.assert_array_equal(host(dn), rn)
+
+
 @pytest.mark.parametrize("kind,shape,G", LAYERS)
 def test_gauss_rule_bit_exact(kind, shape, G):
     w = weights(kind, shape, "gauss")

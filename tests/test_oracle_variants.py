@@ -81,6 +81,13 @@ def test_asym_all_zero_and_one_sided():
     assert list(t) == [1, 0, 1, 0] and a == np.float32(2.5) and dp == 1 and dn == 0
 
 
+def test_asym_tie_keeps_first_maximum():
+    # f(1, 0) = 3^2/1 = 9 and f(1, 3) = (3+1+1+1)^2/4 = 9 tie exactly (every
+    # other pair scores less); the first maximum in (a, then b) order wins
+    t, a, dp, dn = oracle.ternarize_group_asym(np.array([3, -1, -1, -1], np.float32))
+    assert list(t) == [1, 0, 0, 0] and a == 3 and dp == 0 and dn == 1
+
+
 def test_asym_layer_grouping_matches_groups():
     rng = np.random.default_rng(3)
     w = rng.standard_normal((3, 8, 2, 2)).astype(np.float32)
