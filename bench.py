@@ -303,6 +303,11 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
             sets.append((x, q, sx, ws, y))
         q_outs = [torch.empty(M * O * bits // 8, dtype=torch.uint8, device="cuda") for _ in range(nsets)]
         out_scale = torch.ones(1, dtype=torch.float32, device="cuda")
+        # the fully-connected layer (a 1x1 layer on a 1x1 map) runs as the
+        # GEMM at small batch: K split over workgroups, weights read as codes
+        fc = H == 1 and W == 1 and R == 1 and S == 1
+        ws_fc = torch.empty(max(fgq.fgq_gemm_ws_bytes(M, K, O, g, False), 4), dtype=torch.uint8, device="cuda")
+        ws_fc_dfp = torch.empty(max(fgq.fgq_gemm_ws_bytes(M, K, O, g, True), 4), dtype=torch.uint8, device="cuda")
 
         def quant(i):
             x, q, sx, ws, y = sets[i]
@@ -310,15 +315,26 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
 
         def conv(i):
             x, q, sx, ws, y = sets[i]
+            if fc:
+                fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, g, prepared=prep, out=y.view(M, O), ws=ws_fc)
+                return
             fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, prepared=prep, y=y)
 
         def conv_q(i):
             x, q, sx, ws, y = sets[i]
+            if fc:
+                fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, g, prepared=prep, out_bits=bits,
+                                out_scale=out_scale, out=q_outs[i], ws=ws_fc)
+                return
             fgq.fgq_conv2d_q(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, g, bits, out_scale,
                              prepared=prep, q_out=q_outs[i])
 
         def conv_dfp_q(i):
             x, q, sx, ws, y = sets[i]
+            if fc:
+                fgq.fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prep_dfp, O, g, bits, out_scale, out=q_outs[i],
+                                    ws=ws_fc_dfp)
+                return
             if prep_w8 is not None:
                 fgq.fgq_conv2d_w8(q, bits, sx, (B, H, W, C), prep_w8, O, R, S, st, pd, bits, out_scale,
                                   out=q_outs[i])
