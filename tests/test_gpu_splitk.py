@@ -133,6 +133,26 @@ def test_gemm_ws_codes_path_equals_unsplit(case):
     np.testing.assert_array_equal(a.ravel(), b.ravel())
 
 
+@pytest.mark.parametrize("fixed_point", [True, False])
+def test_codes_path_with_unaligned_workspace(fixed_point):
+    # a workspace 4-byte but not 16-byte aligned: sums leave from registers
+    M, K, O, G, bits = 48, 2048, 256, 4, 8
+    w, x, codes, alpha, q, sx = setup(M, K, O, G, bits, tag=("ua", fixed_point))
+    nb = fgq.fgq_gemm_ws_bytes(M, K, O, G, fixed_point)
+    big = torch.empty(nb + 16, dtype=torch.uint8, device="cuda")
+    ws = big[4:4 + nb]
+    assert ws.data_ptr() % 16 == 4
+    if fixed_point:
+        prep = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, G, 8)
+        ref = host(fgq.fgq_gemm_dfp(q, bits, sx, M, K, codes, prep, O, G))
+        got = host(fgq.fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prep, O, G, ws=ws))
+    else:
+        prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+        ref = host(fgq.fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
+        got = host(fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep, ws=ws))
+    np.testing.assert_array_equal(got.view(np.uint32), ref.view(np.uint32))
+
+
 def test_gemm_ws_missing_workspace_and_no_split():
     M, K, O, G, bits = CASES[0]
     w, x, codes, alpha, q, sx = setup(M, K, O, G, bits, "ws")
