@@ -61,6 +61,12 @@ __device__ inline float partials_max(const float* partials, int32_t npart, float
   return block_max(m, red);
 }
 
+// Pass 1.  Aligned input: block b reads the 1024-float4 chunks b, b + grid,
+// ... (one chunk when the grid covers the input), lane l of wave w taking
+// float4 number 256*i + 64*w + l of a chunk: the same chunk-to-block mapping
+// as quantize_coalesced_kernel, so that each chunk is read by the same XCD
+// in both passes (workgroup b runs on XCD b % 8; the grid is a multiple of 8
+// when it loops) and pass 2 finds it in that XCD's L2.
 template <bool kAligned>
 __global__ __launch_bounds__(kThreads) void absmax_partial_kernel(
     const float* __restrict__ x, int64_t n, float* __restrict__ partials) {
@@ -71,11 +77,12 @@ __global__ __launch_bounds__(kThreads) void absmax_partial_kernel(
   if (kAligned) {
     const v4f* x4 = reinterpret_cast<const v4f*>(x);
     const int64_t n4 = n / 4;
-    for (int64_t base = tid; base < n4; base += stride * kP1Vec) {
+    const int64_t nch = ceil_div(n4, static_cast<int64_t>(kThreads) * kP1Vec);
+    for (int64_t c = blockIdx.x; c < nch; c += gridDim.x) {
       v4f v[kP1Vec];
 #pragma unroll
       for (int u = 0; u < kP1Vec; ++u) {
-        const int64_t i = base + u * stride;
+        const int64_t i = c * kThreads * kP1Vec + static_cast<int64_t>(u) * kThreads + threadIdx.x;
         v[u] = i < n4 ? x4[i] : v4f{0.0f, 0.0f, 0.0f, 0.0f};
       }
 #pragma unroll
