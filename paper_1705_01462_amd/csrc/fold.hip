@@ -30,6 +30,7 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
+  if (fold_rows_eligible(a)) return launch_fold_rows(a, g.bits, out.bits, st);
   switch (out.bits) {
     case 0: return launch_fold_out_f32(a, g.bits, st);
     case 8: return launch_fold_out_q8(a, g.bits, st);

@@ -79,6 +79,10 @@ fgq_status launch_fold_dfp_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q4(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_part(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_part(const FoldArgs& a, int bits, hipStream_t st);
+// Short reductions (K <= 128) over many row tiles, fp32 group scales: the
+// row-walking kernel of fold_rows.h, same results.
+bool fold_rows_eligible(const FoldArgs& a);
+fgq_status launch_fold_rows(const FoldArgs& a, int bits, int out_bits, hipStream_t st);
 
 namespace {
 
