@@ -257,7 +257,7 @@ def stack_layers(fi, depth, batch):
     return out
 
 
-def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
+def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=50):
     """Per-layer kernel times of a batch-`batch` ResNet-`depth` stack, every
     distinct layer timed at its full shape (graph replays over `nsets`
     rotating buffer sets) and counted with its multiplicity.  Inputs are
@@ -404,7 +404,7 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=10):
             "per_layer": layers}
 
 
-def alexnet_measure(torch, fgq, fi, batch=64, G=4, bits=8, nsets=3, reps=10):
+def alexnet_measure(torch, fgq, fi, batch=64, G=4, bits=8, nsets=3, reps=50):
     """The AlexNet-shaped layers at batch `batch`, G=4, uint8: each layer timed
     at its full shape (graph replays over rotating sets) two ways: ternary
     weights with fp32 group scales and fp32 output (fgq_conv2d; the
