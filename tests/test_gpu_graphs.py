@@ -1,9 +1,10 @@
 """The hot path captured in a HIP graph (as the benchmark runs it): every
 replay, with eager work and synchronizations in between, must reproduce the
 eager results bit for bit.  Covers the dynamic-scale quantization (two
-passes), the folded and per-group convolutions, the fused 8-bit output, the
-fixed-point convolution, and the split-K GEMMs with their reduction (none of
-them may record a memset).
+passes), the folded and per-group convolutions, the row-walking folded
+kernel (a 1x1 layer with K = 64 over many row tiles), the fused 8-bit
+output, the fixed-point convolution, and the split-K GEMMs with their
+reduction (none of them may record a memset).
 """
 import numpy as np
 import pytest
@@ -34,6 +35,12 @@ def test_graph_replays_match_eager():
     pf = fgq.fgq_prepare_weights(cf, af, OF, KF, GF)
     pfd = fgq.fgq_prepare_weights_dfp(cf, af, OF, KF, GF, 8)
     xf = torch.from_numpy(fi.relu_gauss((M, KF), "graph-fc")).cuda()
+    # a 1x1 layer with K = 64 and 1568 row/channel tiles: the row-walking kernel
+    BR, HR, CR, OR = 16, 56, 64, 256
+    wr = fi.he_weights(OR, CR, 1, 1, "graph-rows", 4)
+    cr, ar, _ = fgq.fgq_ternarize(torch.from_numpy(wr).cuda(), 4)
+    pr = fgq.fgq_prepare_weights(cr, ar, OR, CR, 4)
+    xr = torch.from_numpy(fi.relu_gauss((BR, HR, HR, CR), "graph-rows")).cuda()
 
     n = x.numel()
     q = torch.empty(n, dtype=torch.uint8, device="cuda")
@@ -42,6 +49,9 @@ def test_graph_replays_match_eager():
     qf = torch.empty(xf.numel(), dtype=torch.uint8, device="cuda")
     sxf = torch.empty(1, device="cuda")
     wsf = torch.empty(fgq.fgq_quantize_ws_bytes(xf.numel()), dtype=torch.uint8, device="cuda")
+    qr = torch.empty(xr.numel(), dtype=torch.uint8, device="cuda")
+    sxr = torch.empty(1, device="cuda")
+    wsr = torch.empty(fgq.fgq_quantize_ws_bytes(xr.numel()), dtype=torch.uint8, device="cuda")
     osc = torch.full((1,), 0.05, device="cuda")
     Ho = H
     for key in ("y4", "y64", "yd4", "yd64"):
@@ -49,6 +59,8 @@ def test_graph_replays_match_eager():
     outs["q8"] = torch.empty(B * Ho * Ho * O, dtype=torch.uint8, device="cuda")
     outs["gf"] = torch.empty((M, OF), device="cuda")
     outs["gfd"] = torch.empty((M, OF), device="cuda")
+    outs["yr"] = torch.empty((BR, HR, HR, OR), device="cuda")
+    outs["qr8"] = torch.empty(BR * HR * HR * OR, dtype=torch.uint8, device="cuda")
     wsg = torch.empty(max(fgq.fgq_gemm_ws_bytes(M, KF, OF, GF, False), 4), dtype=torch.uint8, device="cuda")
     wsgd = torch.empty(max(fgq.fgq_gemm_ws_bytes(M, KF, OF, GF, True), 4), dtype=torch.uint8, device="cuda")
 
@@ -64,6 +76,10 @@ def test_graph_replays_match_eager():
                          q_out=outs["q8"])
         fgq.fgq_gemm_ws(qf, 8, sxf, M, KF, cf, af, OF, GF, prepared=pf, out=outs["gf"], ws=wsg)
         fgq.fgq_gemm_dfp_ws(qf, 8, sxf, M, KF, cf, pfd, OF, GF, out=outs["gfd"], ws=wsgd)
+        fgq.fgq_quantize_act(xr, 8, q=qr, scale_out=sxr, ws=wsr)
+        fgq.fgq_conv2d(qr, 8, sxr, (BR, HR, HR, CR), cr, ar, OR, 1, 1, 1, 0, 4, prepared=pr, y=outs["yr"])
+        fgq.fgq_conv2d_q(qr, 8, sxr, (BR, HR, HR, CR), cr, ar, OR, 1, 1, 1, 0, 4, 8, osc, prepared=pr,
+                         q_out=outs["qr8"])
 
     step()
     torch.cuda.synchronize()
