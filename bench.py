@@ -244,6 +244,53 @@ def cpu_baseline(fi, L, G, bits, budget_s=15.0):
             "seconds": round(t_total, 3)}
 
 
+def measured_peaks(torch, fgq, reps=5):
+    """Measured peaks beside the published ones: the int8 matrix-instruction
+    rate (fgq_probe_mfma_i8: two workgroups per compute unit, four
+    independent 32x32x32 chains per wave) and a plain 1 GiB device copy
+    (read plus written bytes over its time); medians of `reps` launches timed
+    with events on the current stream."""
+    def timed(fn):
+        ts = []
+        for _ in range(reps):
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            torch.cuda.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return sorted(ts)[len(ts) // 2]
+
+    blocks = 2 * torch.cuda.get_device_properties(0).multi_processor_count
+    iters = 8192
+    sink = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    fgq.fgq_probe_mfma_i8(blocks, 64, sink)
+    torch.cuda.synchronize()
+    ms = timed(lambda: fgq.fgq_probe_mfma_i8(blocks, iters, sink))
+    mfma_tops = blocks * iters * 16 * 65536 / (ms * 1e-3) / 1e12
+    nbytes = 1 << 30
+    src = torch.ones(nbytes // 4, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    dst.copy_(src)
+    torch.cuda.synchronize()
+    ms_copy = timed(lambda: dst.copy_(src))
+    del src, dst
+    torch.cuda.empty_cache()
+    return {"int8_mfma_tops": round(mfma_tops, 1), "spec_int8_mfma_tops": INT8_PEAK_TOPS,
+            "copy_gbs": round(2 * nbytes / (ms_copy * 1e-3) / 1e9, 1), "spec_hbm_gbs": HBM_PEAK_GBS,
+            "method": f"fgq_probe_mfma_i8 ({blocks} workgroups x {iters} rounds) and a 1 GiB device copy, "
+                      f"median of {reps} event-timed launches"}
+
+
+def valu_floor_us(L, G):
+    """The vector-ALU floor of a per-group fp32 epilogue: one multiply-add per
+    row, channel and group, 64 lanes x 256 compute units per cycle at
+    2.4 GHz."""
+    M, K, _, _ = layer_dims(L)
+    return 2.0 * M * L["O"] * (K // G) / (64 * 256 * 2.4e9) * 1e6
+
+
 def stack_layers(fi, depth, batch):
     """Distinct layer shapes of the ResNet stack with their multiplicities."""
     out, index = [], {}
@@ -742,6 +789,13 @@ def main():
                     "dfp": dfp_entry(LAYER_1X1, 64, bits, r11, ops11)},
     }
     out["gemm_m64"] = gemm_measure(torch, fgq, fi)
+    log("[bench] measured peaks")
+    peaks = measured_peaks(torch, fgq)
+    out["measured_peaks"] = peaks
+    out["roofline"]["frac_of_measured_copy"] = round(out["roofline"]["achieved"] / peaks["copy_gbs"], 4)
+    fl64 = valu_floor_us(LAYER, 64)
+    out["g64"]["valu_floor_us"] = round(fl64, 3)
+    out["g64"]["valu_floor_frac"] = round(fl64 / r64["conv_us"], 4)
     if not args.no_stacks:
         out["stacks"] = {}
         for depth, G, sbits in ((50, 4, 8), (101, 64, 4)):

@@ -433,6 +433,22 @@ fgq_status fgq_group_sums(const uint8_t* q, int32_t bits, int64_t B,
                           int64_t row0, int64_t nrows, int32_t* P,
                           void* stream);
 
+/*
+ * Measurement utility (not part of the method): the rate of the int8 matrix
+ * instruction the layer kernels use, for reporting kernels against a
+ * measured peak next to the published one.
+ *
+ * fgq_probe_mfma_i8 -- launches `blocks` workgroups of 256 threads; each
+ * wave issues `iters` rounds of four independent 32x32x32 int8 matrix
+ * instructions (2 * 32768 int8 operations each), i.e. blocks * iters *
+ * 16 * 65536 operations in all, then writes one int32 per thread to `out`
+ * (a sink that keeps the work alive; values meaningless).  out must hold
+ * blocks * 256 int32 (out_elems); FGQ_ERR_SHAPE for blocks or iters < 1 or
+ * a smaller out.  Enqueued on `stream`.
+ */
+fgq_status fgq_probe_mfma_i8(int32_t blocks, int32_t iters, int32_t* out,
+                             int64_t out_elems, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -71,6 +71,7 @@ _SIGS = {
     "fgq_prepare_weights_w8": ([_P, _I64, _I64, _I32, _I32, _P, _SZ, _P], _I32),
     "fgq_conv2d_w8": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _I64, _I32, _I32, _I32, _I32,
                        _I32, _I32, _I32, _P, _P, _P], _I32),
+    "fgq_probe_mfma_i8": ([_I32, _I32, _P, _I64, _P], _I32),
 }
 
 
@@ -414,3 +415,13 @@ def fgq_group_sums(q, bits, shape, codes, O, R, S, stride, pad, G, row0, nrows, 
                               O, R, S, sh, sw, ph, pw, G, row0, nrows, _dev(P, torch.int32, "P"), _stream())
     _check(rc, "fgq_group_sums")
     return P
+
+
+def fgq_probe_mfma_i8(blocks, iters, out=None):
+    """Measurement utility: blocks * iters * 16 * 65536 int8 matrix operations
+    (see include/fgq.h); returns the int32 sink [blocks * 256]."""
+    if out is None:
+        out = torch.empty(blocks * 256, dtype=torch.int32, device="cuda")
+    rc = lib().fgq_probe_mfma_i8(blocks, iters, _dev(out, torch.int32, "out"), out.numel(), _stream())
+    _check(rc, "fgq_probe_mfma_i8")
+    return out

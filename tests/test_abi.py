@@ -70,6 +70,15 @@ def test_ternarize_validation():
 
 
 @no_device
+def test_probe_validation():
+    L = fgq.lib()
+    assert L.fgq_probe_mfma_i8(4, 8, N, 1024, N) == 1
+    assert L.fgq_probe_mfma_i8(0, 8, P, 1024, N) == 2
+    assert L.fgq_probe_mfma_i8(4, 0, P, 1024, N) == 2
+    assert L.fgq_probe_mfma_i8(4, 8, P, 1023, N) == 2   # needs blocks * 256 sink elements
+
+
+@no_device
 def test_quantize_validation():
     L = fgq.lib()
     assert L.fgq_quantize_act(N, 16, 8, N, P, P, P, 4096, N) == 1
