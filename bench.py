@@ -244,6 +244,41 @@ def cpu_baseline(fi, L, G, bits, budget_s=15.0):
             "seconds": round(t_total, 3)}
 
 
+def stack_cpu_estimate(fi, depth, G, bits, batch=64, rows=256):
+    """The oracle's time for a stack's convolutions (and FC), extrapolated
+    from a row sample: for every distinct layer, the oracle convolution of
+    the first `rows` output rows of one image (a row depends only on its own
+    image, so the cost per row is that of the full batch), scaled to the
+    layer's M = batch * Ho * Wo rows and its multiplicity."""
+    import oracle
+    total_s, ops, sampled = 0.0, 0.0, 0
+    for L, count in stack_layers(fi, depth, 1):
+        B1, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        st, pd = L["stride"], L["pad"]
+        g = G if C % G == 0 else 4
+        w = fi.he_weights(O, C, R, S, "stack-cpu", depth, L["name"])
+        x = fi.relu_gauss((B1, H, W, C), "stack-cpu", depth, L["name"])
+        if L["name"] == "conv1":
+            w[:, 3:] = 0.0
+            x[..., 3:] = 0.0
+        t, a, _ = oracle.ternarize(w, g)
+        codes = oracle.pack_codes(t)
+        q, sx = oracle.quantize_act(x, bits)
+        Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
+        n = min(rows, Ho * Wo)
+        t0 = time.perf_counter()
+        oracle.conv2d(q, bits, sx, x.shape, codes, a, O, R, S, (st, st), (pd, pd), g, rows=(0, n))
+        dt = time.perf_counter() - t0
+        M = batch * Ho * Wo
+        total_s += count * dt * M / n
+        ops += count * 2.0 * M * O * R * S * (3 if L["name"] == "conv1" else C)
+        sampled += n
+    return {"seconds_extrapolated": round(total_s, 2), "effective_tops": ops / total_s / 1e12,
+            "cores": oracle.max_threads(), "kind": "oracle",
+            "sample": f"first {rows} output rows (fewer on small maps) of one image per distinct layer, "
+                      f"{sampled} rows in all, scaled to batch {batch} and each layer's multiplicity"}
+
+
 def measured_peaks(torch, fgq, reps=5):
     """Measured peaks beside the published ones: the int8 matrix-instruction
     rate (fgq_probe_mfma_i8: two workgroups per compute unit, four
@@ -801,6 +836,8 @@ def main():
         for depth, G, sbits in ((50, 4, 8), (101, 64, 4)):
             log(f"[bench] ResNet-{depth} stack, G={G}, u{sbits}")
             out["stacks"][f"resnet{depth}_b64_g{G}_u{sbits}"] = stack_measure(torch, fgq, fi, depth, G, sbits)
+            if not args.no_cpu:
+                out["stacks"][f"resnet{depth}_b64_g{G}_u{sbits}"]["cpu_oracle"] = stack_cpu_estimate(fi, depth, G, sbits)
             log(f"[bench] ResNet-{depth}: sum conv {out['stacks'][f'resnet{depth}_b64_g{G}_u{sbits}']['sum_conv_us']} us")
     if not args.no_stacks:
         log("[bench] AlexNet-shaped layers, batch 64, G=4, u8")
