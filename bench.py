@@ -158,7 +158,10 @@ def time_graphs(torch, graphs_and_reps):
     return (t1 - t0) * 1e3, ev0.elapsed_time(ev1)
 
 
-def measure(torch, st, steps, warmup, conv_reps=20):
+def measure(torch, st, steps, warmup, conv_reps=20, trials=1):
+    """Times exactly `steps` steps (the reported figure), then, for
+    trials > 1, repeats the same timed region trials - 1 more times for a
+    median and spread; the component kernels are timed separately."""
     nsets = len(st.sets)
     # eager warm-up and a graph-replay correctness check against eager results
     for i in range(nsets):
@@ -178,6 +181,7 @@ def measure(torch, st, steps, warmup, conv_reps=20):
         full.replay()
     plan = [(full, steps // nsets)] + ([(rem_graph, 1)] if rem_graph else [])
     wall_ms, gpu_ms = time_graphs(torch, plan)
+    trial_ms = [wall_ms] + [time_graphs(torch, plan)[0] for _ in range(trials - 1)]
     # the convolution alone, same stream, same rotation
     conv_g = st.graph(st.conv, nsets)
     conv_g.replay()
@@ -206,7 +210,7 @@ def measure(torch, st, steps, warmup, conv_reps=20):
     _, dfp_ms = time_graphs(torch, [(dfp_g, conv_reps)])
     dfp_us = dfp_ms * 1e3 / (conv_reps * nsets)
     return dict(wall_ms=wall_ms, gpu_ms=gpu_ms, conv_us=conv_us, quant_us=quant_us, conv_fused_us=fused_us,
-                conv_dfp_us=dfp_us)
+                conv_dfp_us=dfp_us, trial_ms=trial_ms)
 
 
 def cpu_baseline(fi, L, G, bits, budget_s=15.0):
@@ -757,7 +761,7 @@ def main():
 
     log(f"[bench] setting up G=4 ({args.sets} buffer sets)")
     st4 = Setup(torch, fgq, fi, LAYER, 4, bits, args.sets, folded=not args.direct)
-    r4 = measure(torch, st4, args.steps, args.warmup)
+    r4 = measure(torch, st4, args.steps, args.warmup, trials=5)
     log(f"[bench] G=4: {r4}")
     ms_per_step = r4["wall_ms"] / args.steps
     del st4
@@ -803,6 +807,8 @@ def main():
         "roofline": roofline(LAYER, 4, bits, r4["conv_us"]),
         "step_detail": {"conv_us": round(r4["conv_us"], 3), "quantize_us": round(r4["quant_us"], 3),
                         "gpu_ms_per_step": round(r4["gpu_ms"] / args.steps, 5),
+                        "trials_ms_per_step": [round(t / args.steps, 5) for t in r4["trial_ms"]],
+                        "median_of_5_tops": round(ops / (sorted(r4["trial_ms"])[2] / args.steps * 1e-3) / 1e12, 2),
                         "conv_only_tops": round(ops / (r4["conv_us"] * 1e-6) / 1e12, 1)},
         "fused": fused_entry(LAYER, 4, bits, r4, ops),
         "dfp": dfp_entry(LAYER, 4, bits, r4, ops),
