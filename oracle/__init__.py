@@ -153,6 +153,18 @@ def gauss_u():
 KS_SAMPLE = 16384
 
 
+def paper_weight_layout(w, N):
+    """Sec. 3.2's weight layout [K][C/N][R*S][N] of weights [O][C][R][S] (the
+    paper's K is the output-channel count, O here): for each output channel,
+    input-channel block and filter tap, the N weights of one group are
+    contiguous.  A pure rearrangement (no arithmetic)."""
+    w = np.asarray(w)
+    O, C, R, S = w.shape
+    if C % N:
+        raise ValueError("N must divide C")
+    return np.ascontiguousarray(w.reshape(O, C // N, N, R * S).transpose(0, 1, 3, 2))
+
+
 def pack_codes(t):
     t = np.ascontiguousarray(t, dtype=np.int8)
     O, K = t.shape

@@ -172,6 +172,31 @@ def test_layer_grouping_layout_and_decomposition_identity():
     assert total <= err16 + 1e-9
 
 
+def test_paper_weight_layout_groups():
+    """Sec. 3.2 stores the weights as [K][C/N][R*S][N] so that each group of
+    N is contiguous.  That tensor is a rearrangement of the weights, and
+    solving every contiguous N-vector of it by brute force over all 3^N
+    ternary assignments (Eq. (1)) reproduces the oracle's codes and scales
+    for the group (o, tap, block), i.e. the oracle's groups are the paper's."""
+    O, C, R, S, N = 3, 12, 2, 3, 4
+    W = fi.he_weights(O, C, R, S, "paper-layout")
+    Pw = oracle.paper_weight_layout(W, N)
+    assert Pw.shape == (O, C // N, R * S, N)
+    np.testing.assert_array_equal(np.sort(Pw.ravel()), np.sort(W.ravel()))
+    t, a, _ = oracle.ternarize(W, N)
+    K = C * R * S
+    t4 = t.reshape(O, R * S, C // N, N)   # k = tap*C + c: [O][tap][block][N]
+    a3 = a.reshape(O, R * S, C // N)
+    for o in range(O):
+        for cb in range(C // N):
+            for tap in range(R * S):
+                err, T, alpha, gap = brute_force(Pw[o, cb, tap])
+                assert gap > 1e-9  # a unique optimum
+                np.testing.assert_array_equal(t4[o, tap, cb], T.astype(np.int8))
+                assert abs(float(a3[o, tap, cb]) - alpha) <= 1e-6 * max(alpha, 1e-30)
+    assert t.shape == (O, K)
+
+
 def test_lemma1_exponential_magnitudes():
     """Lemma 1 and its proof (Appendix): with |W| ~ Exp(lambda) the kept
     fraction is exp(-lambda*Delta) and sum_kept|W| = n(lambda*Delta+1)
