@@ -343,6 +343,18 @@ def stack_layers(fi, depth, batch):
     return out
 
 
+def stack_layer_roofline(L, g, bits):
+    """(ops, algorithmic bytes, roofline us) of one stack layer: 2*M*O*K with
+    the unpadded reduction for conv1 (3 image channels), activations in +
+    2-bit codes + fp32 scales + fp32 output, and the larger of the int8 and
+    HBM times at the published peaks."""
+    M, K, _, _ = layer_dims(L)
+    k_true = L["R"] * L["S"] * (3 if L["name"] == "conv1" else L["C"])
+    ops = 2.0 * M * L["O"] * k_true
+    nbytes = L["B"] * L["H"] * L["W"] * L["C"] * bits // 8 + L["O"] * K // 4 + 4 * L["O"] * K // g + 4 * M * L["O"]
+    return ops, nbytes, max(ops / (INT8_PEAK_TOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+
+
 def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=50):
     """Per-layer kernel times of a batch-`batch` ResNet-`depth` stack, every
     distinct layer timed at its full shape (graph replays over `nsets`
@@ -456,10 +468,7 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=50):
         quant_us = q_ms * 1e3 / (reps * nsets)
         fused_us = f_ms * 1e3 / (reps * nsets)
         dfp_us = d_ms * 1e3 / (reps * nsets)
-        k_true = R * S * (3 if L["name"] == "conv1" else C)
-        ops = 2.0 * M * O * k_true
-        nbytes = n * bits // 8 + O * K // 4 + 4 * O * K // g + 4 * M * O
-        roof_us = max(ops / (INT8_PEAK_TOPS * 1e12), nbytes / (HBM_PEAK_GBS * 1e9)) * 1e6
+        ops, nbytes, roof_us = stack_layer_roofline(L, g, bits)
         layers.append([L["name"], count, round(conv_us, 2), round(roof_us / conv_us, 3), round(fused_us, 2),
                        round(dfp_us, 2)])
         tot["conv_us"] += count * conv_us
