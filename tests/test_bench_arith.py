@@ -2,7 +2,8 @@
 independently from the layer shapes for the benchmark configurations:
 algorithmic bytes and operations of the single layers, the vector-ALU floor
 of the per-group epilogue, and the roofline sums and bytes of the two
-network stacks (every distinct layer counted with its multiplicity)."""
+network stacks (every distinct layer counted with its multiplicity); and
+that a request for more than one GPU ends with a message, not a result."""
 import math
 
 import bench
@@ -42,3 +43,15 @@ def test_stack_rooflines():
         assert n == nlayers
         assert math.isclose(tot_us, roof_us, abs_tol=0.05), (depth, tot_us)
         assert math.isclose(tot_bytes / 1e9, gbytes, abs_tol=0.005), (depth, tot_bytes)
+
+
+def test_more_than_one_gpu_exits_with_a_message():
+    import os
+    import subprocess
+    import sys
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    r = subprocess.run([sys.executable, os.path.join(root, "bench.py"), "--gpus", "2"],
+                       capture_output=True, text=True, timeout=300)
+    assert r.returncode != 0
+    assert "one GPU" in r.stdout + r.stderr
+    assert r.stdout.strip() == "" or not r.stdout.lstrip().startswith("{")  # no result line
