@@ -213,13 +213,34 @@ def measure(torch, st, steps, warmup, conv_reps=20, trials=1):
                 conv_dfp_us=dfp_us, trial_ms=trial_ms)
 
 
-def cpu_baseline(fi, L, G, bits, budget_s=15.0):
+def host_cpu():
+    """The host the oracle runs on: CPU model, the CPUs of this process's
+    affinity mask, and the oracle's thread count (all of those CPUs, capped by
+    OMP_NUM_THREADS when the environment sets it), passed to every oracle
+    call so that the reported count is the count used."""
+    model = "unknown"
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                model = line.split(":", 1)[1].strip()
+                break
+    except OSError:
+        pass
+    affinity = len(os.sched_getaffinity(0))
+    env = os.environ.get("OMP_NUM_THREADS", "")
+    threads = min(affinity, int(env)) if env.isdigit() and int(env) > 0 else affinity
+    return {"cpu_model": model, "affinity_cpus": affinity, "threads": threads}
+
+
+def cpu_baseline(fi, L, G, bits, budget_s=15.0, tag="bench"):
     """The plain oracle on the host: quantize of the whole input plus the
     convolution of a bounded sample of output rows, scaled to the metric."""
     import oracle
+    hc = host_cpu()
+    nt = hc["threads"]
     M, K, Ho, Wo = layer_dims(L)
-    w = fi.he_weights(L["O"], L["C"], L["R"], L["S"], "bench", G)
-    x = fi.relu_gauss((L["B"], L["H"], L["W"], L["C"]), "bench-x", 0)
+    w = fi.he_weights(L["O"], L["C"], L["R"], L["S"], tag, G)
+    x = fi.relu_gauss((L["B"], L["H"], L["W"], L["C"]), tag + "-x", 0)
     t, a, _ = oracle.ternarize(w, G)
     codes = oracle.pack_codes(t)
     t0 = time.perf_counter()
@@ -228,24 +249,48 @@ def cpu_baseline(fi, L, G, bits, budget_s=15.0):
     args = (q, bits, s, x.shape, codes, a, L["O"], L["R"], L["S"], (L["stride"],) * 2, (L["pad"],) * 2, G)
     probe = 256
     t0 = time.perf_counter()
-    oracle.conv2d(*args, rows=(0, probe))
+    oracle.conv2d(*args, rows=(0, probe), nthreads=nt)
     t_probe = time.perf_counter() - t0
     nrows = int(min(M, max(probe, probe * budget_s / max(t_probe, 1e-6))))
     reps = 3 if nrows == M and t_probe * M / probe * 3 < budget_s * 2 else 1
     times = []
     for _ in range(reps):
         t0 = time.perf_counter()
-        oracle.conv2d(*args, rows=(0, nrows))
+        oracle.conv2d(*args, rows=(0, nrows), nthreads=nt)
         times.append(time.perf_counter() - t0)
     t_c = sorted(times)[len(times) // 2]
     t_total = t_c + t_q * nrows / M
     ops = 2.0 * nrows * L["O"] * K
-    return {"value": ops / t_total / 1e12, "unit": "TOPS", "cores": oracle.max_threads(),
-            "kind": "oracle",
+    return {"value": ops / t_total / 1e12, "unit": "TOPS", "cores": nt, "kind": "oracle",
+            "cpu_model": hc["cpu_model"], "affinity_cpus": hc["affinity_cpus"],
             "sample": f"quantize of the full {L['B']}x{L['H']}x{L['W']}x{L['C']} input "
                       f"({t_q:.3f} s, prorated) + convolution of output rows [0, {nrows}) of {M} "
                       f"({t_c:.2f} s, median of {reps}); scaled per row",
             "seconds": round(t_total, 3)}
+
+
+def cpu_baseline_gemm(fi, M=64, K=256, O=128, G=4, bits=8, budget_s=2.0):
+    """The oracle on the single FGQ GEMM (whole layer, repeated until
+    `budget_s` of CPU time; quantize + GEMM per call)."""
+    import oracle
+    hc = host_cpu()
+    nt = hc["threads"]
+    w = fi.gauss_weights(O, K, 0.05, "bench-gemm")
+    x = fi.relu_gauss((M, K), "bench-gemm", 0)
+    t, a, _ = oracle.ternarize(w.reshape(O, K, 1, 1), G)
+    codes = oracle.pack_codes(t)
+    calls, t0 = 0, time.perf_counter()
+    while True:
+        q, s = oracle.quantize_act(x, bits)
+        oracle.gemm(q, bits, s, M, K, codes, a, O, G, nthreads=nt)
+        calls += 1
+        dt = time.perf_counter() - t0
+        if dt >= budget_s or calls >= 100000:
+            break
+    us = dt / calls * 1e6
+    return {"value": 2.0 * M * K * O / (us * 1e-6) / 1e12, "unit": "TOPS", "us_per_call": round(us, 2),
+            "cores": nt, "kind": "oracle", "cpu_model": hc["cpu_model"], "affinity_cpus": hc["affinity_cpus"],
+            "sample": f"the whole M={M} K={K} O={O} layer (quantize + GEMM), {calls} calls"}
 
 
 def stack_cpu_estimate(fi, depth, G, bits, batch=64, rows=256):
@@ -255,6 +300,7 @@ def stack_cpu_estimate(fi, depth, G, bits, batch=64, rows=256):
     image, so the cost per row is that of the full batch), scaled to the
     layer's M = batch * Ho * Wo rows and its multiplicity."""
     import oracle
+    hc = host_cpu()
     total_s, ops, sampled = 0.0, 0.0, 0
     for L, count in stack_layers(fi, depth, 1):
         B1, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
@@ -271,14 +317,16 @@ def stack_cpu_estimate(fi, depth, G, bits, batch=64, rows=256):
         Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
         n = min(rows, Ho * Wo)
         t0 = time.perf_counter()
-        oracle.conv2d(q, bits, sx, x.shape, codes, a, O, R, S, (st, st), (pd, pd), g, rows=(0, n))
+        oracle.conv2d(q, bits, sx, x.shape, codes, a, O, R, S, (st, st), (pd, pd), g, rows=(0, n),
+                      nthreads=hc["threads"])
         dt = time.perf_counter() - t0
         M = batch * Ho * Wo
         total_s += count * dt * M / n
         ops += count * 2.0 * M * O * R * S * (3 if L["name"] == "conv1" else C)
         sampled += n
     return {"seconds_extrapolated": round(total_s, 2), "effective_tops": ops / total_s / 1e12,
-            "cores": oracle.max_threads(), "kind": "oracle",
+            "cores": hc["threads"], "kind": "oracle", "cpu_model": hc["cpu_model"],
+            "affinity_cpus": hc["affinity_cpus"],
             "sample": f"first {rows} output rows (fewer on small maps) of one image per distinct layer, "
                       f"{sampled} rows in all, scaled to batch {batch} and each layer's multiplicity"}
 
@@ -862,6 +910,9 @@ def main():
     if not args.no_cpu:
         log("[bench] CPU oracle baseline")
         out["cpu_baseline"] = cpu_baseline(fi, LAYER, 4, bits)
+        out["g64"]["cpu_baseline"] = cpu_baseline(fi, LAYER, 64, bits, budget_s=6.0)
+        out["g64_1x1"]["cpu_baseline"] = cpu_baseline(fi, LAYER_1X1, 64, bits, budget_s=4.0)
+        out["gemm_m64"]["cpu_baseline"] = cpu_baseline_gemm(fi)
     print(json.dumps(out), flush=True)
 
 

@@ -122,6 +122,26 @@ def test_ternarize_reports_nonfinite():
         fgq.fgq_ternarize(dev(w), 4)
 
 
+
+def test_ternarize_code_bytes_golden():
+    """fgq_ternarize writes the hand-worked bytes of tests/golden/code_bytes.txt
+    (the byte layout of include/fgq.h): with groups of one weight, w = t gives
+    alpha = |w| and codes t, so the stored bytes are exactly the golden ones."""
+    import os
+    path = os.path.join(os.path.dirname(__file__), "golden", "code_bytes.txt")
+    n = 0
+    for line in open(path):
+        if line.startswith("#") or not line.strip():
+            continue
+        K, ts, bs = (p.strip() for p in line.split("|"))
+        t = np.array([[int(v) for v in r.split()] for r in ts.split(";")], np.float32)
+        b = np.array([[int(v, 16) for v in r.split()] for r in bs.split(";")], np.uint8)
+        codes, alpha, _ = fgq.fgq_ternarize(dev(t), 1)
+        assert np.array_equal(host(codes), b), f"K={K} t={ts}"
+        assert np.array_equal(host(alpha), np.abs(t))
+        n += 1
+    assert n >= 10
+
 @pytest.mark.parametrize("bits", [8, 4])
 @pytest.mark.parametrize("n", [2, 4096 * 16 + 2, 3 * 7 * 5 * 16, 32 * 28 * 28 * 128, 4 * 5_000_003])
 @pytest.mark.parametrize("given_scale", [False, True])
