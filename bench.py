@@ -416,7 +416,7 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=50):
     Finally each layer runs as the paper's own pipeline (Sec. 4): 8-bit
     fixed-point group scales (fgq_conv2d_dfp) with the fused output codes,
     and conv1 at 8-bit weights (fgq_conv2d_w8)."""
-    layers = []
+    layers, direct_layers = [], []
     tot = dict(conv_us=0.0, quant_us=0.0, fused_us=0.0, dfp_us=0.0, ops=0.0, roof_us=0.0, bytes=0.0,
                first_quant_us=0.0)
     gen = torch.Generator(device="cuda")
@@ -429,7 +429,11 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=50):
             w[:, 3:] = 0.0
         codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), g)
         K = R * S * C
-        prep = fgq.fgq_prepare_weights(codes, alpha, O, K, g)
+        # a layer whose group scales fail the folded layout's accuracy guard
+        # runs the direct kernel (prepared = None), as a network would
+        prep = fgq.fgq_prepare_weights(codes, alpha, O, K, g, fallback=True)
+        if prep is None:
+            direct_layers.append(L["name"])
         prep_dfp = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, g, 8)
         # the paper keeps the first layer at 8-bit weights (8w-8a)
         prep_w8 = fgq.fgq_prepare_weights_w8(torch.from_numpy(w).cuda()) if L["name"] == "conv1" else None
@@ -544,7 +548,8 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=50):
             "algorithmic_bytes": int(tot["bytes"]),
             "per_layer_columns": ["layer", "count", "conv_us", "roofline_frac", "conv_fused_us",
                                   "conv_dfp8_fused_us"],
-            "per_layer": layers}
+            "per_layer": layers,
+            "direct_kernel_layers": direct_layers}
 
 
 def alexnet_measure(torch, fgq, fi, batch=64, G=4, bits=8, nsets=3, reps=50):
@@ -566,7 +571,7 @@ def alexnet_measure(torch, fgq, fi, batch=64, G=4, bits=8, nsets=3, reps=50):
             w[:, 3:] = 0.0
         codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
         K = R * S * C
-        prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+        prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G, fallback=True)
         prep_dfp = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, G, 8)
         prep_w8 = fgq.fgq_prepare_weights_w8(torch.from_numpy(w).cuda()) if L["name"] == "conv1" else None
         Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1

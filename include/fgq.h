@@ -68,7 +68,11 @@ enum {
                               the 8-bit weights: NaN or Inf) */
   FGQ_ERR_HIP = 6,         /* HIP runtime error (also: no device) */
   FGQ_ERR_UNSUPPORTED = 7, /* method or path not available for the shape */
-  FGQ_ERR_WORKSPACE = 8    /* workspace missing or too small */
+  FGQ_ERR_WORKSPACE = 8,   /* workspace missing or too small */
+  FGQ_ERR_RANGE = 9        /* fgq_prepare_weights: the group scales of some
+                              output channel spread too widely for the folded
+                              layout to meet its accuracy bound; run the layer
+                              without a prepared buffer (direct kernel) */
 };
 
 /* Ternarization methods of fgq_ternarize. */
@@ -192,6 +196,7 @@ fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits,
                             float* scale_out, void* ws, size_t ws_bytes,
                             void* stream);
 
+
 /*
  * fgq_prepare_weights -- per-layer constants for the matrix-core kernels
  * (built once per layer, like the ternarization itself).  The layout
@@ -203,20 +208,34 @@ fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits,
  * group; 1 byte per weight plus 4 bytes per group.
  *
  * Any other G (folded-scale kernel): the group scales are brought to one
- * fixed-point grid per output channel: A[o][g] = rint(alpha[o][g] * 2^E_o),
- * with E_o the largest exponent keeping every A of the channel within
+ * grid per output channel: A[o][g] = rint(alpha[o][g] / h_o), with h_o the
+ * smallest fp32 step keeping every A of the channel within
  * 127*(1 + 255 + 255^2), written as three balanced base-255 digits in
  * [-127, 127].  The folded weights t*digit are int8, so the layer runs as
  * three exact int8 products whose integer sums are combined exactly; only
- * the rounding of alpha to the grid (an error of at most 1.21e-7 times the
+ * the rounding of alpha to the grid (at most h_o / 2, about 6e-8 times the
  * channel's largest alpha) and the fp32 conversions and fused multiply-adds
  * of the final combination differ from the exact formula.  3 bytes per
  * weight.
+ *
+ * Accuracy guard (folded layout only): the result is within 1e-5 of
+ * s_x * sum_g alpha_g |P_g| for every input when each non-zero scale of a
+ * channel lies within a relative 9.2e-6 of its grid value A * h_o (the
+ * fp32 combination adds less than 7.75e-7 of that magnitude).  That fails only
+ * for channels whose scales spread over a wide range (the grid step follows
+ * the channel's largest alpha; smaller scales keep fewer bits).  The check
+ * is exact, per channel, on the device; then the call returns
+ * FGQ_ERR_RANGE, and the layer must run without the prepared buffer (the
+ * direct kernel, exact).  The buffer is still written, with a NaN scale for
+ * each failing channel, so that a layer run with it anyway gives NaN fp32
+ * outputs in those channels.  A negative or non-finite alpha fails its
+ * channel too.
  *
  * codes, alpha  [in]  as produced by fgq_ternarize for an [O][K] layer
  * prepared      [out] device buffer of fgq_prepared_bytes(O, K, G) bytes,
  *                     256-byte aligned; opaque; read by fgq_conv2d/fgq_gemm
  *                     with the same O, K, G.
+ * Synchronizes `stream` (the folded layout's guard is read back).
  */
 size_t fgq_prepared_bytes(int64_t O, int64_t K, int32_t G);
 fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha,

@@ -22,7 +22,8 @@ FGQ_TERN_KS = 4
 
 _STATUS = {0: "FGQ_OK", 1: "FGQ_ERR_NULL", 2: "FGQ_ERR_SHAPE", 3: "FGQ_ERR_GROUP",
            4: "FGQ_ERR_BITS", 5: "FGQ_ERR_NONFINITE", 6: "FGQ_ERR_HIP",
-           7: "FGQ_ERR_UNSUPPORTED", 8: "FGQ_ERR_WORKSPACE"}
+           7: "FGQ_ERR_UNSUPPORTED", 8: "FGQ_ERR_WORKSPACE", 9: "FGQ_ERR_RANGE"}
+FGQ_ERR_RANGE = 9
 
 
 class FgqError(RuntimeError):
@@ -190,8 +191,13 @@ def fgq_prepared_bytes(O, K, G):
     return int(lib().fgq_prepared_bytes(O, K, G))
 
 
-def fgq_prepare_weights(codes, alpha, O, K, G, prepared=None):
-    """Per-layer constants of the folded-scale kernel (opaque uint8 buffer)."""
+def fgq_prepare_weights(codes, alpha, O, K, G, prepared=None, fallback=False):
+    """Per-layer constants of the matrix-core kernels (opaque uint8 buffer).
+
+    When the folded layout cannot meet its accuracy bound for some channel
+    (FGQ_ERR_RANGE: the channel's group scales spread too widely), raises
+    FgqError, or with fallback=True returns None, so that the layer calls
+    given prepared=None run the direct kernel."""
     nb = fgq_prepared_bytes(O, K, G)
     if nb == 0:
         raise FgqError(3, "fgq_prepare_weights")
@@ -201,6 +207,8 @@ def fgq_prepare_weights(codes, alpha, O, K, G, prepared=None):
         raise ValueError("prepared buffer must be 256-byte aligned")
     rc = lib().fgq_prepare_weights(_dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
                                    O, K, G, ctypes.c_void_p(prepared.data_ptr()), nb, _stream())
+    if rc == FGQ_ERR_RANGE and fallback:
+        return None
     _check(rc, "fgq_prepare_weights")
     return prepared
 

@@ -112,11 +112,12 @@ const char* fgq_status_string(fgq_status s) {
     case FGQ_ERR_HIP: return "FGQ_ERR_HIP: HIP runtime error or no device";
     case FGQ_ERR_UNSUPPORTED: return "FGQ_ERR_UNSUPPORTED: method or shape not supported";
     case FGQ_ERR_WORKSPACE: return "FGQ_ERR_WORKSPACE: workspace missing or too small";
+    case FGQ_ERR_RANGE: return "FGQ_ERR_RANGE: group scales too widely spread for the folded layout";
     default: return "FGQ: unknown status";
   }
 }
 
-int32_t fgq_abi_version(void) { return 1; }
+int32_t fgq_abi_version(void) { return 2; }
 
 int32_t fgq_device_count(void) {
   int n = 0;
@@ -224,8 +225,20 @@ fgq_status fgq_prepare_weights(const uint8_t* codes, const float* alpha, int64_t
   if (G < 1 || K % G != 0) return FGQ_ERR_GROUP;
   if (O > (1LL << 31) || K > (1LL << 31)) return FGQ_ERR_SHAPE;
   if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
-  if (prepared_bytes < static_cast<size_t>(prepared_layout(O, K, G).total)) return FGQ_ERR_WORKSPACE;
-  return launch_prepare(codes, alpha, O, K, G, prepared, as_stream(stream));
+  const PreparedLayout L = prepared_layout(O, K, G);
+  if (prepared_bytes < static_cast<size_t>(L.total)) return FGQ_ERR_WORKSPACE;
+  hipStream_t st = as_stream(stream);
+  fgq_status rc = launch_prepare(codes, alpha, O, K, G, prepared, st);
+  if (rc != FGQ_OK || L.kind != kPrepFold) return rc;
+  // The folded layout's accuracy guard: a channel whose scales do not fit
+  // its fixed-point grid closely enough carries a NaN scale.
+  std::vector<float> scale(static_cast<size_t>(O));
+  FGQ_TRY_HIP(hipMemcpyAsync(scale.data(), static_cast<const char*>(prepared) + L.scale_off,
+                             sizeof(float) * O, hipMemcpyDeviceToHost, st));
+  FGQ_TRY_HIP(hipStreamSynchronize(st));
+  for (int64_t o = 0; o < O; ++o)
+    if (scale[o] != scale[o]) return FGQ_ERR_RANGE;
+  return FGQ_OK;
 }
 
 fgq_status fgq_conv2d(const uint8_t* q, int32_t bits, const float* sx, int64_t B, int64_t H,

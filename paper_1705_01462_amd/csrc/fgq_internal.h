@@ -53,7 +53,7 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 //      planes : int8 folded digits t*d_j (j = 0 least significant),
 //               [O32/32][Kp/64][3 planes][2 K halves][64 lanes][16 bytes]
 //      bias   : int32 [3][O]  128 * sum_k plane_j[o][k] (uint8 offset term)
-//      scale  : fp32  [O]     2^-E_o
+//      scale  : fp32  [O]     the grid step h_o (NaN: the channel fails the accuracy guard)
 //      xcodes, xacodes (G a power of two in 4..128): the 2-bit codes and the
 //               three digits of each group's scale in the codes-expanding
 //               GEMM's order (xlayout.h; digits plane-major)
@@ -85,6 +85,18 @@ constexpr int64_t kFoldMaxK = 65536;
 // The per-group kernel accumulates one fp32 product per group; with at most
 // 160 groups its rounding error stays below 1e-5 of the summand magnitude.
 constexpr int64_t kGroupMaxGroups = 160;
+// Accuracy guard of the folded layout.  With every group scale on the
+// channel's grid, Ahat_g = A_g h (A_g = rint(alpha_g / h)), the integer sums
+// are exact and S_j = sum_g d_j(g) P_g, so the fp32 combination of the three
+// digit sums (three conversions, c0 = s_x h and two coefficients c0 255^j
+// rounded, a product and two fused multiply-adds) is within 13 * 2^-24 <
+// kFoldCombineRel of s_x * sum_g Ahat_g |P_g| (balanced digits have
+// sum_j 255^j |d_j| < 3 A).  A channel whose scales all satisfy
+// |Ahat_g - alpha_g| <= kFoldMaxRel * alpha_g therefore meets 1e-5 of
+// s_x * sum_g alpha_g |P_g| for every input:
+// 9.2e-6 + 7.75e-7 * (1 + 9.2e-6) < 1e-5.
+constexpr double kFoldMaxRel = 9.2e-6;
+constexpr double kFoldCombineRel = 7.75e-7;
 PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G);
 PreparedLayout prepared_layout_dfp(int64_t O, int64_t K, int32_t G);
 

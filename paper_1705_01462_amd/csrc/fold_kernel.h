@@ -9,7 +9,7 @@
 // prepare.hip), the layer is three exact int8 GEMMs sharing one activation
 // operand:
 //   S_j[o][m] = sum_k plane_j[o][k] * q'[m][k],   q' = q ^ 0x80 (uint8) or q (uint4)
-//   y[m][o]   = sum_j (S_j + bias_j[o]) * (s_x * 2^-E_o * 255^j)
+//   y[m][o]   = sum_j (S_j + bias_j[o]) * (s_x * h_o * 255^j)
 // The integer sums are exact (|S_j + bias_j| <= 255 * 127 * K < 2^31 for
 // K <= 65536); the combination is three fp32 conversions and fused
 // multiply-adds per output.  With fixed-point scales (kDfp, see dfp.hip)

@@ -7,18 +7,20 @@
 //
 // Other group sizes: the folded-scale kernel.
 // y[m][o] = s_x * sum_k q[m][k] * alpha[o][g(k)] * t[o][k] is a dense GEMM
-// with real weights.  Putting every alpha of channel o on one fixed-point
-// grid, A[o][g] = rint(alpha[o][g] * 2^E_o) <= 127*(1+255+255^2), and writing
-// A in three balanced base-255 digits d_j in [-127, 127] gives int8 weights
-// t*d_j, so the layer becomes three exact int8 products combined as
-//   y = s_x * 2^-E_o * sum_j 255^j * (S_j + bias_j[o]),
+// with real weights.  Putting every alpha of channel o on one grid of step
+// h_o (the smallest fp32 value with alpha_max(o) / h_o <= 127*(1+255+255^2)),
+// A[o][g] = rint(alpha[o][g] / h_o), and writing A in three balanced base-255
+// digits d_j in [-127, 127] gives int8 weights t*d_j, so the layer becomes
+// three exact int8 products combined as
+//   y = s_x * h_o * sum_j 255^j * (S_j + bias_j[o]),
 // S_j = sum_k q'[m][k] * t[o][k] * d_j[o][g(k)] over offset activations
 // q' = q - 128 (uint8) and bias_j = 128 * sum_k t*d_j (zero for uint4).
 // The only departures from the exact value are the rounding of alpha to the
-// grid (step 2^-E_o < alpha_max(o) / 4145343) and the final fp32 rounding.
+// grid and the final fp32 combination; the accuracy guard below checks the
+// first against kFoldMaxRel per scale.
 //
 // One block per output channel (channels padded to a multiple of 32 get
-// zero planes): max alpha -> E_o, then digits, planes (written in the
+// zero planes): max alpha -> h_o, then digits, planes (written in the
 // fragment order of the matrix-core kernel) and the per-plane sums.  For G
 // a power of two in 4..128 the layout also holds the 2-bit codes and each
 // group's three digits in the codes-expanding GEMM's order (xlayout.h;
@@ -84,6 +86,7 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
     int32_t* __restrict__ bias, float* __restrict__ scale, uint8_t* __restrict__ xcodes,
     int8_t* __restrict__ xdigits, int32_t xnb) {
   __shared__ float redf[kThreads / 64];
+  __shared__ double redw[kThreads / 64];
   __shared__ int64_t redi[3][kThreads / 64];
   const int64_t o = blockIdx.x;
   const int64_t nks = Kp / kFoldKStep;
@@ -113,17 +116,44 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
   amax = redf[0];
   for (int i = 1; i < kThreads / 64; ++i) amax = fmaxf(amax, redf[i]);
 
-  // Largest E with rint(amax * 2^E) <= kAmax (E = 0 for an all-zero row).
-  int E = 0;
+  // Grid step h: the smallest fp32 value with amax / h <= kAmax, so that the
+  // largest scale uses the whole three-digit range (A = rint(alpha / h)).
+  float h = 0.0f;
   if (amax > 0.0f) {
-    int e2;
-    frexpf(amax, &e2);  // amax = f * 2^e2, f in [0.5, 1)
-    E = 23 - e2;
-    if (rint(ldexp(static_cast<double>(amax), E)) > static_cast<double>(kAmax)) E -= 1;
-    if (E > 126) E = 126;
-    if (E < -126) E = -126;
+    h = static_cast<float>(static_cast<double>(amax) / static_cast<double>(kAmax));
+    if (static_cast<double>(h) * static_cast<double>(kAmax) < static_cast<double>(amax))
+      h = nextafterf(h, INFINITY);
   }
-  const double two_e = ldexp(1.0, E);
+  const double hd = h;
+
+  // Accuracy guard: the largest relative error of a group scale on the
+  // grid, max_g |A_g h - alpha_g| / alpha_g over the channel's non-zero
+  // scales (A_g h and the difference are exact in fp64).  The folded result
+  // then differs from the exact one by at most that fraction of
+  // s_x * sum_g alpha_g |P_g|, plus the fp32 combination (below
+  // kFoldCombineRel of the same magnitude); a channel beyond kFoldMaxRel
+  // gets a NaN scale, which the host reports.  A negative or non-finite
+  // scale, or a step below the normal fp32 range, fails the channel too.
+  double worst = (amax > 0.0f && h < __FLT_MIN__) ? INFINITY : 0.0;
+  for (int64_t gi = threadIdx.x; gi < ng; gi += kThreads) {
+    const float a = alpha[o * ng + gi];
+    if (!(a >= 0.0f) || !(a < INFINITY)) {
+      worst = INFINITY;
+    } else if (a > 0.0f) {
+      const double A = rint(static_cast<double>(a) / hd);
+      worst = fmax(worst, fabs(A * hd - static_cast<double>(a)) / static_cast<double>(a));
+    }
+  }
+  for (int off = 32; off > 0; off >>= 1) worst = fmax(worst, __shfl_xor(worst, off));
+  if (lane == 0) redw[wid] = worst;
+  __syncthreads();
+  worst = redw[0];
+  for (int i = 1; i < kThreads / 64; ++i) worst = fmax(worst, redw[i]);
+  const bool fits = worst <= kFoldMaxRel;
+  // the grid code of a scale (0 for a zero scale or a failed channel)
+  auto grid_code = [&](float a) -> int64_t {
+    return fits && a > 0.0f ? static_cast<int64_t>(rint(static_cast<double>(a) / hd)) : 0;
+  };
 
   if (xnb > 0) {
     write_xcodes(codes, o, K, Kp, true, xcodes);
@@ -132,7 +162,7 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
       const int hf = static_cast<int>((e / xnb) % 2), jb = static_cast<int>(e % xnb);
       const int64_t k = xscale_k(ks, hf, jb, G);
       int d[3] = {0, 0, 0};
-      if (k < K) digits_of(static_cast<int64_t>(rint(static_cast<double>(alpha[o * ng + k / G]) * two_e)), d);
+      if (k < K) digits_of(grid_code(alpha[o * ng + k / G]), d);
       const int64_t ln = xfrag_lane(nk, o, ks, hf);
       for (int j = 0; j < 3; ++j) xdigits[j * xplane + ln * xnb + jb] = static_cast<int8_t>(d[j]);
     }
@@ -145,8 +175,7 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
     if (k < K) {
       const uint32_t c = (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u;
       t = c == 1 ? 1 : (c == 3 ? -1 : 0);
-      const int64_t A = static_cast<int64_t>(rint(static_cast<double>(alpha[o * ng + k / G]) * two_e));
-      digits_of(A, d);
+      digits_of(grid_code(alpha[o * ng + k / G]), d);
     }
 #pragma unroll
     for (int j = 0; j < 3; ++j) {
@@ -168,7 +197,7 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
       for (int i = 0; i < kThreads / 64; ++i) v += redi[j][i];
       bias[j * O + o] = static_cast<int32_t>(128 * v);
     }
-    scale[o] = static_cast<float>(ldexp(1.0, -E));
+    scale[o] = fits ? h : NAN;
   }
 }
 

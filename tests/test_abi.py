@@ -35,7 +35,7 @@ def test_library_exports_every_declared_symbol():
 
 def test_host_helpers():
     L = fgq.lib()
-    assert L.fgq_abi_version() == 1
+    assert L.fgq_abi_version() == 2
     assert L.fgq_codes_bytes(128, 1152) == 128 * 288
     assert L.fgq_codes_bytes(3, 5) == 3 * 2
     assert L.fgq_group_count(128, 1152, 4) == 128 * 288
@@ -44,7 +44,7 @@ def test_host_helpers():
     assert L.fgq_prepared_bytes(128, 1152, 5) == 0
     assert L.fgq_prepared_bytes(128, 1152, 4) % 256 == 0
     assert L.fgq_quantize_ws_bytes(32 * 28 * 28 * 128) >= 4
-    for code in range(9):
+    for code in range(10):
         assert L.fgq_status_string(code).startswith(b"FGQ")
     # per-group layout (G = 64, at most 160 groups): 1 byte per weight + alpha
     assert L.fgq_prepared_bytes(128, 1152, 64) == 128 * 1152 + 4 * 18 * 128

@@ -252,6 +252,12 @@ def test_conv_direct_path_bit_exact(case):
 def test_conv_folded_path(case):
     B, H, W, C, O, R, S, st, pd, G, bits = case
     w = fi.he_weights(O, C, R, S, "fold", case)
+    if G < 4:
+        # with one or two weights per group the scales of random weights come
+        # arbitrarily close to zero, which the folded layout's accuracy guard
+        # rejects (test_gpu_guard.py); here magnitudes are kept >= sigma / 4
+        sd = np.float32(np.sqrt(2.0 / (C * R * S)))
+        w = np.where(w < 0, -1.0, 1.0).astype(np.float32) * np.maximum(np.abs(w), sd / 4)
     x = fi.relu_gauss((B, H, W, C), "fold", case)
     ref = ref_layer(w, x, G, bits, R, S, st, pd)
     codes, alpha, _, q, sx = gpu_inputs(w, x, G, bits)

@@ -122,7 +122,10 @@ def test_alexnet_layer(L):
     codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
     q, sx = fgq.fgq_quantize_act(torch.from_numpy(x).cuda(), bits)
     K = R * S * C
-    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+    # as a network would: a layer whose group scales fail the folded layout's
+    # accuracy guard runs the direct kernel (fc6 here: one channel of 4096)
+    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G, fallback=True)
+    print(f"[alexnet] {L['name']}: {'folded layout' if prep is not None else 'direct kernel (guard)'}", flush=True)
     Ho, Wo = (H + 2 * pd - R) // st + 1, (W + 2 * pd - S) // st + 1
     M = B * Ho * Wo
     if fc:
