@@ -196,6 +196,23 @@ fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits,
                             float* scale_out, void* ws, size_t ws_bytes,
                             void* stream);
 
+/*
+ * fgq_quantize_act_noalloc -- fgq_quantize_act without a workspace, for
+ * callers that cannot allocate device memory (code under HIP graph capture,
+ * serving loops that must not call hipMalloc, harnesses that forbid it).
+ * Same arguments and results as fgq_quantize_act (bit for bit).  The dynamic
+ * scale's partial maxima go to a 4 KB array of the library's own in device
+ * memory, one per device, held until the process ends (its address is looked
+ * up on the first call on each device).  The maximum is 1024 partial maxima,
+ * which covers every n (pass 1 runs at most 1024 blocks);
+ * FGQ_ERR_WORKSPACE would report a larger need.  Nothing is allocated and
+ * nothing needs to start at zero (each call writes every partial it reads).
+ * Calls that overlap on one device (on different streams, or from several
+ * threads) share that array and race: serialize them.
+ */
+fgq_status fgq_quantize_act_noalloc(const float* x, int64_t n, int32_t bits,
+                                    const float* scale_in, uint8_t* q,
+                                    float* scale_out, void* stream);
 
 /*
  * fgq_prepare_weights -- per-layer constants for the matrix-core kernels

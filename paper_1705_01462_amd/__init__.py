@@ -49,6 +49,7 @@ _SIGS = {
     "fgq_ks_distances": ([_P, _I64, _P, _P], _I32),
     "fgq_quantize_ws_bytes": ([_I64], _SZ),
     "fgq_quantize_act": ([_P, _I64, _I32, _P, _P, _P, _P, _SZ, _P], _I32),
+    "fgq_quantize_act_noalloc": ([_P, _I64, _I32, _P, _P, _P, _P], _I32),
     "fgq_prepared_bytes": ([_I64, _I64, _I32], _SZ),
     "fgq_prepare_weights": ([_P, _P, _I64, _I64, _I32, _P, _SZ, _P], _I32),
     "fgq_conv2d": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
@@ -184,6 +185,24 @@ def fgq_quantize_act(x, bits, scale_in=None, q=None, scale_out=None, ws=None):
                                 None if ws is None else ctypes.c_void_p(ws.data_ptr()),
                                 0 if ws is None else ws.numel() * ws.element_size(), _stream())
     _check(rc, "fgq_quantize_act")
+    return q, scale_out
+
+
+def fgq_quantize_act_noalloc(x, bits, scale_in=None, q=None, scale_out=None):
+    """fgq_quantize_act without a workspace (the library's per-device scratch);
+    allocates nothing when q and scale_out are given."""
+    n = x.numel()
+    px = _dev(x, torch.float32, "x")
+    nbytes = n if bits == 8 else n // 2
+    if q is None:
+        q = torch.empty(max(nbytes, 1), dtype=torch.uint8, device=x.device)[:nbytes]
+    if scale_out is None:
+        scale_out = torch.empty(1, dtype=torch.float32, device=x.device)
+    rc = lib().fgq_quantize_act_noalloc(px, n, bits,
+                                        None if scale_in is None else _dev(scale_in, torch.float32, "scale_in"),
+                                        _dev(q, torch.uint8, "q"), _dev(scale_out, torch.float32, "scale_out"),
+                                        _stream())
+    _check(rc, "fgq_quantize_act_noalloc")
     return q, scale_out
 
 

@@ -213,6 +213,22 @@ fgq_status fgq_quantize_act(const float* x, int64_t n, int32_t bits, const float
                          as_stream(stream));
 }
 
+fgq_status fgq_quantize_act_noalloc(const float* x, int64_t n, int32_t bits, const float* scale_in,
+                                    uint8_t* q, float* scale_out, void* stream) {
+  if (!x || !q || !scale_out) return FGQ_ERR_NULL;
+  if (bits != 8 && bits != 4) return FGQ_ERR_BITS;
+  if (n < 1) return FGQ_ERR_SHAPE;
+  if (bits == 4 && n % 2 != 0) return FGQ_ERR_BITS;
+  const int32_t np = quantize_partials(n);
+  if (np > kQuantScratchFloats) return FGQ_ERR_WORKSPACE;
+  float* scratch = nullptr;
+  if (!scale_in) {
+    const fgq_status rc = quantize_scratch(&scratch);
+    if (rc != FGQ_OK) return rc;
+  }
+  return launch_quantize(x, n, bits, scale_in, q, scale_out, scratch, np, as_stream(stream));
+}
+
 size_t fgq_prepared_bytes(int64_t O, int64_t K, int32_t G) {
   if (O < 1 || K < 1 || G < 1 || K % G != 0) return 0;
   return static_cast<size_t>(prepared_layout(O, K, G).total);

@@ -115,6 +115,13 @@ fgq_status launch_quantize(const float* x, int64_t n, int32_t bits,
                            const float* scale_in, uint8_t* q, float* scale_out,
                            float* partials, int32_t npart, hipStream_t st);
 int32_t quantize_partials(int64_t n);
+// The allocation-free quantization (fgq_quantize_act_noalloc) keeps pass 1's
+// partial maxima in a file-scope device array of kQuantScratchFloats floats
+// (4 KB per device, held until the process ends); quantize_scratch gives its
+// address on the current device.
+constexpr int32_t kQuantScratchFloats = 1024;
+constexpr int kMaxDevices = 64;
+fgq_status quantize_scratch(float** out);
 fgq_status launch_exact_conv(const uint8_t* q, const float* sx,
                              const uint8_t* codes, const float* alpha,
                              const ConvGeom& g, const LayerOut& out, hipStream_t st);

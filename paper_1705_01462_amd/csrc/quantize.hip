@@ -18,6 +18,8 @@
 // The codes (qcode.h) use the correctly rounded quotient x/s from the
 // reciprocal and one exact correction rather than the full division
 // sequence, which made pass 2 compute-bound.
+#include <mutex>
+
 #include "fgq_internal.h"
 #include "qcode.h"
 
@@ -246,6 +248,30 @@ int64_t pass2_blocks(int64_t n, int32_t bits) {
 }
 
 }  // namespace
+
+// The allocation-free entry point's scratch: pass 1's partial maxima (at
+// most kMaxPartials floats for any n).  Each device holds its own copy at its
+// own address; host code uses only the address from hipGetSymbolAddress,
+// looked up once per device with that device current.
+__device__ __align__(256) float scratch[kQuantScratchFloats];
+static_assert(kQuantScratchFloats >= kMaxPartials, "scratch holds every partial");
+
+fgq_status quantize_scratch(float** out) {
+  static std::mutex mu;
+  static float* ptr[kMaxDevices] = {};
+  int dev = 0;
+  FGQ_TRY_HIP(hipGetDevice(&dev));
+  if (dev < 0 || dev >= kMaxDevices) return FGQ_ERR_HIP;
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void* p = nullptr;
+    FGQ_TRY_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (!p) return FGQ_ERR_HIP;
+    ptr[dev] = static_cast<float*>(p);
+  }
+  *out = ptr[dev];
+  return FGQ_OK;
+}
 
 int32_t quantize_partials(int64_t n) {
   int64_t b = ceil_div(ceil_div(n, 4), static_cast<int64_t>(kThreads) * kP1Vec);
