@@ -220,16 +220,19 @@ fgq_status fgq_quantize_act_noalloc(const float* x, int64_t n, int32_t bits,
  * depends on G alone:
  *
  * G = 64 with K/64 <= 160 (per-group kernel, Sec. 4: 32-bit group sums,
- * then one multiplication by the group scale per group): the ternary
- * weights as int8 in the kernel's operand order and alpha transposed per
- * group; 1 byte per weight plus 4 bytes per group.
+ * then one multiplication by the group scale per group): the 2-bit codes in
+ * the kernel's operand order (expanded to int8 in registers) and alpha
+ * transposed per group; 0.25 bytes per weight plus 4 bytes per group.
  *
  * Any other G (folded-scale kernel): the group scales are brought to one
  * grid per output channel: A[o][g] = rint(alpha[o][g] / h_o), with h_o the
  * smallest fp32 step keeping every A of the channel within
  * 127*(1 + 255 + 255^2), written as three balanced base-255 digits in
  * [-127, 127].  The folded weights t*digit are int8, so the layer runs as
- * three exact int8 products whose integer sums are combined exactly; only
+ * three exact int8 products whose integer sums are combined exactly (for
+ * G = 4 and G = 64 the convolution reads the 2-bit codes and each group's
+ * three digits, 0.25 + 3/G bytes per weight, and expands them in
+ * registers; for other G it reads the int8 planes); only
  * the rounding of alpha to the grid (at most h_o / 2, about 6e-8 times the
  * channel's largest alpha) and the fp32 conversions and fused multiply-adds
  * of the final combination differ from the exact formula.  3 bytes per

@@ -42,6 +42,7 @@
 
 #include "fgq_internal.h"
 #include "igemm.h"
+#include "xexpand.h"
 
 namespace fgq {
 namespace {
@@ -58,66 +59,6 @@ struct DfpxArgs {
   int32_t* part;          // [splits][planes][M][O]
   int32_t M, K, O, n_otiles, n_mtiles, splits, sps, nk, staged;
   int32_t q_bytes, xcodes_bytes, xacodes_bytes, xplane;  // xplane: bytes between planes
-};
-
-// Permute selectors of a quarter's 16 weights: word i, byte b = the code of
-// weight 4i+b.
-__device__ inline void selectors(uint32_t c32, uint32_t (&s)[4]) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i) s[i] = (c32 >> (2 * i)) & 0x03030303u;
-}
-
-// The quarter's int8 weights for scale bytes a (A, or a digit of it, in
-// [-127, 127]): table [0, a, 0, -a] per group, indexed by the selectors.
-// -a is formed four bytes at a time as ((a ^ 0x7F7F7F7F) + 0x01010101) ^
-// 0x80808080 (one's complement of a + 128, plus one, minus 128), with no
-// carry between bytes because no byte is -128.
-template <int kG>
-__device__ inline v4i expand16(const uint32_t (&s)[4], uint32_t a) {
-  const uint32_t na = ((a ^ 0x7F7F7F7Fu) + 0x01010101u) ^ 0x80808080u;  // per byte: -a
-  v4i w;
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t j = kG == 4 ? i : (kG == 8 ? i / 2 : 0);  // the scale byte of weights 4i..4i+3
-    // table bytes [0, a_j, 0, -a_j]; selector 12 gives a zero byte
-    const uint32_t T = __builtin_amdgcn_perm(na, a, 0x0Cu | (j << 8) | (0x0Cu << 16) | ((4u + j) << 24));
-    w[i] = static_cast<int>(__builtin_amdgcn_perm(0u, T, s[i]));
-  }
-  return w;
-}
-
-// Scale-code bytes of one lane and step: 64/G of them (one for G >= 64).
-template <int kG>
-struct ACodes {
-  static constexpr int kBytes = kG >= 64 ? 1 : 64 / kG;
-  static constexpr int kWords = kBytes >= 4 ? kBytes / 4 : 1;
-  uint32_t w[kWords];
-
-  __device__ void load(__amdgpu_buffer_rsrc_t rs, int off) {
-    if constexpr (kBytes == 16) {
-      const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
-      for (int i = 0; i < 4; ++i) w[i] = static_cast<uint32_t>(v[i]);
-    } else if constexpr (kBytes == 8) {
-      const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
-      w[0] = static_cast<uint32_t>(v.x);
-      w[1] = static_cast<uint32_t>(v.y);
-    } else if constexpr (kBytes == 4) {
-      w[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, 0, 0);
-    } else if constexpr (kBytes == 2) {
-      w[0] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, 0, 0);
-    } else {
-      w[0] = __builtin_amdgcn_raw_buffer_load_b8(rs, off, 0, 0);
-    }
-  }
-  // The A bytes of quarter h (16 weights), placed where expand16<kG> reads
-  // them: four (G = 4), two (G = 8) or one (byte 0).
-  __device__ uint32_t quarter(int h) const {
-    if constexpr (kG == 4) return w[h];
-    else if constexpr (kG == 8) return w[h / 2] >> (16 * (h % 2));
-    else if constexpr (kG == 16) return w[0] >> (8 * h);
-    else if constexpr (kG == 32) return w[0] >> (8 * (h / 2));
-    else return w[0];
-  }
 };
 
 template <int kNB, int kPlanes>

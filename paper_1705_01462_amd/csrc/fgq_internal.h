@@ -46,8 +46,8 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 // Two kinds, chosen by G alone:
 //  * group (G = 64 and at most kGroupMaxGroups groups per channel): the
 //    per-group kernel.
-//      planes : int8 ternary weights t in fragment order
-//               [O32/32][Kp/64][2 K halves][64 lanes][16 bytes]
+//      planes : the 2-bit codes in the kernel's operand order
+//               [O32/32][Kp/128][64 lanes][4 words of 16 codes] (prepare.hip)
 //      alpha  : fp32 [Kp/64][O32], alpha of group k/64 of channel o
 //  * fold (every other G): the folded-scale kernel.
 //      planes : int8 folded digits t*d_j (j = 0 least significant),
@@ -56,7 +56,8 @@ __host__ __device__ inline int64_t round_up(int64_t a, int64_t b) { return ceil_
 //      scale  : fp32  [O]     the grid step h_o (NaN: the channel fails the accuracy guard)
 //      xcodes, xacodes (G a power of two in 4..128): the 2-bit codes and the
 //               three digits of each group's scale in the codes-expanding
-//               GEMM's order (xlayout.h; digits plane-major)
+//               order (xlayout.h; digits plane-major), read by the GEMM at
+//               small batch and, for G = 4 and 64, by the convolution
 // A third kind is written by fgq_prepare_weights_dfp (any G), for the layer
 // with fixed-point group scales:
 //      header : int32 fl, the fractional length of the layer's scales

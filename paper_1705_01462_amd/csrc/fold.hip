@@ -30,6 +30,7 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
+  set_codes_operand(a, g.G, base, L, 3);
   if (fold_rows_eligible(a)) return launch_fold_rows(a, g.bits, out.bits, st);
   switch (out.bits) {
     case 0: return launch_fold_out_f32(a, g.bits, st);
@@ -61,6 +62,7 @@ fgq_status launch_fold_splitk(const uint8_t* q, const float* sx, const void* pre
   a.staged = 0;
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
+  a.xg = 0;
   fgq_status rc = launch_fold_part(a, g.bits, st);
   if (rc != FGQ_OK) return rc;
   return launch_splitk_reduce(ws, splits, /*dfp=*/false, g.M, g.O, sx, a.scale, nullptr, out, st);

@@ -30,6 +30,7 @@ fgq_status launch_fold_dfp_conv(const uint8_t* q, const float* sx, const void* p
   a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(L.O32 * L.Kp);
+  a.xg = 0;  // the one-plane kernel reads the plane (see launch_out)
   switch (out.bits) {
     case 0: return launch_fold_dfp_out_f32(a, g.bits, st);
     case 8: return launch_fold_dfp_out_q8(a, g.bits, st);
@@ -62,6 +63,7 @@ fgq_status launch_fold_dfp_splitk(const uint8_t* q, const float* sx, const void*
   a.staged = 0;
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(L.O32 * L.Kp);
+  a.xg = 0;
   fgq_status rc = launch_fold_dfp_part(a, g.bits, st);
   if (rc != FGQ_OK) return rc;
   return launch_splitk_reduce(ws, splits, /*dfp=*/true, g.M, g.O, sx, nullptr, a.fl, out, st);

@@ -51,6 +51,7 @@
 #include "igemm.h"
 #include "epilogue.h"
 #include "qcode.h"
+#include "xexpand.h"
 
 namespace fgq {
 
@@ -68,7 +69,30 @@ struct FoldArgs {
   int32_t splits, steps_per_split;  // K steps [split*sps, min(nk, (split+1)*sps)) per workgroup
   int32_t staged;        // epilogue through LDS (epi_staged)
   int32_t nks, planes_bytes;
+  // Weights as stored (xg = 4 or 64; 0: the int8 planes above): 2-bit codes
+  // and per-group int8 scale bytes (three digit planes, or the fixed-point
+  // scale codes) in the operand order of xlayout.h, expanded in registers.
+  int32_t xg;
+  const uint8_t* xcodes;
+  const int8_t* xdigits;
+  int32_t xcodes_bytes, xdigits_bytes, xplane, nk128;
 };
+
+// The codes operand of a prepared buffer (fold or fixed-point layout, with
+// `planes` scale bytes per group): used for G = 4 and G = 64, where the
+// layout holds it; otherwise xg = 0 and the kernels read the int8 planes.
+inline void set_codes_operand(FoldArgs& a, int32_t G, const char* base, const PreparedLayout& L, int planes) {
+  a.xg = 0;
+  const int64_t xnb = dfpx_acode_bytes(G);
+  if ((G != 4 && G != 64) || xnb == 0) return;
+  a.xg = G;
+  a.xcodes = reinterpret_cast<const uint8_t*>(base + L.xcodes_off);
+  a.xdigits = reinterpret_cast<const int8_t*>(base + L.xacodes_off);
+  a.xcodes_bytes = static_cast<int32_t>(L.xacodes_off - L.xcodes_off);
+  a.xdigits_bytes = static_cast<int32_t>(L.total - L.xacodes_off);
+  a.xplane = planes > 1 ? static_cast<int32_t>(round_up(a.x.O, 128) * (L.Kp / 64) * xnb) : 0;
+  a.nk128 = static_cast<int32_t>(L.Kp / 128);
+}
 
 // One launcher per output kind: kOut = 0 (fp32 y), 8 or 4 (codes).
 fgq_status launch_fold_out_f32(const FoldArgs& a, int bits, hipStream_t st);
@@ -88,7 +112,7 @@ namespace {
 
 using namespace ig;
 
-template <int kBits, int kNWO, int kNB, int kCM, int kOut, bool kDfp>
+template <int kBits, int kNWO, int kNB, int kCM, int kOut, bool kDfp, int kG>
 __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(FoldArgs a) {
   constexpr int kNWM = 4 / kNWO;
   constexpr int kTO = 32 * kNWO;
@@ -129,19 +153,40 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   // The step is the scalar offset, which the buffer range check does not
   // cover, so a step past the last is clamped to the last one (those loads
   // are never used).
-  v4i wring[2][kPlanes][4];
+  // kG > 0: the codes (16 bytes per lane and step) and each plane's scale
+  // bytes (64/G per lane and step) of the lane's channel, from the
+  // 128-channel region of the operand order that holds it; the step is the
+  // scalar offset (4 KB of codes, 256 * 64/G bytes of each plane).
+  constexpr bool kX = kG > 0;
+  using DW = ACodes<kX ? kG : 4>;
+  constexpr int kAB = DW::kBytes;
+  const int xl = ((o0 / 128) * a.nk128 * 4 + (o0 % 128) / 32) * 64 + lane;  // lane index at step 0
+  const __amdgpu_buffer_rsrc_t crs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.xcodes), 0, a.xcodes_bytes, kBufFlags);
+  const __amdgpu_buffer_rsrc_t drs =
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.xdigits), 0, a.xdigits_bytes, kBufFlags);
+
+  v4i wring[2][kX ? 1 : kPlanes][4];
+  v4i cring[2];
+  DW dring[2][kPlanes];
   auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
     ks = ks < nk ? ks : nk - 1;
+    if constexpr (kX) {
+      cring[u] = __builtin_amdgcn_raw_buffer_load_b128(crs, 16 * xl, 4096 * ks, 0);
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-      const int kso = (2 * ks + blk) * kTileB;
+      for (int j = 0; j < kPlanes; ++j) dring[u][j].load(drs, j * a.xplane + kAB * xl, 256 * kAB * ks);
+    } else {
 #pragma unroll
-      for (int j = 0; j < kPlanes; ++j)
+      for (int blk = 0; blk < 2; ++blk) {
+        const int kso = (2 * ks + blk) * kTileB;
 #pragma unroll
-        for (int h = 0; h < 2; ++h)
-          wring[u][j][2 * blk + h] =
-              __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, kso, 0);
+        for (int j = 0; j < kPlanes; ++j)
+#pragma unroll
+          for (int h = 0; h < 2; ++h)
+            wring[u][j][2 * blk + h] =
+                __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, kso, 0);
+      }
     }
   };
 
@@ -161,15 +206,18 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
     }
   }
 
-  // A-operand fragment addresses (row = wave rows + 32c + lane%32, slot
-  // 2*quarter + lane/32)
+  // A-operand fragment addresses (row = wave rows + 32c + lane%32; slot
+  // 2*quarter + lane/32 for the planes' fragment order, 4*(lane/32) +
+  // quarter for the codes' operand order: the same 16 k as the lane's
+  // weights, which is all the matrix instruction needs)
   int afrag[kNB][4];
 #pragma unroll
   for (int c = 0; c < kNB; ++c)
 #pragma unroll
-    for (int h = 0; h < 4; ++h) afrag[c][h] = lds_off(wm * kNB * 32 + 32 * c + lane % 32, 2 * h + lane / 32);
+    for (int h = 0; h < 4; ++h)
+      afrag[c][h] = lds_off(wm * kNB * 32 + 32 * c + lane % 32, kX ? 4 * (lane / 32) + h : 2 * h + lane / 32);
 
-  auto compute = [&](int stage, const v4i (&w)[kPlanes][4]) {
+  auto compute = [&](int stage, const v4i (&w)[kX ? 1 : kPlanes][4]) {
     const unsigned char* base = lds + stage * kStage;
     if constexpr (kNB <= 2) {
       // Two workgroups share the compute unit: read each K slice's
@@ -184,7 +232,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
         for (int c = 0; c < kNB; ++c)
 #pragma unroll
           for (int j = 0; j < kPlanes; ++j)
-            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], w[j][h], acc[j][c], 0, 0, 0);
+            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], w[kX ? 0 : j][h], acc[j][c], 0, 0, 0);
       }
     } else {
       v4i xf[kNB][4];
@@ -198,7 +246,29 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
         for (int c = 0; c < kNB; ++c)
 #pragma unroll
           for (int j = 0; j < kPlanes; ++j)
-            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][h], w[j][h], acc[j][c], 0, 0, 0);
+            acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][h], w[kX ? 0 : j][h], acc[j][c], 0, 0, 0);
+    }
+  };
+
+  // The same with the weights expanded from codes and scale bytes, one K
+  // quarter at a time: four permute selectors per quarter (shared by the
+  // planes), then per plane the quarter's 16 int8 weights and its matrix
+  // instructions.
+  auto compute_x = [&](int stage, const v4i& cw, const DW (&dw)[kPlanes]) {
+    const unsigned char* base = lds + stage * kStage;
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      uint32_t sel[4];
+      selectors(static_cast<uint32_t>(cw[h]), sel);
+      v4i xf[kNB];
+#pragma unroll
+      for (int c = 0; c < kNB; ++c) xf[c] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+#pragma unroll
+      for (int j = 0; j < kPlanes; ++j) {
+        const v4i wf = expand16<kX ? kG : 4>(sel, dw[j].quarter(h));
+#pragma unroll
+        for (int c = 0; c < kNB; ++c) acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], wf, acc[j][c], 0, 0, 0);
+      }
     }
   };
 
@@ -218,7 +288,10 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
     xs.load(a.x);
     __builtin_amdgcn_sched_barrier(0);
     load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
-    compute(u, wring[u]);
+    if constexpr (kX)
+      compute_x(u, cring[u], dring[u]);
+    else
+      compute(u, wring[u]);
     // Schedule: every fragment read first (distinct registers, LDS latency
     // paid once), then the matrix instructions with the weight prefetch
     // loads and their address arithmetic slotted between them, so the per-CU
@@ -299,7 +372,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   }
 }
 
-template <int kOut, bool kDfp, int kBits, int kNWO, int kNB>
+template <int kOut, bool kDfp, int kG, int kBits, int kNWO, int kNB>
 fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   constexpr int kTO = 32 * kNWO, kTM = (4 / kNWO) * kNB * 32;
   FoldArgs a = a0;
@@ -309,10 +382,20 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
   if (n > 0x7fffffffLL) return FGQ_ERR_SHAPE;
   const dim3 grid(static_cast<uint32_t>(n));
   switch (c_mode(a.x.C)) {
-    case 0: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 0, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
-    case 1: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 1, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
-    case 4: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 4, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
-    default: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 8, kOut, kDfp>), grid, dim3(kThreads), 0, st, a); break;
+    case 0: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 0, kOut, kDfp, kG>), grid, dim3(kThreads), 0, st, a); break;
+    case 1: hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 1, kOut, kDfp, kG>), grid, dim3(kThreads), 0, st, a); break;
+    case 4:
+      if constexpr (kG == 0 || kG == 4)
+        hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 4, kOut, kDfp, kG>), grid, dim3(kThreads), 0, st, a);
+      else
+        return FGQ_ERR_UNSUPPORTED;  // a group of kG channels needs C >= kG
+      break;
+    default:
+      if constexpr (kG == 0 || kG == 4)
+        hipLaunchKernelGGL((fold_conv_kernel<kBits, kNWO, kNB, 8, kOut, kDfp, kG>), grid, dim3(kThreads), 0, st, a);
+      else
+        return FGQ_ERR_UNSUPPORTED;
+      break;
   }
   return last_launch();
 }
@@ -322,21 +405,35 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
 // matrix instruction) and 128-row tiles (one workgroup per compute unit,
 // and register spills in the per-group kernel) were slower, and a tile
 // count balance of ceil(tiles / CUs) * kNB never prefers kNB = 4 over 2.
-template <int kOut, bool kDfp, int kBits, int kNWO>
+template <int kOut, bool kDfp, int kG, int kBits, int kNWO>
 fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
-  return launch_cfg<kOut, kDfp, kBits, kNWO, 2>(a, st);
+  return launch_cfg<kOut, kDfp, kG, kBits, kNWO, 2>(a, st);
 }
 
-template <int kOut, bool kDfp, int kBits>
+template <int kOut, bool kDfp, int kG, int kBits>
 fgq_status launch_bits(const FoldArgs& a, hipStream_t st) {
-  if (a.x.O > 64) return launch_nwo<kOut, kDfp, kBits, 4>(a, st);
-  if (a.x.O > 32) return launch_nwo<kOut, kDfp, kBits, 2>(a, st);
-  return launch_nwo<kOut, kDfp, kBits, 1>(a, st);
+  if (a.x.O > 64) return launch_nwo<kOut, kDfp, kG, kBits, 4>(a, st);
+  if (a.x.O > 32) return launch_nwo<kOut, kDfp, kG, kBits, 2>(a, st);
+  return launch_nwo<kOut, kDfp, kG, kBits, 1>(a, st);
 }
 
+template <int kOut, bool kDfp, int kG>
+fgq_status launch_g(const FoldArgs& a, int bits, hipStream_t st) {
+  return bits == 8 ? launch_bits<kOut, kDfp, kG, 8>(a, st) : launch_bits<kOut, kDfp, kG, 4>(a, st);
+}
+
+// Weights from codes for G = 4 and G = 64 (a.xg), else from the planes; the
+// split-K partial kernels and the one-plane layer with fixed-point scales
+// always read the planes (with one plane, the expansion's vector work
+// outweighs the bytes it saves: 10.5 against 9.4 us on the 3x3 layer of
+// 128 channels at 28x28, batch 32).
 template <int kOut, bool kDfp = false>
 fgq_status launch_out(const FoldArgs& a, int bits, hipStream_t st) {
-  return bits == 8 ? launch_bits<kOut, kDfp, 8>(a, st) : launch_bits<kOut, kDfp, 4>(a, st);
+  if constexpr (kOut != 1 && !kDfp) {
+    if (a.xg == 4) return launch_g<kOut, kDfp, 4>(a, bits, st);
+    if (a.xg == 64) return launch_g<kOut, kDfp, 64>(a, bits, st);
+  }
+  return launch_g<kOut, kDfp, 0>(a, bits, st);
 }
 
 }  // namespace

@@ -6,7 +6,7 @@ namespace fgq {
 
 bool group_supported(const ConvGeom& g, const uint8_t* q) {
   const PreparedLayout L = prepared_layout(g.O, g.K, g.G);
-  return L.kind == kPrepGroup && ig::igemm_shape_ok(g, q) && L.O32 * L.Kp < (1LL << 31) &&
+  return L.kind == kPrepGroup && ig::igemm_shape_ok(g, q) && L.O32 * L.Kp / 4 < (1LL << 31) &&
          4 * L.nks * L.O32 < (1LL << 31);
 }
 
@@ -17,7 +17,7 @@ fgq_status launch_group_conv(const uint8_t* q, const float* sx, const void* prep
   GroupArgs a;
   ig::fill_act_args(g, q, &a.x);
   a.sx = sx;
-  a.planes = reinterpret_cast<const int8_t*>(base + L.planes_off);
+  a.codes = reinterpret_cast<const uint32_t*>(base + L.planes_off);
   a.alpha = reinterpret_cast<const float*>(base + L.alpha_off);
   a.y = out.y;
   a.qo = out.q;
@@ -25,7 +25,7 @@ fgq_status launch_group_conv(const uint8_t* q, const float* sx, const void* prep
   a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
   a.nks = static_cast<int32_t>(L.nks);
   a.O32 = static_cast<int32_t>(L.O32);
-  a.planes_bytes = static_cast<int32_t>(L.O32 * L.Kp);
+  a.codes_bytes = static_cast<int32_t>(L.O32 * L.Kp / 4);
   a.alpha_bytes = static_cast<int32_t>(4 * L.nks * L.O32);
   switch (out.bits) {
     case 0: return launch_group_out_f32(a, g.bits, st);

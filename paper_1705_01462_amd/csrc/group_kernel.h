@@ -18,8 +18,10 @@
 // result is exactly -P and the epilogue multiplies by -alpha.  uint4
 // activations (0..15) need no offset.
 //
-// Staging of activations (LDS) and weights (fragment-ordered, straight to
-// registers) follows the folded-scale kernel; see igemm.h.
+// Staging of activations (LDS) follows the folded-scale kernel; see
+// igemm.h.  The weights are read as the 2-bit codes (one 16-byte load per
+// lane and step, a contiguous kilobyte per wave, see prepare.hip) and
+// expanded to int8 in registers, one byte permute per four weights.
 //
 // The output kind is a template parameter (fp32 y, or 8-/4-bit codes of the
 // next layer's activations); each kind is instantiated in a source file of
@@ -29,19 +31,20 @@
 #include "igemm.h"
 #include "epilogue.h"
 #include "qcode.h"
+#include "xexpand.h"
 
 namespace fgq {
 
 struct GroupArgs {
   ig::ActArgs x;
   const float* sx;
-  const int8_t* planes;  // [O32/32][Kp/64][2][64][16]
+  const uint32_t* codes;  // [O32/32][Kp/128][64 lanes][4 words], see prepare.hip
   const float* alpha;    // [Kp/64][O32]
   float* y;
   uint8_t* qo;           // output codes (kOut 8 or 4)
   const float* oscale;   // their scale
   int32_t staged;        // epilogue through LDS (epi_staged)
-  int32_t nks, O32, planes_bytes, alpha_bytes;
+  int32_t nks, O32, codes_bytes, alpha_bytes;
 };
 
 // One launcher per output kind: kOut = 0 (fp32 y), 8 or 4 (codes).
@@ -53,7 +56,7 @@ namespace {
 
 using namespace ig;
 
-constexpr int kBlkBytes = 2 * 64 * 16;  // one channel tile, one group
+constexpr int kStepBytes = 64 * 16;  // codes of one channel tile, one 128-wide step
 
 // Two workgroups may share a compute unit (at most 256 registers per lane):
 // with two waves per SIMD, one wave's conversions and multiply-adds run
@@ -76,33 +79,29 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
   const int m0 = (tile / a.x.n_otiles) * kTM;             // workgroup's first row
 
   const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.planes), 0, a.planes_bytes, kBufFlags);
+      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(a.codes), 0, a.codes_bytes, kBufFlags);
   const __amdgpu_buffer_rsrc_t ars =
       __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.alpha), 0, a.alpha_bytes, kBufFlags);
-  const int wbase = (o0 / 32) * a.nks * kBlkBytes + 16 * lane;
+  const int nk = (a.x.K + kKT - 1) / kKT;
+  const int wbase = (o0 / 32) * nk * kStepBytes + 16 * lane;
   const int abase = 4 * (o0 + lane % 32);
 
-  const int nk = (a.x.K + kKT - 1) / kKT;
   Stager xs;
   xs.init(a.x, m0, tid);
 
-  // Weights and scales of one step (two groups).  The step is the scalar
+  // Codes and scales of one step (two groups).  The step is the scalar
   // offset, which the buffer range check does not cover, so a step past the
   // last is clamped to the last one (those loads are never used).
-  v4i wring[2][2][2];
+  v4i cring[2];
   float aring[2][2];
   auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
     ks = ks < nk ? ks : nk - 1;
+    cring[u] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase, ks * kStepBytes, 0);
 #pragma unroll
-    for (int blk = 0; blk < 2; ++blk) {
-      const int g = 2 * ks + blk;
-#pragma unroll
-      for (int h = 0; h < 2; ++h)
-        wring[u][blk][h] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + h * 1024, g * kBlkBytes, 0);
+    for (int blk = 0; blk < 2; ++blk)
       aring[u][blk] = __builtin_bit_cast(
-          float, __builtin_amdgcn_raw_buffer_load_b32(ars, abase, g * a.O32 * 4, 0));
-    }
+          float, __builtin_amdgcn_raw_buffer_load_b32(ars, abase, (2 * ks + blk) * a.O32 * 4, 0));
   };
 
   v16f acc[kNB];
@@ -121,10 +120,12 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
                          static_cast<int>(0x81818181u), static_cast<int>(0x81818181u)};
   const v16i kZero = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
 
-  auto compute = [&](int stage, const v4i (&w)[2][2], const float (&al)[2]) {
+  auto compute = [&](int stage, const v4i& cw, const float (&al)[2]) {
     const unsigned char* base = lds + stage * kStage;
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk) {
+      const v4i w[2] = {expand_ternary16(static_cast<uint32_t>(cw[2 * blk])),
+                        expand_ternary16(static_cast<uint32_t>(cw[2 * blk + 1]))};
       v4i xf[kNB][2];
 #pragma unroll
       for (int c = 0; c < kNB; ++c)
@@ -133,14 +134,14 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
           xf[c][h] = *reinterpret_cast<const v4i*>(base + afrag[c][2 * blk + h]);
       v16i init = kZero;
       if constexpr (kBits == 8) {
-        init = __builtin_amdgcn_mfma_i32_32x32x32_i8(kMinus127, w[blk][0], kZero, 0, 0, 0);
-        init = __builtin_amdgcn_mfma_i32_32x32x32_i8(kMinus127, w[blk][1], init, 0, 0, 0);
+        init = __builtin_amdgcn_mfma_i32_32x32x32_i8(kMinus127, w[0], kZero, 0, 0, 0);
+        init = __builtin_amdgcn_mfma_i32_32x32x32_i8(kMinus127, w[1], init, 0, 0, 0);
       }
       const float s = kBits == 8 ? -al[blk] : al[blk];
 #pragma unroll
       for (int c = 0; c < kNB; ++c) {
-        v16i p = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][0], w[blk][0], init, 0, 0, 0);
-        p = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][1], w[blk][1], p, 0, 0, 0);
+        v16i p = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][0], w[0], init, 0, 0, 0);
+        p = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c][1], w[1], p, 0, 0, 0);
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[c][r] = fmaf(s, static_cast<float>(p[r]), acc[c][r]);
       }
@@ -159,7 +160,7 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
     xs.load(a.x);
     __builtin_amdgcn_sched_barrier(0);
     load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
-    compute(u, wring[u], aring[u]);
+    compute(u, cring[u], aring[u]);
     __builtin_amdgcn_sched_barrier(0);  // the publish waits for the prefetch: keep it last
     xs.store(lds + (1 - u) * kStage, kMask);
     __syncthreads();

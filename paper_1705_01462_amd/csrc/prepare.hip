@@ -1,9 +1,10 @@
 // prepare.hip -- per-layer constants of the matrix-core kernels.
 //
 // Group size 64 (a group is two K slices of the 32x32x32 int8 instruction):
-// the per-group kernel takes the ternary weights as int8 in fragment order
-// and alpha transposed to [K/64][O32], so that one wave reads the alphas of
-// its 32 channels for one group as 128 contiguous bytes.
+// the per-group kernel takes the ternary weights as 2-bit codes in its
+// operand order (expanded to int8 in registers) and alpha transposed to
+// [K/64][O32], so that one wave reads the alphas of its 32 channels for one
+// group as 128 contiguous bytes.
 //
 // Other group sizes: the folded-scale kernel.
 // y[m][o] = s_x * sum_k q[m][k] * alpha[o][g(k)] * t[o][k] is a dense GEMM
@@ -41,7 +42,7 @@ PreparedLayout prepared_layout(int64_t O, int64_t K, int32_t G) {
   L.planes_off = 0;
   if (G == 64 && K / 64 <= kGroupMaxGroups) {
     L.kind = kPrepGroup;
-    L.alpha_off = round_up(L.O32 * L.Kp, 256);
+    L.alpha_off = round_up(L.O32 * L.Kp / 4, 256);
     L.total = round_up(L.alpha_off + 4 * L.nks * L.O32, 256);
     L.bias_off = L.scale_off = L.total;
     L.xcodes_off = L.xacodes_off = L.total;
@@ -201,23 +202,30 @@ __global__ __launch_bounds__(kThreads) void prepare_kernel(
   }
 }
 
-// Group kind: one block per channel of the padded channel range.
+// Group kind: one block per channel of the padded channel range.  The
+// ternary codes go in the per-group kernel's operand order: lane
+// l = o%32 + 32*hf of channel tile o/32 holds, in 128-wide step ks, four
+// 32-bit words d = 2*blk + h, word d holding the 16 codes of
+// k = 128*ks + 64*blk + 32*h + 16*hf + [0, 16) with the code of k0 + 4i + b
+// in byte b at bits 2i (so one wave-wide load of a step is one contiguous
+// kilobyte, and a word's four permute selectors are a shift and a mask).
 __global__ __launch_bounds__(kThreads) void prepare_group_kernel(
     const uint8_t* __restrict__ codes, const float* __restrict__ alpha, int64_t O,
-    int64_t K, int64_t Kp, int64_t O32, int8_t* __restrict__ planes,
+    int64_t K, int64_t Kp, int64_t O32, uint32_t* __restrict__ gcodes,
     float* __restrict__ alpha_t) {
   const int64_t o = blockIdx.x;
-  const int64_t nks = Kp / kFoldKStep, ng = K / 64, rb = ceil_div(K, 4);
-  for (int64_t k = threadIdx.x; k < Kp; k += kThreads) {
-    int t = 0;
-    if (o < O && k < K) {
-      const uint32_t c = (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u;
-      t = c == 1 ? 1 : (c == 3 ? -1 : 0);
+  const int64_t nks = Kp / kFoldKStep, nk = Kp / 128, ng = K / 64, rb = ceil_div(K, 4);
+  for (int64_t e = threadIdx.x; e < nk * 8; e += kThreads) {
+    const int64_t ks = e / 8;
+    const int hf = static_cast<int>((e / 4) % 2), d = static_cast<int>(e % 4);
+    const int64_t k0 = 128 * ks + 32 * d + 16 * hf;  // 64*blk + 32*h = 32*d
+    uint32_t v = 0;
+    for (int j = 0; j < 16; ++j) {
+      const int64_t k = k0 + j;
+      const uint32_t c = (o < O && k < K) ? (codes[o * rb + k / 4] >> (2 * (k % 4))) & 3u : 0u;
+      v |= c << (8 * (j % 4) + 2 * (j / 4));
     }
-    const int64_t tile = o / 32, ks = k / kFoldKStep;
-    const int kk = static_cast<int>(k % kFoldKStep);
-    const int half = kk / 32, lane = static_cast<int>(o % 32) + 32 * ((kk % 32) / 16);
-    planes[((tile * nks + ks) * 2 + half) * 1024 + lane * 16 + (kk % 16)] = static_cast<int8_t>(t);
+    gcodes[((o / 32 * nk + ks) * 64 + o % 32 + 32 * hf) * 4 + d] = v;
   }
   for (int64_t gi = threadIdx.x; gi < nks; gi += kThreads)
     alpha_t[gi * O32 + o] = (o < O && gi < ng) ? alpha[o * ng + gi] : 0.0f;
@@ -233,7 +241,7 @@ fgq_status launch_prepare(const uint8_t* codes, const float* alpha, int64_t O, i
   if (L.kind == kPrepGroup) {
     hipLaunchKernelGGL(prepare_group_kernel, dim3(static_cast<uint32_t>(L.O32)), dim3(kThreads), 0,
                        st, codes, alpha, O, K, L.Kp, L.O32,
-                       reinterpret_cast<int8_t*>(base + L.planes_off),
+                       reinterpret_cast<uint32_t*>(base + L.planes_off),
                        reinterpret_cast<float*>(base + L.alpha_off));
     return last_launch();
   }

@@ -46,8 +46,8 @@ def test_host_helpers():
     assert L.fgq_quantize_ws_bytes(32 * 28 * 28 * 128) >= 4
     for code in range(10):
         assert L.fgq_status_string(code).startswith(b"FGQ")
-    # per-group layout (G = 64, at most 160 groups): 1 byte per weight + alpha
-    assert L.fgq_prepared_bytes(128, 1152, 64) == 128 * 1152 + 4 * 18 * 128
+    # per-group layout (G = 64, at most 160 groups): 2-bit codes + alpha
+    assert L.fgq_prepared_bytes(128, 1152, 64) == 128 * 1152 // 4 + 4 * 18 * 128
     assert L.fgq_prepared_bytes(40, 64 * 161, 64) >= 3 * 64 * 64 * 161  # folded beyond 160 groups
 
 
