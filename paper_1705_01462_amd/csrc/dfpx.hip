@@ -25,13 +25,13 @@
 // exactly this order ([O/128][K/128][4 waves][64 lanes][16 code bytes, or
 // 64/G scale-code bytes]), so every weight load of a wave reads one
 // contiguous block (a kilobyte of codes), and within a quarter's 32 bits of
-// codes byte b holds, at bits 2i, the code of weight 4i+b: the selector
-// bytes of weights 4i..4i+3 are (codes >> 2i) & 0x03030303.
+// codes byte b holds, at bits 2i, the code of weight 4i+b: the codes of
+// weights 4i..4i+3 are the bytes of (codes >> 2i) & 0x03030303.
 //
-// Expansion of 4 weights of one group: a byte table [0, A, 0, -A] (-A
-// formed four bytes at a time as (0x80808080 - a) ^ 0x80808080, exact
-// because 0 <= A <= 127) indexed by those selectors with one byte permute.
-// Code 2 is never written; its table byte is 0.
+// Expansion (xexpand.h): each weight's code is turned into a byte selector
+// by a permute through a constant table, then one permute per four weights
+// picks 0, A or -A from the scale bytes and their negations.  Code 2 is
+// never written.
 //
 // Padding: codes and scale codes past K and past O are zero in the prepared
 // layout, so padded activations (past K, or rows past M) meet zero weights;
@@ -181,13 +181,13 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
       uint32_t sel[4];
-      selectors(static_cast<uint32_t>(cw[s][h]), sel);
+      selectors<kG>(static_cast<uint32_t>(cw[s][h]), sel);
       v4i xf[kNB];
 #pragma unroll
       for (int c = 0; c < kNB; ++c) xf[c] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
 #pragma unroll
       for (int j = 0; j < kPlanes; ++j) {
-        const v4i wf = expand16<kG>(sel, aw[j][s].quarter(h));
+        const v4i wf = expand16(sel, aw[j][s].quarter(h));
 #pragma unroll
         for (int c = 0; c < kNB; ++c) acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], wf, acc[j][c], 0, 0, 0);
       }

@@ -252,22 +252,55 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 
   // The same with the weights expanded from codes and scale bytes, one K
   // quarter at a time: four permute selectors per quarter (shared by the
-  // planes), then per plane the quarter's 16 int8 weights and its matrix
-  // instructions.
+  // planes), then per plane the quarter's 16 int8 weights.  Software
+  // pipelined: quarter h+1 is expanded (vector ALU) while quarter h's matrix
+  // instructions run, so only quarter 0's expansion precedes them.
+  auto expand_q = [&](int h, const v4i& cw, const DW (&dw)[kPlanes], v4i (&wq)[kPlanes]) {
+    uint32_t sel[4];
+    selectors<kX ? kG : 4>(static_cast<uint32_t>(cw[h]), sel);
+#pragma unroll
+    for (int j = 0; j < kPlanes; ++j) wq[j] = expand16(sel, dw[j].quarter(h));
+  };
   auto compute_x = [&](int stage, const v4i& cw, const DW (&dw)[kPlanes]) {
     const unsigned char* base = lds + stage * kStage;
+    v4i wq[2][kPlanes];
+    v4i xf[2][kNB];
+#pragma unroll
+    for (int c = 0; c < kNB; ++c) xf[0][c] = *reinterpret_cast<const v4i*>(base + afrag[c][0]);
+    expand_q(0, cw, dw, wq[0]);
 #pragma unroll
     for (int h = 0; h < 4; ++h) {
-      uint32_t sel[4];
-      selectors(static_cast<uint32_t>(cw[h]), sel);
-      v4i xf[kNB];
+      if (h < 3) {
 #pragma unroll
-      for (int c = 0; c < kNB; ++c) xf[c] = *reinterpret_cast<const v4i*>(base + afrag[c][h]);
+        for (int c = 0; c < kNB; ++c) xf[(h + 1) & 1][c] = *reinterpret_cast<const v4i*>(base + afrag[c][h + 1]);
+        expand_q(h + 1, cw, dw, wq[(h + 1) & 1]);
+      }
 #pragma unroll
-      for (int j = 0; j < kPlanes; ++j) {
-        const v4i wf = expand16<kX ? kG : 4>(sel, dw[j].quarter(h));
+      for (int j = 0; j < kPlanes; ++j)
 #pragma unroll
-        for (int c = 0; c < kNB; ++c) acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[c], wf, acc[j][c], 0, 0, 0);
+        for (int c = 0; c < kNB; ++c)
+          acc[j][c] = __builtin_amdgcn_mfma_i32_32x32x32_i8(xf[h & 1][c], wq[h & 1][j], acc[j][c], 0, 0, 0);
+    }
+  };
+  // Instruction order of a codes step (a hint to the scheduler, in groups):
+  // the first quarter's fragment reads and expansion, then each quarter's
+  // matrix instructions one at a time with the next quarter's expansion
+  // and fragment reads between them, the weight prefetch loads among the
+  // first quarter's.
+  constexpr int kExpV = kX ? 11 + (kG == 4 ? 7 : 4) * kPlanes : 0;  // vector ops per quarter's expansion
+  constexpr int kMq = kPlanes * kNB;                                   // matrix ops per quarter
+  constexpr int kVper = (kExpV + kMq - 1) / (kMq > 0 ? kMq : 1);
+  auto schedule_x = [&]() {
+    __builtin_amdgcn_sched_group_barrier(0x100, kNB, 0);   // quarter 0 fragment reads
+    __builtin_amdgcn_sched_group_barrier(0x002, kExpV, 0);  // quarter 0 expansion
+#pragma unroll
+    for (int h = 0; h < 4; ++h) {
+      if (h < 3) __builtin_amdgcn_sched_group_barrier(0x100, kNB, 0);  // next quarter's fragments
+#pragma unroll
+      for (int i = 0; i < kMq; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (h == 0 && i < 1 + kPlanes) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);  // weight prefetch
+        if (h < 3) __builtin_amdgcn_sched_group_barrier(0x002, kVper, 0);
       }
     }
   };
@@ -288,10 +321,12 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
     xs.load(a.x);
     __builtin_amdgcn_sched_barrier(0);
     load_w(std::integral_constant<int, 1 - u>{}, ks + 1);
-    if constexpr (kX)
+    if constexpr (kX) {
       compute_x(u, cring[u], dring[u]);
-    else
+      schedule_x();
+    } else {
       compute(u, wring[u]);
+    }
     // Schedule: every fragment read first (distinct registers, LDS latency
     // paid once), then the matrix instructions with the weight prefetch
     // loads and their address arithmetic slotted between them, so the per-CU

@@ -17,29 +17,33 @@
 namespace fgq {
 namespace ig {
 
-// Permute selectors of a quarter's 16 weights: word i, byte b = the code of
-// weight 4i+b.
+// Permute selectors of a quarter's 16 weights for the scale bytes' table:
+// word i, byte b selects the int8 weight of weight 4i+b from the pair
+// (-a, a) of scale-byte words (v_perm: selector j picks byte j of a, 4+j
+// byte j of -a, 12 a zero byte).  The code c of each weight is turned into
+// that selector by a first permute through the constant table
+// [12, j, 12, 4+j] (code 0 -> zero, 1 -> +a_j, 3 -> -a_j; code 2 is never
+// written), j being the scale byte of weights 4i..4i+3.  The selectors
+// depend on the codes only, so the planes of one quarter share them.
+template <int kG>
 __device__ inline void selectors(uint32_t c32, uint32_t (&s)[4]) {
 #pragma unroll
-  for (int i = 0; i < 4; ++i) s[i] = (c32 >> (2 * i)) & 0x03030303u;
+  for (int i = 0; i < 4; ++i) {
+    const uint32_t j = kG == 4 ? i : (kG == 8 ? i / 2 : 0);
+    const uint32_t lut = 0x0Cu | (j << 8) | (0x0Cu << 16) | ((4u + j) << 24);
+    s[i] = __builtin_amdgcn_perm(0u, lut, (c32 >> (2 * i)) & 0x03030303u);
+  }
 }
 
 // The quarter's int8 weights for scale bytes a (A, or a digit of it, in
-// [-127, 127]): table [0, a, 0, -a] per group, indexed by the selectors.
-// -a is formed four bytes at a time as ((a ^ 0x7F7F7F7F) + 0x01010101) ^
-// 0x80808080 (one's complement of a + 128, plus one, minus 128), with no
-// carry between bytes because no byte is -128.
-template <int kG>
+// [-127, 127]).  -a is formed four bytes at a time as ((a ^ 0x7F7F7F7F) +
+// 0x01010101) ^ 0x80808080 (one's complement of a + 128, plus one, minus
+// 128), with no carry between bytes because no byte is -128.
 __device__ inline v4i expand16(const uint32_t (&s)[4], uint32_t a) {
   const uint32_t na = ((a ^ 0x7F7F7F7Fu) + 0x01010101u) ^ 0x80808080u;  // per byte: -a
   v4i w;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const uint32_t j = kG == 4 ? i : (kG == 8 ? i / 2 : 0);  // the scale byte of weights 4i..4i+3
-    // table bytes [0, a_j, 0, -a_j]; selector 12 gives a zero byte
-    const uint32_t T = __builtin_amdgcn_perm(na, a, 0x0Cu | (j << 8) | (0x0Cu << 16) | ((4u + j) << 24));
-    w[i] = static_cast<int>(__builtin_amdgcn_perm(0u, T, s[i]));
-  }
+  for (int i = 0; i < 4; ++i) w[i] = static_cast<int>(__builtin_amdgcn_perm(na, a, s[i]));
   return w;
 }
 
