@@ -46,6 +46,9 @@ def lib():
                                  _c_i64, _c_i64, _c_i32, _c_p]
         L.orc_gemm.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_p, _c_p, _c_i64, _c_i32,
                                _c_i32, _c_p]
+        L.orc_conv2d_rows.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_i64, _c_i64, _c_p, _c_p,
+                                      _c_i64, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32,
+                                      _c_p, _c_i64, _c_i32, _c_p, _c_p]
         L.orc_dfp_alpha.argtypes = [_c_p, _c_i64, _c_i32, _c_p, _c_p]
         L.orc_conv2d_dfp.argtypes = [_c_p, _c_i32, _c_f32, _c_i64, _c_i64, _c_i64, _c_i64, _c_p, _c_p,
                                      _c_i32, _c_i64, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32, _c_i32,
@@ -63,7 +66,7 @@ def lib():
         L.orc_gauss_u.argtypes = []
         L.orc_gauss_u.restype = ctypes.c_double
         for f in ("orc_ternarize_group", "orc_ternarize", "orc_quantize_act",
-                  "orc_group_sums_conv", "orc_conv2d", "orc_gemm", "orc_dfp_alpha",
+                  "orc_group_sums_conv", "orc_conv2d", "orc_conv2d_rows", "orc_gemm", "orc_dfp_alpha",
                   "orc_conv2d_dfp", "orc_gemm_dfp", "orc_w8_quantize", "orc_conv2d_w8",
                   "orc_max_threads", "orc_ternarize_group_asym", "orc_ternarize_asym",
                   "orc_ks_distances"):
@@ -229,6 +232,22 @@ def conv2d(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, G, rows=None,
                             R, S, stride[0], stride[1], pad[0], pad[1], G, row0, nrows,
                             nthreads, _ptr(y)))
     return y
+
+
+def conv2d_rows(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, G, rows, nthreads=0):
+    """The layer on the listed output rows: (y float32 [len(rows)][O], summand
+    magnitude s_x * sum_g alpha_g |P_g| float64 [len(rows)][O])."""
+    B, H, W, C = shape
+    rows = np.ascontiguousarray(rows, dtype=np.int64)
+    y = np.empty((len(rows), O), np.float32)
+    mag = np.empty((len(rows), O), np.float64)
+    q = np.ascontiguousarray(q, dtype=np.uint8)
+    codes = np.ascontiguousarray(codes, dtype=np.uint8)
+    alpha = np.ascontiguousarray(alpha, dtype=np.float32)
+    _check(lib().orc_conv2d_rows(_ptr(q), bits, float(sx), B, H, W, C, _ptr(codes), _ptr(alpha), O,
+                                 R, S, stride[0], stride[1], pad[0], pad[1], G, _ptr(rows), len(rows),
+                                 nthreads, _ptr(y), _ptr(mag)))
+    return y, mag
 
 
 def gemm(q, bits, sx, M, K, codes, alpha, O, G, nthreads=0):

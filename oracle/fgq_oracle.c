@@ -501,6 +501,45 @@ int orc_conv2d(const uint8_t* q, int32_t bits, float sx, int64_t B, int64_t H,
   return ORC_OK;
 }
 
+int orc_conv2d_rows(const uint8_t* q, int32_t bits, float sx, int64_t B, int64_t H,
+                    int64_t W, int64_t C, const uint8_t* codes, const float* alpha,
+                    int64_t O, int32_t R, int32_t S, int32_t sh, int32_t sw,
+                    int32_t ph, int32_t pw, int32_t G, const int64_t* rows,
+                    int64_t nrows, int32_t nthreads, float* y, double* mag) {
+  if (!q || !codes || !alpha || !rows || !y || !mag) return ORC_ERR_NULL;
+  if (bits != 8 && bits != 4) return ORC_ERR_BITS;
+  geom_t g;
+  int rc = conv_geom(B, H, W, C, O, R, S, sh, sw, ph, pw, &g);
+  if (rc) return rc;
+  if (G < 1 || C % G != 0) return ORC_ERR_GROUP;
+  const int64_t M = g.B * g.Ho * g.Wo;
+  for (int64_t i = 0; i < nrows; ++i)
+    if (rows[i] < 0 || rows[i] >= M) return ORC_ERR_SHAPE;
+  const int64_t K = g.K, ng = K / G;
+  int8_t* t = (int8_t*)malloc((size_t)(O * K));
+  if (!t) return ORC_ERR_SHAPE;
+  orc_unpack_codes(codes, O, K, t);
+  const int nt = nthreads > 0 ? nthreads : omp_get_max_threads();
+#pragma omp parallel for schedule(dynamic, 4) num_threads(nt)
+  for (int64_t i = 0; i < nrows; ++i) {
+    const int64_t m = rows[i];
+    for (int64_t o = 0; o < O; ++o) {
+      double acc = 0.0, abs_acc = 0.0;
+      for (int64_t gi = 0; gi < ng; ++gi) {
+        int64_t P = 0;
+        for (int64_t k = gi * G; k < (gi + 1) * G; ++k)
+          P += (int64_t)t[o * K + k] * (int64_t)conv_a(q, bits, &g, m, k);
+        acc += (double)alpha[o * ng + gi] * (double)P;
+        abs_acc += (double)alpha[o * ng + gi] * (double)(P < 0 ? -P : P);
+      }
+      y[i * O + o] = (float)((double)sx * acc);
+      mag[i * O + o] = (double)sx * abs_acc;
+    }
+  }
+  free(t);
+  return ORC_OK;
+}
+
 int orc_gemm(const uint8_t* q, int32_t bits, float sx, int64_t M, int64_t K,
              const uint8_t* codes, const float* alpha, int64_t O, int32_t G,
              int32_t nthreads, float* y) {

@@ -129,6 +129,17 @@ int orc_conv2d(const uint8_t* q, int32_t bits, float sx, int64_t B, int64_t H,
                int32_t ph, int32_t pw, int32_t G, int64_t row0, int64_t nrows,
                int32_t nthreads, float* y);
 
+/* The layer of orc_conv2d on a list of output rows (rows[0..nrows), any
+ * order): y[i][o] is orc_conv2d's value for row rows[i], and mag[i][o] =
+ * s_x * sum_g alpha[o][g] * |P_g| (fp64), the summand magnitude against
+ * which the matrix-core kernels' tolerance is measured.  For sampled parity
+ * checks of large layers. */
+int orc_conv2d_rows(const uint8_t* q, int32_t bits, float sx, int64_t B, int64_t H,
+                    int64_t W, int64_t C, const uint8_t* codes, const float* alpha,
+                    int64_t O, int32_t R, int32_t S, int32_t sh, int32_t sw,
+                    int32_t ph, int32_t pw, int32_t G, const int64_t* rows,
+                    int64_t nrows, int32_t nthreads, float* y, double* mag);
+
 int orc_gemm(const uint8_t* q, int32_t bits, float sx, int64_t M, int64_t K,
              const uint8_t* codes, const float* alpha, int64_t O, int32_t G,
              int32_t nthreads, float* y);

@@ -52,6 +52,7 @@ CASES = [
     (2, 6, 6, 6, 6, 3, 3, 1, 1, 3, 8, 8),       # direct path only (C % 4 != 0)
     (32, 28, 28, 128, 128, 3, 3, 1, 1, 4, 8, 8),  # benchmark layer, G=4
     (32, 28, 28, 128, 128, 3, 3, 1, 1, 64, 8, 8),  # and G=64
+    (2, 9, 11, 256, 72, 3, 3, 1, 1, 4, 4, 4),   # input-patch staging, two chunks
 ]
 
 

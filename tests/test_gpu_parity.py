@@ -23,6 +23,24 @@ pytestmark = [pytest.mark.gpu,
 TOL = 1e-5
 
 
+def sampled_rows(M, seed, tile=64, ntiles=64):
+    """4096 rows of an M-row layer (all of them if fewer): whole tiles, the
+    first and last, the first and last of each eighth of the range, the rest
+    seeded and scattered."""
+    nt = (M + tile - 1) // tile
+    if nt <= ntiles:
+        return np.arange(M)
+    must = {0, nt - 1}
+    for x in range(8):
+        must.add(x * nt // 8)
+        must.add((x + 1) * nt // 8 - 1)
+    rest = np.setdiff1d(np.arange(nt), sorted(must))
+    pick = np.random.default_rng(seed).choice(rest, ntiles - len(must), replace=False)
+    tiles = np.sort(np.concatenate([sorted(must), pick]))
+    rows = (tiles[:, None] * tile + np.arange(tile)[None, :]).ravel()
+    return rows[rows < M]
+
+
 def dev(a):
     return torch.from_numpy(np.ascontiguousarray(a)).cuda()
 
@@ -216,6 +234,14 @@ LAYER_CASES = [
     (2, 6, 6, 6, 5, 3, 3, 1, 1, 3, 8),         # G = 3, C % 4 != 0
     (2, 6, 6, 16, 9, 3, 3, 1, 1, 1, 4),        # G = 1
     (4, 14, 14, 256, 64, 1, 1, 1, 0, 64, 8),
+    # input-patch staging (C % 128 == 0, R*S > 1, O > 64): several chunks,
+    # 4-bit activations, stride 2, a 5x5 filter, tiles spanning images, and
+    # G = 64 beyond 160 groups (folded layout)
+    (2, 9, 11, 256, 72, 3, 3, 1, 1, 4, 4),
+    (3, 12, 10, 384, 130, 3, 3, 2, 1, 4, 8),
+    (2, 8, 8, 128, 96, 5, 5, 1, 2, 4, 8),
+    (5, 5, 5, 256, 128, 3, 3, 1, 1, 4, 8),
+    (1, 6, 6, 1280, 80, 3, 3, 1, 1, 64, 8),
 ]
 
 
@@ -330,7 +356,8 @@ FULL = [
 @pytest.mark.parametrize("case", FULL)
 def test_full_size_layers_sampled_rows(case):
     """Full-size layers, launched exactly as the benchmark launches them;
-    the oracle computes sampled row ranges (first, middle, last)."""
+    the oracle computes 4096 sampled rows (64 tiles of 64, scattered, the
+    first and last tile and those at each eighth of the range included)."""
     B, H, W, C, O, R, S, st, pd, G, bits = case
     w = fi.he_weights(O, C, R, S, "full", case)
     x = fi.relu_gauss((B, H, W, C), "full", case)
@@ -346,14 +373,11 @@ def test_full_size_layers_sampled_rows(case):
                                  prepared=prep)).reshape(-1, O)
     y_dir = host(fgq.fgq_conv2d(q, bits, sx, (B, H, W, C), codes, alpha, O, R, S, st, pd, G)).reshape(-1, O)
     M = y_fold.shape[0]
-    ref = dict(q=q_ref, s=s_ref, codes=codes_ref, a=a)
-    for row0 in (0, M // 2 - 97, M - 200):
-        rows = (row0, 200)
-        y_ref = oracle.conv2d(q_ref, bits, s_ref, x.shape, codes_ref, a, O, R, S, (st, st), (pd, pd), G,
-                              rows=rows)[row0:row0 + 200]
-        mag = summand_magnitude(ref, x.shape, G, bits, O, R, S, st, pd, row0, 200)
-        assert_fold_close(y_fold[row0:row0 + 200], y_ref, mag)
-        np.testing.assert_array_equal(y_dir[row0:row0 + 200].view(np.uint32), y_ref.view(np.uint32))
+    rows = sampled_rows(M, seed=sum(case))
+    y_ref, mag = oracle.conv2d_rows(q_ref, bits, s_ref, x.shape, codes_ref, a, O, R, S, (st, st), (pd, pd), G,
+                                    rows)
+    assert_fold_close(y_fold[rows], y_ref, mag)
+    np.testing.assert_array_equal(y_dir[rows].view(np.uint32), y_ref.view(np.uint32))
 
 
 @pytest.mark.parametrize("G", [4, 64])

@@ -52,6 +52,16 @@ def setup(M, K, O, G, bits, tag):
     return w, x, codes, alpha, q, sx
 
 
+def oracle_close(w, x, y, M, K, O, G, bits):
+    """y within 1e-5 of the oracle's summand magnitude, element by element."""
+    t, a, _ = oracle.ternarize(w, G)
+    qr, sr = oracle.quantize_act(x, bits)
+    y_ref, mag = oracle.conv2d_rows(qr, bits, sr, (1, M, 1, K), oracle.pack_codes(t), a, O, 1, 1, (1, 1),
+                                    (0, 0), G, np.arange(M))
+    err = np.abs(y.reshape(M, O).astype(np.float64) - y_ref.astype(np.float64))
+    assert np.all(err <= 1e-5 * mag), f"worst {np.max(err / np.maximum(mag, 1e-300)):.3e}"
+
+
 @pytest.mark.parametrize("case", CASES)
 def test_gemm_ws_equals_unsplit(case):
     M, K, O, G, bits = case
@@ -61,6 +71,7 @@ def test_gemm_ws_equals_unsplit(case):
     y = host(fgq.fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
     y_ws = host(fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
     np.testing.assert_array_equal(y_ws.view(np.uint32), y.view(np.uint32))
+    oracle_close(w, x, y_ws, M, K, O, G, bits)
     for out_bits in (8, 4):
         sc = dev(np.array([np.float32(0.9 * float(np.abs(y).max()) / (2 ** out_bits - 1))], np.float32))
         a = host(fgq.fgq_gemm_q(q, bits, sx, M, K, codes, alpha, O, G, out_bits, sc, prepared=prep))
@@ -133,6 +144,7 @@ def test_gemm_ws_codes_path_equals_unsplit(case):
     y = host(fgq.fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
     y_ws = host(fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep))
     np.testing.assert_array_equal(y_ws.view(np.uint32), y.view(np.uint32))
+    oracle_close(w, x, y_ws, M, K, O, G, bits)
     sc = dev(np.array([np.float32(0.9 * float(np.abs(y).max()) / 255)], np.float32))
     a = host(fgq.fgq_gemm_q(q, bits, sx, M, K, codes, alpha, O, G, 8, sc, prepared=prep))
     b = host(fgq.fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=prep, out_bits=8, out_scale=sc))

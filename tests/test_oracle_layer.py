@@ -112,6 +112,30 @@ def test_group_sums_against_unfold():
     np.testing.assert_array_equal(P2, P[5:12])
 
 
+@pytest.mark.parametrize("case", [(2, 9, 7, 16, 12, 3, 3, 2, 1, 4, 8), (3, 6, 6, 64, 5, 1, 1, 1, 0, 64, 4)])
+def test_rows_variant_and_summand_magnitude(case):
+    """conv2d_rows (a list of rows, any order, repeats allowed) gives the
+    full convolution's values bit for bit, and its magnitude is
+    s_x * sum_g alpha_g |P_g| from the group sums (pinned against unfold
+    below), summed independently with numpy."""
+    B, H, W, C, O, R, S, st, pd, G, bits = case
+    w = fi.he_weights(O, C, R, S, "rows", case)
+    x = fi.relu_gauss((B, H, W, C), "rows", case)
+    t, a, _ = oracle.ternarize(w, G)
+    codes = oracle.pack_codes(t)
+    q, s = oracle.quantize_act(x, bits)
+    y = oracle.conv2d(q, bits, s, x.shape, codes, a, O, R, S, (st, st), (pd, pd), G)
+    M = y.shape[0]
+    rows = np.random.default_rng(7).integers(0, M, 40)
+    rows[:3] = [M - 1, 0, M - 1]
+    yr, mag = oracle.conv2d_rows(q, bits, s, x.shape, codes, a, O, R, S, (st, st), (pd, pd), G, rows)
+    np.testing.assert_array_equal(yr.view(np.uint32), y[rows].view(np.uint32))
+    P = oracle.group_sums_conv(q, bits, x.shape, codes, O, R, S, (st, st), (pd, pd), G).astype(np.float64)
+    ref = float(s) * np.einsum("mog,og->mo", np.abs(P[rows]), a.astype(np.float64))
+    np.testing.assert_allclose(mag, ref, rtol=1e-12, atol=0)
+    assert np.all(mag >= np.abs(yr.astype(np.float64)) * (1 - 1e-6))
+
+
 def test_one_hot_and_all_ones_activations():
     M, K, O, G = 4, 64, 3, 4
     w = fi.gauss_weights(O, K, 1.0, "onehot")
