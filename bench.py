@@ -42,9 +42,9 @@ _CSRC = "paper_1705_01462_amd/csrc/"
 # Sources of the convolution kernel that runs at each group size.
 KERNEL_SOURCES = {
     4: [_CSRC + f for f in ("fold.hip", "fold_kernel.h", "igemm.h", "epilogue.h", "qcode.h", "prepare.hip",
-                            "fgq_internal.h", "xexpand.h", "xlayout.h")],
+                            "fgq_internal.h", "xexpand.h", "xlayout.h", "bufcheck.h")],
     64: [_CSRC + f for f in ("group.hip", "group_kernel.h", "igemm.h", "epilogue.h", "qcode.h", "prepare.hip",
-                             "fgq_internal.h", "xexpand.h")],
+                             "fgq_internal.h", "xexpand.h", "bufcheck.h")],
 }
 
 

@@ -95,6 +95,27 @@ const char* fgq_status_string(fgq_status s);
 /* Interface version; bumped on any incompatible change of this header. */
 int32_t fgq_abi_version(void);
 
+/*
+ * fgq_check_violations -- the bounds checks of the checking build.
+ * libfgq_check.so is the same library compiled with -DFGQ_CHECK: every
+ * global-memory load of the kernels that goes through a buffer descriptor
+ * is tested for the one case the hardware's range check does not cover (a
+ * vector offset in range carried past the end by the scalar offset), and
+ * every output, split-sum and code store is tested against the extent of
+ * what it writes.  A failing access is suppressed (the load reads zeros,
+ * the store is skipped) and counted.  This call waits for the current
+ * device, then returns in *count the number of such accesses since the
+ * previous call (and in *first_site / *first_offset, when not NULL, the
+ * kind of access and the byte or element offset of the first: 1
+ * activations, 2 weight planes, 3 codes, 4 scale bytes, 5 group scales,
+ * 6 offset terms, 7 partial maxima, 8 layer outputs, 9 split-K sums, 10
+ * activation codes), and clears the counts.  For testing, not for
+ * production: the normal library (libfgq.so) returns FGQ_ERR_UNSUPPORTED.
+ * FGQ_ERR_NULL if count is NULL; FGQ_ERR_HIP on a runtime error.
+ */
+fgq_status fgq_check_violations(int64_t* count, int32_t* first_site,
+                                int64_t* first_offset);
+
 /* Number of visible HIP devices (0 when none or on runtime error). */
 int32_t fgq_device_count(void);
 

@@ -13,7 +13,9 @@ import os
 import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libfgq.so")
+# FGQ_LIBRARY=check selects the checking build, libfgq_check.so (bounds-
+# checked loads and stores, fgq_check_violations), in place of libfgq.so.
+LIB_PATH = os.path.join(_HERE, "libfgq_check.so" if os.environ.get("FGQ_LIBRARY") == "check" else "libfgq.so")
 
 FGQ_TERN_EXACT = 0
 FGQ_TERN_EXP_LEMMA = 1
@@ -41,6 +43,7 @@ _SZ = ctypes.c_size_t
 _SIGS = {
     "fgq_status_string": ([_I32], ctypes.c_char_p),
     "fgq_abi_version": ([], _I32),
+    "fgq_check_violations": ([_P, _P, _P], _I32),
     "fgq_device_count": ([], _I32),
     "fgq_codes_bytes": ([_I64, _I64], _SZ),
     "fgq_group_count": ([_I64, _I64, _I32], _I64),
@@ -82,8 +85,8 @@ def lib():
     global _lib
     if _lib is None:
         if not os.path.exists(LIB_PATH):
-            raise RuntimeError(f"libfgq.so not found at {LIB_PATH}; run __graft_entry__.build() "
-                               "(hipcc --offload-arch=gfx950) first")
+            raise RuntimeError(f"{os.path.basename(LIB_PATH)} not found at {LIB_PATH}; run "
+                               "__graft_entry__.build() (hipcc --offload-arch=gfx950) first")
         L = ctypes.CDLL(LIB_PATH)
         for name, (args, res) in _SIGS.items():
             f = getattr(L, name)
@@ -96,6 +99,15 @@ def lib():
 def _check(rc, where):
     if rc != 0:
         raise FgqError(rc, where)
+
+
+def fgq_check_violations():
+    """Checking build only: (count, first_site, first_offset) of the
+    suppressed out-of-bounds accesses since the previous call (cleared)."""
+    n, site, off = ctypes.c_int64(0), ctypes.c_int32(0), ctypes.c_int64(0)
+    _check(lib().fgq_check_violations(ctypes.byref(n), ctypes.byref(site), ctypes.byref(off)),
+           "fgq_check_violations")
+    return n.value, site.value, off.value
 
 
 def _stream():

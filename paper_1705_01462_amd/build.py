@@ -12,7 +12,9 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
 CSRC = os.path.join(HERE, "csrc")
 BUILD = os.path.join(HERE, "_build")
+BUILD_CHECK = os.path.join(HERE, "_build_check")
 LIB = os.path.join(HERE, "libfgq.so")
+LIB_CHECK = os.path.join(HERE, "libfgq_check.so")
 ARCH = "gfx950"
 
 FLAGS = [
@@ -44,9 +46,9 @@ def sources():
     return sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
 
 
-def _compile(src, verbose):
-    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = ["hipcc", *FLAGS, *extra_flags(src), "-c", src, "-o", obj]
+def _compile(src, verbose, check=False):
+    obj = os.path.join(BUILD_CHECK if check else BUILD, os.path.basename(src) + ".o")
+    cmd = ["hipcc", *FLAGS, *(["-DFGQ_CHECK"] if check else []), *extra_flags(src), "-c", src, "-o", obj]
     if verbose:
         print(" ".join(cmd), flush=True)
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -58,21 +60,25 @@ def _compile(src, verbose):
     return obj
 
 
-def build(verbose=False, jobs=None):
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose=False, jobs=None, check=False):
+    """Compile libfgq.so; with check=True the checking build
+    libfgq_check.so (-DFGQ_CHECK: bounds-checked loads and stores, see
+    csrc/bufcheck.h), from the same sources into its own object folder."""
+    os.makedirs(BUILD_CHECK if check else BUILD, exist_ok=True)
     # the kernel-heavy sources first, so the parallel compile ends together
     srcs = sorted(sources(), key=lambda s: not os.path.basename(s).startswith(("fold", "group")))
     jobs = jobs or min(len(srcs), 8)
     with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose), srcs))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, verbose, check), srcs))
+    out = LIB_CHECK if check else LIB
+    tmp = out + ".tmp"
     cmd = ["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, out)
+    return out
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, check="--check" in sys.argv))

@@ -4,11 +4,34 @@
 #include <stdlib.h>
 
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "fgq_internal.h"
 
 using namespace fgq;
+
+#ifdef FGQ_CHECK
+namespace fgq {
+namespace {
+std::mutex& check_mutex() {
+  static std::mutex m;
+  return m;
+}
+std::vector<const void*>& check_records() {
+  static std::vector<const void*> v;
+  return v;
+}
+}  // namespace
+
+// Called at load time by every compilation unit of a checking build (no
+// HIP call here: the records are looked up when they are read).
+void check_register(const void* symbol) {
+  std::lock_guard<std::mutex> g(check_mutex());
+  check_records().push_back(symbol);
+}
+}  // namespace fgq
+#endif
 
 namespace {
 
@@ -118,6 +141,41 @@ const char* fgq_status_string(fgq_status s) {
 }
 
 int32_t fgq_abi_version(void) { return 2; }
+
+fgq_status fgq_check_violations(int64_t* count, int32_t* first_site, int64_t* first_offset) {
+#ifndef FGQ_CHECK
+  (void)count, (void)first_site, (void)first_offset;
+  return FGQ_ERR_UNSUPPORTED;
+#else
+  if (!count) return FGQ_ERR_NULL;
+  if (hipDeviceSynchronize() != hipSuccess) return FGQ_ERR_HIP;
+  std::vector<const void*> syms;
+  {
+    std::lock_guard<std::mutex> g(check_mutex());
+    syms = check_records();
+  }
+  int64_t total = 0, offset = 0;
+  int32_t site = 0;
+  for (const void* sym : syms) {
+    void* p = nullptr;
+    if (hipGetSymbolAddress(&p, sym) != hipSuccess) return FGQ_ERR_HIP;
+    unsigned int rec[4];
+    if (hipMemcpy(rec, p, sizeof rec, hipMemcpyDeviceToHost) != hipSuccess) return FGQ_ERR_HIP;
+    if (rec[0] == 0) continue;
+    if (site == 0) {
+      site = static_cast<int32_t>(rec[1]);
+      offset = static_cast<int64_t>(rec[2]) | (static_cast<int64_t>(rec[3]) << 32);
+    }
+    total += rec[0];
+    if (hipMemset(p, 0, sizeof rec) != hipSuccess) return FGQ_ERR_HIP;
+  }
+  if (hipDeviceSynchronize() != hipSuccess) return FGQ_ERR_HIP;
+  *count = total;
+  if (first_site) *first_site = site;
+  if (first_offset) *first_offset = offset;
+  return FGQ_OK;
+#endif
+}
 
 int32_t fgq_device_count(void) {
   int n = 0;

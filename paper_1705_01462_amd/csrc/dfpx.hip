@@ -91,20 +91,17 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
   const bool ocok = oc < a.O;
   int bj[kPlanes] = {};
   if constexpr (kBits == 8) {
-    const __amdgpu_buffer_rsrc_t brs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<int32_t*>(a.bias), 0, 4 * kPlanes * a.O, kBufFlags);
+    const Buf brs = make_buf(a.bias, 4 * kPlanes * a.O, kSiteBias, kBufFlags);
 #pragma unroll
     for (int j = 0; j < kPlanes; ++j)
-      bj[j] = static_cast<int>(__builtin_amdgcn_raw_buffer_load_b32(
-          brs, ocok && ks0 == 0 && sh == 0 ? 4 * (j * a.O + oc) : kOutOfRange, 0, 0));
+      bj[j] = static_cast<int>(buf_load_b32(brs, ocok && ks0 == 0 && sh == 0 ? 4 * (j * a.O + oc) : kOutOfRange, 0));
   }
 
   // ---- activation slice: piece p = tid + 512*i is row p / (8*kSteps),
   // 16-k slot p % (8*kSteps) (a row's slots are consecutive threads, so a
   // wave reads one contiguous kilobyte of a row).  Rows >= M and steps past
   // the split read nothing.
-  const __amdgpu_buffer_rsrc_t qrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
+  const Buf qrs = make_buf(a.q, a.q_bytes, kSiteActs, kBufFlags);
   typedef typename std::conditional<kBits == 8, v4i, v2i>::type raw_t;
   raw_t xraw[kXP];
 #pragma unroll
@@ -115,19 +112,17 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
     const bool ok = (m < a.M) & (ksl < kSlots * nsteps) & (k < a.K);
     const uint32_t e = static_cast<uint32_t>(m) * static_cast<uint32_t>(a.K) + static_cast<uint32_t>(k);
     if constexpr (kBits == 8)
-      xraw[i] = __builtin_amdgcn_raw_buffer_load_b128(qrs, ok ? e : kOutOfRange, 0, 0);
+      xraw[i] = buf_load_b128(qrs, ok ? e : kOutOfRange, 0);
     else
-      xraw[i] = __builtin_amdgcn_raw_buffer_load_b64(qrs, ok ? e >> 1 : kOutOfRange, 0, 0);
+      xraw[i] = buf_load_b64(qrs, ok ? e >> 1 : kOutOfRange, 0);
   }
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- every weight load of the wave's steps (kHalf*sh + s), in the
   // prepared order.  Steps past the split re-read the split's last step (in
   // range; never used).
-  const __amdgpu_buffer_rsrc_t crs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.xcodes), 0, a.xcodes_bytes, kBufFlags);
-  const __amdgpu_buffer_rsrc_t ars =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.xacodes), 0, a.xacodes_bytes, kBufFlags);
+  const Buf crs = make_buf(a.xcodes, a.xcodes_bytes, kSiteCodes, kBufFlags);
+  const Buf ars = make_buf(a.xacodes, a.xacodes_bytes, kSiteScales, kBufFlags);
   const int lane0 = ((tile % a.n_otiles) * a.nk + ks0) * 256 + 64 * wo + lane;  // lane index of step ks0
   constexpr int kAB = ACodes<kG>::kBytes;
   v4i cw[kHalf];
@@ -136,7 +131,7 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
   for (int s = 0; s < kHalf; ++s) {
     const int st = kHalf * sh + s;
     const int ln = lane0 + 256 * (st < nsteps ? st : nsteps - 1);
-    cw[s] = __builtin_amdgcn_raw_buffer_load_b128(crs, 16 * ln, 0, 0);
+    cw[s] = buf_load_b128(crs, 16 * ln, 0);
 #pragma unroll
     for (int j = 0; j < kPlanes; ++j) aw[j][s].load(ars, j * a.xplane + kAB * ln);
   }
@@ -206,6 +201,9 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
 #pragma unroll
   for (int j = 0; j < kPlanes; ++j) {
     int32_t* const part = a.part + (static_cast<int64_t>(split) * kPlanes + j) * a.M * a.O;
+    // element range of this split's plane j (checking builds)
+    const int64_t pbase = (static_cast<int64_t>(split) * kPlanes + j) * a.M * a.O;
+    const int64_t plimit = static_cast<int64_t>(a.splits) * kPlanes * a.M * a.O;
     if (kSets == 1 && !a.staged) {
       if (ocok) {
 #pragma unroll
@@ -213,7 +211,8 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
-            if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = acc[j][c][r];
+            const int64_t e = static_cast<int64_t>(m) * a.O + oc;
+            if (m < a.M && check_store(kSiteStorePart, pbase + e, 1, plimit)) part[e] = acc[j][c][r];
           }
       }
       continue;
@@ -242,7 +241,8 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
 #pragma unroll
             for (int r = 0; r < 16; ++r) {
               const int m = m0 + 32 * c + 8 * (r / 4) + 4 * hf + (r % 4);
-              if (m < a.M) part[static_cast<int64_t>(m) * a.O + oc] = *at(c, r);
+              const int64_t e = static_cast<int64_t>(m) * a.O + oc;
+              if (m < a.M && check_store(kSiteStorePart, pbase + e, 1, plimit)) part[e] = *at(c, r);
             }
         }
         continue;
@@ -255,9 +255,9 @@ __global__ __launch_bounds__((wg_threads<kNB, kPlanes>()), 2) void dfpx_gemm_ker
     for (int t = tid; t < kRows * 32; t += kWG) {
       const int row = t / 32, ch = o0 + 4 * (t % 32);
       const int m = m0 + row;
-      if (m < a.M && ch < a.O)
-        *reinterpret_cast<v4i*>(part + static_cast<int64_t>(m) * a.O + ch) =
-            *reinterpret_cast<const v4i*>(lds + row * kPitch + 16 * (t % 32));
+      const int64_t e = static_cast<int64_t>(m) * a.O + ch;
+      if (m < a.M && ch < a.O && check_store(kSiteStorePart, pbase + e, 4, plimit))
+        *reinterpret_cast<v4i*>(part + e) = *reinterpret_cast<const v4i*>(lds + row * kPitch + 16 * (t % 32));
     }
   }
 }

@@ -74,14 +74,17 @@ __device__ inline void store_direct(const OutPtrs& out, const QScale& qs, int m_
       const int m = m_wave + 32 * c + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
       if (m >= out.M) continue;
       const int64_t e = static_cast<int64_t>(m) * out.O + o;
+      const int64_t n = static_cast<int64_t>(out.M) * out.O;
       const float v = val(c, r);
       if constexpr (kOut == 0) {
-        __builtin_nontemporal_store(v, out.y + e);
+        if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(v, out.y + e);
       } else if constexpr (kOut == 8) {
-        __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), out.q + e);
+        if (check_store(kSiteStoreY, e, 1, n))
+          __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), out.q + e);
       } else {
         const unsigned b = pair_nibbles(qcode<kRcp>(v, qs));
-        if ((o & 1) == 0) __builtin_nontemporal_store(static_cast<uint8_t>(b), out.q + (e >> 1));
+        if ((o & 1) == 0 && check_store(kSiteStoreY, e >> 1, 1, (n + 1) / 2))
+          __builtin_nontemporal_store(static_cast<uint8_t>(b), out.q + (e >> 1));
       }
     }
   }
@@ -131,7 +134,9 @@ __device__ inline void store_staged(unsigned char* lds, const OutPtrs& out, cons
       if (m < out.M && ch < out.O) {
         const u32x4 w = *reinterpret_cast<const u32x4*>(lds + lr * T::kPitch + 16 * cb);
         const int64_t byte = (static_cast<int64_t>(m) * out.O + ch) * (kOut == 0 ? 4 : 1) / (kOut == 4 ? 2 : 1);
-        __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(base + byte));
+        const int64_t nbytes = static_cast<int64_t>(out.M) * out.O * (kOut == 0 ? 4 : 1) / (kOut == 4 ? 2 : 1);
+        if (check_store(kSiteStoreY, byte, 16, nbytes))
+          __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(base + byte));
       }
     }
   }

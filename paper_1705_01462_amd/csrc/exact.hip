@@ -212,7 +212,7 @@ __global__ __launch_bounds__(256) void exact_conv_kernel(
       for (int j = 0; j < 4; ++j) {
         const int64_t o = o0 + tx + 16 * j;  // lanes tx and tx^1 hold channels o and o^1
         if (o < g.O)
-          emit_out<kOut, decltype(rcp)::value>(out.y, out.q, qs, m * g.O + o, static_cast<int>(o),
+          emit_out<kOut, decltype(rcp)::value>(out.y, out.q, qs, m * g.O + o, g.M * g.O, static_cast<int>(o),
                                                static_cast<float>(sx * acc[i][j]));
       }
     }

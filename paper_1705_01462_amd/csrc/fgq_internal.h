@@ -6,6 +6,7 @@
 #include <stddef.h>
 #include <stdint.h>
 
+#include "bufcheck.h"
 #include "fgq.h"
 
 #define FGQ_TRY_HIP(expr)                      \

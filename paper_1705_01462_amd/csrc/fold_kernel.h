@@ -133,8 +133,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   const int o0 = (tile % a.x.n_otiles) * kTO + 32 * wo;  // this wave's first channel
   const int m0 = (tile / a.x.n_otiles) * kTM;             // workgroup's first row
 
-  const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.planes), 0, a.planes_bytes, kBufFlags);
+  const Buf wrs = make_buf(a.planes, a.planes_bytes, kSitePlanes, kBufFlags);
 
   // ---- weight fragments: lane supplies channel o0 + lane%32, k-slot
   // 16*(lane/32) of K half h; the fragment-ordered planes put the wave's
@@ -161,10 +160,8 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   using DW = ACodes<kX ? kG : 4>;
   constexpr int kAB = DW::kBytes;
   const int xl = ((o0 / 128) * a.nk128 * 4 + (o0 % 128) / 32) * 64 + lane;  // lane index at step 0
-  const __amdgpu_buffer_rsrc_t crs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.xcodes), 0, a.xcodes_bytes, kBufFlags);
-  const __amdgpu_buffer_rsrc_t drs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.xdigits), 0, a.xdigits_bytes, kBufFlags);
+  const Buf crs = make_buf(a.xcodes, a.xcodes_bytes, kSiteCodes, kBufFlags);
+  const Buf drs = make_buf(a.xdigits, a.xdigits_bytes, kSiteScales, kBufFlags);
 
   v4i wring[2][kX ? 1 : kPlanes][4];
   v4i cring[2];
@@ -173,7 +170,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
     constexpr int u = decltype(U)::value;
     ks = ks < nk ? ks : nk - 1;
     if constexpr (kX) {
-      cring[u] = __builtin_amdgcn_raw_buffer_load_b128(crs, 16 * xl, 4096 * ks, 0);
+      cring[u] = buf_load_b128(crs, 16 * xl, 4096 * ks);
 #pragma unroll
       for (int j = 0; j < kPlanes; ++j) dring[u][j].load(drs, j * a.xplane + kAB * xl, 256 * kAB * ks);
     } else {
@@ -185,7 +182,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 #pragma unroll
           for (int h = 0; h < 2; ++h)
             wring[u][j][2 * blk + h] =
-                __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, kso, 0);
+                buf_load_b128(wrs, wbase + (2 * j + h) * 1024, kso);
       }
     }
   };
@@ -373,7 +370,9 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
 #pragma unroll
         for (int r = 0; r < 16; ++r) {
           const int m = m0 + wm * kNB * 32 + 32 * c + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
-          if (m < M) part[(static_cast<int64_t>(split * kPlanes + j) * M + m) * O + o] = acc[j][c][r];
+          const int64_t e = (static_cast<int64_t>(split * kPlanes + j) * M + m) * O + o;
+          if (m < M && check_store(kSiteStorePart, e, 1, static_cast<int64_t>(a.splits) * kPlanes * M * O))
+            part[e] = acc[j][c][r];
         }
   } else {
     const float sx = *a.sx;

@@ -51,8 +51,7 @@ __global__ __launch_bounds__(kThreads, 2) void fold_rows_kernel(FoldArgs a) {
 
   // the step's weight fragments, as fold_conv_kernel loads them for step 0
   constexpr int kTileB = kPlanes * 2 * 1024;
-  const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<int8_t*>(a.planes), 0, a.planes_bytes, kBufFlags);
+  const Buf wrs = make_buf(a.planes, a.planes_bytes, kSitePlanes, kBufFlags);
   const int wbase = (o0 / 32) * a.nks * kTileB + 16 * lane;
   v4i w[kPlanes][4];
 #pragma unroll
@@ -61,7 +60,7 @@ __global__ __launch_bounds__(kThreads, 2) void fold_rows_kernel(FoldArgs a) {
     for (int j = 0; j < kPlanes; ++j)
 #pragma unroll
       for (int h = 0; h < 2; ++h)
-        w[j][2 * blk + h] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase + (2 * j + h) * 1024, blk * kTileB, 0);
+        w[j][2 * blk + h] = buf_load_b128(wrs, wbase + (2 * j + h) * 1024, blk * kTileB);
 
   int32_t bias[kPlanes];
 #pragma unroll

@@ -78,13 +78,15 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
   const int o0 = (tile % a.x.n_otiles) * kTO + 32 * wo;  // this wave's first channel
   const int m0 = (tile / a.x.n_otiles) * kTM;             // workgroup's first row
 
-  const __amdgpu_buffer_rsrc_t wrs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<uint32_t*>(a.codes), 0, a.codes_bytes, kBufFlags);
-  const __amdgpu_buffer_rsrc_t ars =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(a.alpha), 0, a.alpha_bytes, kBufFlags);
+  const Buf wrs = make_buf(a.codes, a.codes_bytes, kSiteCodes, kBufFlags);
+  const Buf ars = make_buf(a.alpha, a.alpha_bytes, kSiteAlpha, kBufFlags);
   const int nk = (a.x.K + kKT - 1) / kKT;
   const int wbase = (o0 / 32) * nk * kStepBytes + 16 * lane;
-  const int abase = 4 * (o0 + lane % 32);
+  // The group's alphas are the scalar offset, which the buffer range check
+  // does not cover: lanes of a channel tile past the padded channel count
+  // (O32) take an out-of-range vector offset, which reads zeros, instead of
+  // addressing past the end of the buffer.
+  const int abase = o0 + lane % 32 < a.O32 ? 4 * (o0 + lane % 32) : static_cast<int>(kOutOfRange);
 
   Stager xs;
   xs.init(a.x, m0, tid);
@@ -97,11 +99,11 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
   auto load_w = [&](auto U, int ks) {
     constexpr int u = decltype(U)::value;
     ks = ks < nk ? ks : nk - 1;
-    cring[u] = __builtin_amdgcn_raw_buffer_load_b128(wrs, wbase, ks * kStepBytes, 0);
+    cring[u] = buf_load_b128(wrs, wbase, ks * kStepBytes);
 #pragma unroll
     for (int blk = 0; blk < 2; ++blk)
       aring[u][blk] = __builtin_bit_cast(
-          float, __builtin_amdgcn_raw_buffer_load_b32(ars, abase, (2 * ks + blk) * a.O32 * 4, 0));
+          float, buf_load_b32(ars, abase, (2 * ks + blk) * a.O32 * 4));
   };
 
   v16f acc[kNB];

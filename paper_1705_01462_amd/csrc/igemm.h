@@ -86,13 +86,13 @@ struct ActStager {
   bool rowok[kXP];
   int tr, ts, tc, tk;
   raw_t xraw[kXP];
-  __amdgpu_buffer_rsrc_t rs;
+  Buf rs;
 
   // Piece p = tid + 256*i is row p/kSlots of the tile, k-slot
   // 16*(p%kSlots) = 16*(tid%kSlots) of every step; the tap state starts at
   // step ks0.
   __device__ void init(const ActArgs& a, int m0, int tid, int ks0 = 0) {
-    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
+    rs = make_buf(a.q, a.q_bytes, kSiteActs, kBufFlags);
 #pragma unroll
     for (int i = 0; i < kXP; ++i) {
       const int p = tid + kThreads * i;
@@ -143,10 +143,10 @@ struct ActStager {
       const int e = (rowbase[i] + tr * a.W + ts) * a.C + tc;  // element offset
       if constexpr (kBits == 8) {
         const uint32_t off = ok ? static_cast<uint32_t>(e) : kOutOfRange;
-        xraw[i] = __builtin_amdgcn_raw_buffer_load_b128(rs, off, 0, 0);
+        xraw[i] = buf_load_b128(rs, off, 0);
       } else {
         const uint32_t off = ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange;
-        xraw[i] = __builtin_amdgcn_raw_buffer_load_b64(rs, off, 0, 0);
+        xraw[i] = buf_load_b64(rs, off, 0);
       }
     }
   }
@@ -188,10 +188,10 @@ struct ActStagerTinyC {
   bool rowok[kXP];
   int tk;
   uint32_t part[kXP][kSub][kC * kBits / 32 > 0 ? kC * kBits / 32 : 1];
-  __amdgpu_buffer_rsrc_t rs;
+  Buf rs;
 
   __device__ void init(const ActArgs& a, int m0, int tid, int ks0 = 0) {
-    rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint8_t*>(a.q), 0, a.q_bytes, kBufFlags);
+    rs = make_buf(a.q, a.q_bytes, kSiteActs, kBufFlags);
 #pragma unroll
     for (int i = 0; i < kXP; ++i) {
       const int p = tid + kThreads * i;
@@ -226,15 +226,15 @@ struct ActStagerTinyC {
                         (static_cast<unsigned>(wi) < static_cast<unsigned>(a.W));
         const int e = (rowbase[i] + r * a.W + t) * kC;  // element offset of the tap
         if constexpr (kBits == 8 && kC == 4) {
-          part[i][j][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, ok ? static_cast<uint32_t>(e) : kOutOfRange, 0, 0);
+          part[i][j][0] = buf_load_b32(rs, ok ? static_cast<uint32_t>(e) : kOutOfRange, 0);
         } else if constexpr (kBits == 8) {
-          const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, ok ? static_cast<uint32_t>(e) : kOutOfRange, 0, 0);
+          const v2i v = buf_load_b64(rs, ok ? static_cast<uint32_t>(e) : kOutOfRange, 0);
           part[i][j][0] = static_cast<uint32_t>(v.x);
           part[i][j][1] = static_cast<uint32_t>(v.y);
         } else if constexpr (kC == 4) {
-          part[i][j][0] = __builtin_amdgcn_raw_buffer_load_b16(rs, ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange, 0, 0);
+          part[i][j][0] = buf_load_b16(rs, ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange, 0);
         } else {
-          part[i][j][0] = __builtin_amdgcn_raw_buffer_load_b32(rs, ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange, 0, 0);
+          part[i][j][0] = buf_load_b32(rs, ok ? static_cast<uint32_t>(e) >> 1 : kOutOfRange, 0);
         }
       }
     }

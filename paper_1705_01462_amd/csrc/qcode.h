@@ -66,23 +66,24 @@ __device__ inline void with_rcp(const QScale& c, F&& f) {
     f(std::false_type{});
 }
 
-// One output value of a layer, at element index e = m*O + o, by output
-// kind: kOut = 0 stores fp32 to y; kOut = 8 stores its code as one byte;
+// One output value of a layer, at element index e = m*O + o of n = M*O, by
+// output kind: kOut = 0 stores fp32 to y; kOut = 8 stores its code as one byte;
 // kOut = 4 packs two codes per byte (the lanes holding channels o and o^1
 // must call together; the even one writes).  All stores are non-temporal:
 // the output is written once, and streaming it out leaves no dirty lines in
 // the per-XCD L2 caches for the end of the kernel to write back.
 template <int kOut, bool kRcp = true>
-__device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t e, int o, float v) {
+__device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t e, int64_t n, int o, float v) {
   if constexpr (kOut == 0) {
-    __builtin_nontemporal_store(v, y + e);
+    if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(v, y + e);
   } else if constexpr (kOut == 8) {
-    __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), q + e);
+    if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), q + e);
   } else {
     static_assert(kOut == 4, "output kind");
     const unsigned c = qcode<kRcp>(v, qs);
     const unsigned other = static_cast<unsigned>(__builtin_amdgcn_mov_dpp(static_cast<int>(c), 0xB1, 0xF, 0xF, false));
-    if ((o & 1) == 0) __builtin_nontemporal_store(static_cast<uint8_t>(c | (other << 4)), q + (e >> 1));
+    if ((o & 1) == 0 && check_store(kSiteStoreY, e >> 1, 1, (n + 1) / 2))
+      __builtin_nontemporal_store(static_cast<uint8_t>(c | (other << 4)), q + (e >> 1));
   }
 }
 

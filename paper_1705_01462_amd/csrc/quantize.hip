@@ -51,12 +51,11 @@ __device__ inline float block_max(float v, float* red) {
 // (reads past npart return 0, neutral for maxima of non-negative values),
 // so the reduction costs one round trip, then one block reduction.
 __device__ inline float partials_max(const float* partials, int32_t npart, float* red) {
-  const __amdgpu_buffer_rsrc_t rs =
-      __builtin_amdgcn_make_buffer_rsrc(const_cast<float*>(partials), 0, 4 * npart, 0x00020000);
+  const Buf rs = make_buf(partials, 4 * npart, kSitePartials, 0x00020000);
   float p[kMaxPartials / kThreads];
 #pragma unroll
   for (int u = 0; u < kMaxPartials / kThreads; ++u)
-    p[u] = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, 4 * (threadIdx.x + kThreads * u), 0, 0));
+    p[u] = __uint_as_float(buf_load_b32(rs, 4 * (threadIdx.x + kThreads * u), 0));
   float m = 0.0f;
 #pragma unroll
   for (int u = 0; u < kMaxPartials / kThreads; ++u) m = fmaxf(m, p[u]);
@@ -158,7 +157,9 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
         out[wd] = word;
       }
       uint8_t* dst = q + ch * kBytes;
-      if (kAligned) {
+      const int64_t nq = kBits == 8 ? n : n / 2;  // code bytes
+      if (!check_store(kSiteStoreQ, ch * kBytes, kBytes, nq)) {
+      } else if (kAligned) {
 #pragma unroll
         for (int i = 0; i < kBytes / 16; ++i) {
           typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
@@ -175,10 +176,11 @@ __global__ __launch_bounds__(kThreads) void quantize_kernel(
     const int64_t tail_bytes = kBits == 8 ? (n - done) : (n - done) / 2;
     if (ch < tail_bytes) {
       if (kBits == 8) {
-        q[done + ch] = static_cast<uint8_t>(code(x[done + ch]));
+        if (check_store(kSiteStoreQ, done + ch, 1, n)) q[done + ch] = static_cast<uint8_t>(code(x[done + ch]));
       } else {
         const int64_t e = done + 2 * ch;
-        q[e / 2] = static_cast<uint8_t>(code(x[e]) | (code(x[e + 1]) << 4));
+        if (check_store(kSiteStoreQ, e / 2, 1, n / 2))
+          q[e / 2] = static_cast<uint8_t>(code(x[e]) | (code(x[e + 1]) << 4));
       }
     }
   });
@@ -222,19 +224,20 @@ __global__ __launch_bounds__(kThreads) void quantize_coalesced_kernel(
       if (f < n4) {
         if constexpr (kBits == 8) {
           const uint32_t word = code(v[i].x) | (code(v[i].y) << 8) | (code(v[i].z) << 16) | (code(v[i].w) << 24);
-          __builtin_nontemporal_store(word, reinterpret_cast<uint32_t*>(q) + f);
+          if (check_store(kSiteStoreQ, 4 * f, 4, n)) __builtin_nontemporal_store(word, reinterpret_cast<uint32_t*>(q) + f);
         } else {
           const uint32_t half = code(v[i].x) | (code(v[i].y) << 4) | (code(v[i].z) << 8) | (code(v[i].w) << 12);
-          __builtin_nontemporal_store(static_cast<uint16_t>(half), reinterpret_cast<uint16_t*>(q) + f);
+          if (check_store(kSiteStoreQ, 2 * f, 2, n / 2))
+            __builtin_nontemporal_store(static_cast<uint16_t>(half), reinterpret_cast<uint16_t*>(q) + f);
         }
       }
     }
     // the tail (n % 4 values; n is even for uint4), by the first block
     const int64_t done = n4 * 4;
     if (blockIdx.x == 0) {
-      if (kBits == 8 && threadIdx.x < n - done)
+      if (kBits == 8 && threadIdx.x < n - done && check_store(kSiteStoreQ, done + threadIdx.x, 1, n))
         q[done + threadIdx.x] = static_cast<uint8_t>(code(x[done + threadIdx.x]));
-      if (kBits == 4 && threadIdx.x == 0 && n - done == 2)
+      if (kBits == 4 && threadIdx.x == 0 && n - done == 2 && check_store(kSiteStoreQ, done / 2, 1, n / 2))
         q[done / 2] = static_cast<uint8_t>(code(x[done]) | (code(x[done + 1]) << 4));
     }
   });

@@ -71,7 +71,7 @@ __global__ __launch_bounds__(256) void splitk_reduce_kernel(const int32_t* __res
         v = fmaf(static_cast<float>(S[2 % kPlanes]), c2,
                  fmaf(static_cast<float>(S[1 % kPlanes]), c1, static_cast<float>(S[0]) * c0));
       }
-      emit_out<kOut, decltype(rcp)::value>(y, qo, qs, e, o, v);
+      emit_out<kOut, decltype(rcp)::value>(y, qo, qs, e, n, o, v);
     }
   });
 }
@@ -119,6 +119,7 @@ __global__ __launch_bounds__(256) void splitk_reduce4_kernel(const int32_t* __re
                       fmaf(static_cast<float>(S[1 % kPlanes][i]), c1, static_cast<float>(S[0][i]) * c0));
         }
       }
+      if (!check_store(kSiteStoreY, e, 4, n)) continue;
       if constexpr (kOut == 0) {
         __builtin_nontemporal_store(v4f{v[0], v[1], v[2], v[3]}, reinterpret_cast<v4f*>(y + e));
       } else {

@@ -56,20 +56,20 @@ struct ACodes {
 
   // off: per-lane byte offset; soff: a wave-uniform byte offset (not
   // covered by the buffer's range check).
-  __device__ void load(__amdgpu_buffer_rsrc_t rs, int off, int soff = 0) {
+  __device__ void load(const Buf& rs, int off, int soff = 0) {
     if constexpr (kBytes == 16) {
-      const v4i v = __builtin_amdgcn_raw_buffer_load_b128(rs, off, soff, 0);
+      const v4i v = buf_load_b128(rs, off, soff);
       for (int i = 0; i < 4; ++i) w[i] = static_cast<uint32_t>(v[i]);
     } else if constexpr (kBytes == 8) {
-      const v2i v = __builtin_amdgcn_raw_buffer_load_b64(rs, off, soff, 0);
+      const v2i v = buf_load_b64(rs, off, soff);
       w[0] = static_cast<uint32_t>(v.x);
       w[1] = static_cast<uint32_t>(v.y);
     } else if constexpr (kBytes == 4) {
-      w[0] = __builtin_amdgcn_raw_buffer_load_b32(rs, off, soff, 0);
+      w[0] = buf_load_b32(rs, off, soff);
     } else if constexpr (kBytes == 2) {
-      w[0] = __builtin_amdgcn_raw_buffer_load_b16(rs, off, soff, 0);
+      w[0] = buf_load_b16(rs, off, soff);
     } else {
-      w[0] = __builtin_amdgcn_raw_buffer_load_b8(rs, off, soff, 0);
+      w[0] = buf_load_b8(rs, off, soff);
     }
   }
   // The A bytes of quarter h (16 weights), placed where expand16<kG> reads

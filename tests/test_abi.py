@@ -33,6 +33,23 @@ def test_library_exports_every_declared_symbol():
         assert callable(getattr(fgq, n))
 
 
+def test_checking_build_exports_every_declared_symbol():
+    """libfgq_check.so (the -DFGQ_CHECK build) has the same ABI; the normal
+    library answers fgq_check_violations with FGQ_ERR_UNSUPPORTED."""
+    path = os.path.join(os.path.dirname(fgq.LIB_PATH), "libfgq_check.so")
+    if not os.path.exists(path):
+        pytest.skip("checking build not built")
+    L = ctypes.CDLL(path)
+    for n in declared_functions():
+        assert hasattr(L, n), n
+    N = ctypes.CDLL(os.path.join(os.path.dirname(fgq.LIB_PATH), "libfgq.so"))
+    N.fgq_check_violations.argtypes = [ctypes.c_void_p] * 3
+    n = ctypes.c_int64(-1)
+    assert N.fgq_check_violations(ctypes.byref(n), None, None) == 7
+    L.fgq_check_violations.argtypes = [ctypes.c_void_p] * 3
+    assert L.fgq_check_violations(None, None, None) == 1  # FGQ_ERR_NULL before any device call
+
+
 def test_host_helpers():
     L = fgq.lib()
     assert L.fgq_abi_version() == 2
