@@ -552,6 +552,177 @@ def stack_measure(torch, fgq, fi, depth, G, bits, batch=64, nsets=3, reps=50):
             "direct_kernel_layers": direct_layers}
 
 
+class ResNetChain:
+    """A whole ResNet-`depth` forward pass on the library (torchvision v1.5
+    bottlenecks, hw x hw input, batch `batch`).  Every convolution and the
+    fully-connected layer is an FGQ layer on prepared weights (fgq_conv2d;
+    the fully-connected layer through fgq_gemm_ws), and every layer's input
+    is quantized by fgq_quantize_act with its own dynamic per-tensor scale.
+    The glue between layers is plain torch on fp32 NHWC tensors: the
+    stem's 3x3 max pooling, the residual additions with their ReLU and the
+    global average pooling.  The ReLU after the stem and after the first two
+    convolutions of a block is the quantizer's own clamp at zero (the codes
+    and the scale of y and of ReLU(y) are the same), so those layers'
+    outputs are quantized as they are.  The network input is pixel-like uint8 codes (128 + 32 z,
+    clamped, scale 1/255; a zero fourth channel), the weights He-initialised
+    and ternarized per layer (conv1 in groups of 4).  Every buffer is
+    allocated up front, so forward() can be captured in a HIP graph; after
+    it, each layer's input codes (`q`, `sx`) and fp32 output (`y`) stay in
+    `self.layers`, and the stem and block outputs in `self.stem` and
+    `self.blocks`, for checks."""
+
+    def __init__(self, torch, fgq, fi, depth, G, bits, batch, hw=224, tag="chain"):
+        self.torch, self.fgq, self.bits = torch, fgq, bits
+        self.convs = fi.resnet_convs(depth, batch, hw)
+        self.layers = {}
+        self.ops = 0.0
+        for L in self.convs:
+            B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+            g = G if C % G == 0 else 4
+            w = fi.he_weights(O, C, R, S, tag, depth, L["name"])
+            if L["name"] == "conv1":
+                w[:, 3:] = 0.0
+            codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), g)
+            K = R * S * C
+            Ho, Wo = fi.conv_out(H, W, R, S, L["stride"], L["pad"])
+            n = B * H * W * C
+            e = dict(L=L, g=g, K=K, codes=codes, alpha=alpha,
+                     prep=fgq.fgq_prepare_weights(codes, alpha, O, K, g, fallback=True),
+                     q=torch.empty(n * bits // 8, dtype=torch.uint8, device="cuda"),
+                     sx=torch.empty(1, dtype=torch.float32, device="cuda"),
+                     ws=torch.empty(max(fgq.fgq_quantize_ws_bytes(n), 4), dtype=torch.uint8, device="cuda"),
+                     y=torch.empty((B, Ho, Wo, O), dtype=torch.float32, device="cuda"))
+            if L["name"] == "fc":
+                e["wsfc"] = torch.empty(max(fgq.fgq_gemm_ws_bytes(B, K, O, g, False), 4), dtype=torch.uint8,
+                                        device="cuda")
+            self.layers[L["name"]] = e
+            self.ops += 2.0 * B * Ho * Wo * O * R * S * (3 if L["name"] == "conv1" else C)
+        # the network input: pixel-like codes with a zero fourth channel
+        L0 = self.convs[0]
+        z = fi.rng("chain-input", depth, batch, hw).standard_normal((L0["B"], L0["H"], L0["W"], 4))
+        x0 = np.clip(np.rint(128.0 + 32.0 * z), 0, 255).astype(np.uint8)
+        x0[..., 3] = 0
+        if bits == 4:
+            x0 = x0 >> 4
+            x0 = (x0[..., 0::2] | (x0[..., 1::2] << 4)).astype(np.uint8)
+        c1 = self.layers["conv1"]
+        c1["q"].copy_(torch.from_numpy(x0.reshape(-1)))
+        c1["sx"].fill_(1.0 / (255.0 if bits == 8 else 15.0))
+        # block outputs (and the stem's pooled output)
+        y1 = c1["y"]
+        Hp = (y1.shape[1] + 2 - 3) // 2 + 1
+        self.stem = torch.empty((y1.shape[0], Hp, Hp, y1.shape[3]), dtype=torch.float32, device="cuda")
+        self.blocks = {}
+        for L in self.convs:
+            if L["name"].endswith(".c3"):
+                p = L["name"][:-3]
+                self.blocks[p] = torch.empty_like(self.layers[L["name"]]["y"])
+        last = self.blocks[list(self.blocks)[-1]]
+        self.pooled = torch.empty((last.shape[0], last.shape[3]), dtype=torch.float32, device="cuda")
+
+    def calibrate(self):
+        """Static input scales for the fused form: each layer's scale from one
+        forward pass with dynamic scales (the paper's per-layer scales)."""
+        self.forward()
+        for e in self.layers.values():
+            e["sx_static"] = e["sx"].clone()
+
+    def _quant(self, src, e):
+        self.fgq.fgq_quantize_act(src, self.bits, q=e["q"], scale_out=e["sx"], ws=e["ws"])
+
+    def _conv_q(self, e, nxt):
+        """Layer e with the next layer's quantization fused (its codes written
+        straight into nxt's input, at nxt's static scale)."""
+        L = e["L"]
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        self.fgq.fgq_conv2d_q(e["q"], self.bits, e["sx"], (B, H, W, C), e["codes"], e["alpha"], O, R, S,
+                              L["stride"], L["pad"], e["g"], self.bits, nxt["sx_static"], prepared=e["prep"],
+                              q_out=nxt["q"])
+        nxt["sx"].copy_(nxt["sx_static"])
+
+    def _conv(self, e):
+        L = e["L"]
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        if L["name"] == "fc":
+            self.fgq.fgq_gemm_ws(e["q"], self.bits, e["sx"], B, e["K"], e["codes"], e["alpha"], O, e["g"],
+                                 prepared=e["prep"], out=e["y"].view(B, O), ws=e["wsfc"])
+        else:
+            self.fgq.fgq_conv2d(e["q"], self.bits, e["sx"], (B, H, W, C), e["codes"], e["alpha"], O, R, S,
+                                L["stride"], L["pad"], e["g"], prepared=e["prep"], y=e["y"])
+
+    def forward(self, fused=False):
+        """fused=False: every layer's input quantized with a dynamic scale.
+        fused=True (after calibrate()): the first two convolutions of each
+        block write the next layer's codes at its static scale
+        (fgq_conv2d_q), so only the block inputs and the head are quantized
+        separately."""
+        torch, F = self.torch, self.torch.nn.functional
+        c1 = self.layers["conv1"]
+        self._conv(c1)
+        pooled = F.max_pool2d(c1["y"].permute(0, 3, 1, 2), 3, 2, 1)
+        self.stem.copy_(pooled.permute(0, 2, 3, 1))
+        h = self.stem
+        for p, out in self.blocks.items():
+            a, b, c = (self.layers[f"{p}.c{i}"] for i in (1, 2, 3))
+            ds = self.layers.get(f"{p}.ds")
+            self._quant(h, a)
+            if ds is not None:
+                ds["q"], ds["sx"] = a["q"], a["sx"]  # the block input's codes (the stride is the conv's)
+                self._conv(ds)
+            if fused:
+                self._conv_q(a, b)
+                self._conv_q(b, c)
+            else:
+                self._conv(a)
+                self._quant(a["y"], b)
+                self._conv(b)
+                self._quant(b["y"], c)
+            self._conv(c)
+            torch.add(c["y"], ds["y"] if ds is not None else h, out=out)
+            out.relu_()
+            h = out
+        torch.mean(h, dim=(1, 2), out=self.pooled)
+        fc = self.layers["fc"]
+        self._quant(self.pooled, fc)
+        self._conv(fc)
+        return fc["y"]
+
+
+def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10):
+    """End-to-end time of ResNetChain's forward pass, captured in one HIP
+    graph: every layer's quantization, every FGQ layer and the torch glue."""
+    net = ResNetChain(torch, fgq, fi, depth, G, bits, batch)
+    net.calibrate()
+    res = {}
+    for fused in (False, True):
+        net.forward(fused)
+        torch.cuda.synchronize()
+        ref = net.forward(fused).clone()
+        torch.cuda.synchronize()
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            net.forward(fused)
+        g.replay()
+        torch.cuda.synchronize()
+        if not torch.equal(net.layers["fc"]["y"], ref):
+            raise RuntimeError("graph replay of the network differs from eager execution")
+        _, ms = time_graphs(torch, [(g, reps)])
+        res[fused] = (ms * 1e3 / reps, bool(torch.isfinite(ref).all().item()))
+        del g
+    us, fus = res[False][0], res[True][0]
+    out = {"workload": f"ResNet-{depth} forward pass, batch {batch}, 224x224, G={G}, u{bits}: every layer's "
+                       "quantization, FGQ layer and the torch glue (max pooling, residual additions and their ReLU, "
+                       "average pooling) in one graph; fused: the first two convolutions of each block write the "
+                       "next layer's codes at calibrated static scales",
+           "end_to_end_us": round(us, 1), "effective_tops_end_to_end": round(net.ops / (us * 1e-6) / 1e12, 1),
+           "end_to_end_fused_us": round(fus, 1),
+           "effective_tops_end_to_end_fused": round(net.ops / (fus * 1e-6) / 1e12, 1),
+           "logits_finite": res[False][1] and res[True][1]}
+    del net
+    torch.cuda.empty_cache()
+    return out
+
+
 def alexnet_measure(torch, fgq, fi, batch=64, G=4, bits=8, nsets=3, reps=50):
     """The AlexNet-shaped layers at batch `batch`, G=4, uint8: each layer timed
     at its full shape (graph replays over rotating sets) two ways: ternary
@@ -907,6 +1078,10 @@ def main():
             if not args.no_cpu:
                 out["stacks"][f"resnet{depth}_b64_g{G}_u{sbits}"]["cpu_oracle"] = stack_cpu_estimate(fi, depth, G, sbits)
             log(f"[bench] ResNet-{depth}: sum conv {out['stacks'][f'resnet{depth}_b64_g{G}_u{sbits}']['sum_conv_us']} us")
+            out["stacks"][f"resnet{depth}_b64_g{G}_u{sbits}"]["end_to_end"] = chain_measure(torch, fgq, fi, depth,
+                                                                                            G, sbits)
+            log(f"[bench] ResNet-{depth} forward pass: "
+                f"{out['stacks'][f'resnet{depth}_b64_g{G}_u{sbits}']['end_to_end']['end_to_end_us']} us")
     if not args.no_stacks:
         log("[bench] AlexNet-shaped layers, batch 64, G=4, u8")
         out["alexnet_b64_g4_u8"] = alexnet_measure(torch, fgq, fi)

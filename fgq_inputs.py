@@ -61,16 +61,18 @@ CONV1X1_C256 = dict(name="conv 1x1 256->64", B=32, H=56, W=56, C=256, O=64,
                     R=1, S=1, stride=1, pad=0)
 
 
-def resnet_convs(depth, batch):
-    """torchvision v1.5 bottleneck ResNet conv shapes (stride on the 3x3).
+def resnet_convs(depth, batch, hw=224):
+    """torchvision v1.5 bottleneck ResNet conv shapes (stride on the 3x3) for
+    hw x hw input images (224 is the standard size).
 
     conv1 has its 3 input channels zero-padded to 4 so that a group of 4
-    input channels exists.  Returns a list of dicts, then the FC as a 1x1
-    conv on a 1x1 map.
+    input channels exists; the stem's 3x3 max pooling (stride 2, pad 1)
+    follows it.  Returns a list of dicts, then the FC as a 1x1 conv on a
+    1x1 map.
     """
     blocks = {50: [3, 4, 6, 3], 101: [3, 4, 23, 3]}[depth]
-    layers = [dict(name="conv1", B=batch, H=224, W=224, C=4, O=64, R=7, S=7, stride=2, pad=3)]
-    H = 56
+    layers = [dict(name="conv1", B=batch, H=hw, W=hw, C=4, O=64, R=7, S=7, stride=2, pad=3)]
+    H = ((hw + 6 - 7) // 2 + 1 + 2 - 3) // 2 + 1  # conv1 (7x7, stride 2, pad 3), then the max pooling
     cin = 64
     for li, (nb, width) in enumerate(zip(blocks, [64, 128, 256, 512])):
         for bi in range(nb):

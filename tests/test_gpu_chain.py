@@ -1,0 +1,107 @@
+"""GPU: a whole ResNet forward pass on the library, checked layer by layer.
+
+ResNetChain (bench.py) runs every convolution and the fully-connected layer
+as FGQ layers with their inputs quantized by fgq_quantize_act, and the glue
+between them (max pooling, residual additions and their ReLU, average
+pooling) in torch; the other ReLUs are the quantizer's clamp at zero.  Chained layers cannot be compared with an independently chained
+oracle (a one-ulp difference flips a rounding tie and the chains diverge
+legitimately), so each layer is checked on the codes the GPU fed it: its
+output against the oracle's layer on those codes (1e-5 of the summand
+magnitude, bit-exact where the direct kernel ran), every quantization
+against the oracle's quantization of the fp32 tensor it read, and the glue
+against numpy on the GPU's own tensors.
+"""
+import numpy as np
+import pytest
+import torch
+
+import bench
+import fgq_inputs as fi
+import oracle
+
+fgq = pytest.importorskip("paper_1705_01462_amd")
+
+pytestmark = [pytest.mark.gpu,
+              pytest.mark.skipif(not torch.cuda.is_available(), reason="needs a GPU")]
+
+TOL = 1e-5
+
+
+def host(t):
+    torch.cuda.synchronize()
+    return t.cpu().numpy()
+
+
+def maxpool3s2(a):
+    """3x3 max pooling, stride 2, padding 1, of an NHWC array."""
+    B, H, W, C = a.shape
+    p = np.full((B, H + 2, W + 2, C), -np.inf, np.float32)
+    p[:, 1:-1, 1:-1] = a
+    Ho, Wo = (H - 1) // 2 + 1, (W - 1) // 2 + 1
+    out = np.full((B, Ho, Wo, C), -np.inf, np.float32)
+    for r in range(3):
+        for s in range(3):
+            out = np.maximum(out, p[:, r:r + 2 * Ho:2, s:s + 2 * Wo:2])
+    return out
+
+
+@pytest.mark.parametrize("depth,G,bits,hw", [(50, 4, 8, 64), (101, 64, 4, 32)])
+def test_chained_forward_layer_by_layer(depth, G, bits, hw):
+    net = bench.ResNetChain(torch, fgq, fi, depth, G, bits, batch=2, hw=hw, tag="chain-test")
+    logits = host(net.forward())
+    assert np.isfinite(logits).all()
+    print(f"[chain] ResNet-{depth} G={G} u{bits} {hw}x{hw}: {len(net.layers)} layers", flush=True)
+
+    def check_quant(src, e, name):
+        q_ref, s_ref = oracle.quantize_act(host(src), bits)
+        assert host(e["sx"])[0] == np.float32(s_ref), name
+        np.testing.assert_array_equal(host(e["q"]), q_ref, err_msg=name)
+
+    for L in net.convs:
+        name = L["name"]
+        e = net.layers[name]
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        w = fi.he_weights(O, C, R, S, "chain-test", depth, name)
+        if name == "conv1":
+            w[:, 3:] = 0.0
+        t, a, _ = oracle.ternarize(w, e["g"])
+        q = host(e["q"])
+        sx = host(e["sx"])[0]
+        y = host(e["y"]).reshape(-1, O)
+        rows = np.arange(y.shape[0], dtype=np.int64)
+        y_ref, mag = oracle.conv2d_rows(q, bits, sx, (B, H, W, C), oracle.pack_codes(t), a, O, R, S,
+                                        (L["stride"],) * 2, (L["pad"],) * 2, e["g"], rows)
+        err = np.abs(y.astype(np.float64) - y_ref)
+        assert np.all(err <= TOL * mag), (name, float((err / np.maximum(mag, 1e-300)).max()))
+        if e["prep"] is None:
+            np.testing.assert_array_equal(y.view(np.uint32), y_ref.astype(np.float32).view(np.uint32))
+
+    # the stem, the blocks and the head
+    np.testing.assert_array_equal(host(net.stem), maxpool3s2(host(net.layers["conv1"]["y"])))
+    h = net.stem
+    for p, out in net.blocks.items():
+        c1, c2, c3 = (net.layers[f"{p}.c{i}"] for i in (1, 2, 3))
+        ds = net.layers.get(f"{p}.ds")
+        check_quant(h, c1, p + ".c1")
+        check_quant(c1["y"], c2, p + ".c2")
+        check_quant(c2["y"], c3, p + ".c3")
+        idn = host(ds["y"]) if ds is not None else host(h)
+        np.testing.assert_array_equal(host(out), np.maximum(host(c3["y"]) + idn, np.float32(0)), err_msg=p)
+        h = out
+    np.testing.assert_allclose(host(net.pooled), host(h).mean(axis=(1, 2)), rtol=1e-6, atol=0)
+    check_quant(net.pooled, net.layers["fc"], "fc")
+
+
+def test_fused_forward_matches_two_step_layers():
+    """The fused form (fgq_conv2d_q writing the next layer's codes at the
+    calibrated static scale) gives the codes of the layer followed by a
+    separate quantization at that scale, for every fused layer."""
+    net = bench.ResNetChain(torch, fgq, fi, 50, 4, 8, batch=2, hw=64, tag="chain-test")
+    net.calibrate()
+    assert np.isfinite(host(net.forward(fused=True))).all()
+    for p in net.blocks:
+        for i, j in ((1, 2), (2, 3)):
+            e, nxt = net.layers[f"{p}.c{i}"], net.layers[f"{p}.c{j}"]
+            net._conv(e)  # the same layer, fp32 output
+            q2, _ = fgq.fgq_quantize_act(e["y"], 8, scale_in=nxt["sx_static"])
+            np.testing.assert_array_equal(host(nxt["q"]), host(q2), err_msg=f"{p}.c{j}")
