@@ -617,6 +617,13 @@ class ResNetChain:
             if L["name"].endswith(".c3"):
                 p = L["name"][:-3]
                 self.blocks[p] = torch.empty_like(self.layers[L["name"]]["y"])
+        # a downsampling convolution reads the block input's codes (the
+        # stride is the convolution's), quantized once for both
+        for p in self.blocks:
+            ds = self.layers.get(f"{p}.ds")
+            if ds is not None:
+                c1 = self.layers[f"{p}.c1"]
+                ds["q"], ds["sx"], ds["ws"] = c1["q"], c1["sx"], c1["ws"]
         last = self.blocks[list(self.blocks)[-1]]
         self.pooled = torch.empty((last.shape[0], last.shape[3]), dtype=torch.float32, device="cuda")
 
@@ -630,24 +637,28 @@ class ResNetChain:
     def _quant(self, src, e):
         self.fgq.fgq_quantize_act(src, self.bits, q=e["q"], scale_out=e["sx"], ws=e["ws"])
 
-    def _conv_q(self, e, nxt):
-        """Layer e with the next layer's quantization fused (its codes written
-        straight into nxt's input, at nxt's static scale)."""
+    def _conv_q(self, e, nxt, sx=None):
+        """Layer e (input scale sx, default its own) with the next layer's
+        quantization fused: its codes written straight into nxt's input, at
+        nxt's static scale."""
         L = e["L"]
+        sx = e["sx"] if sx is None else sx
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
-        self.fgq.fgq_conv2d_q(e["q"], self.bits, e["sx"], (B, H, W, C), e["codes"], e["alpha"], O, R, S,
+        self.fgq.fgq_conv2d_q(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
                               L["stride"], L["pad"], e["g"], self.bits, nxt["sx_static"], prepared=e["prep"],
                               q_out=nxt["q"])
-        nxt["sx"].copy_(nxt["sx_static"])
 
-    def _conv(self, e):
+    def _conv(self, e, sx=None):
+        """Layer e on its input codes, at scale sx (default: its own, as
+        quantized)."""
         L = e["L"]
+        sx = e["sx"] if sx is None else sx
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
         if L["name"] == "fc":
-            self.fgq.fgq_gemm_ws(e["q"], self.bits, e["sx"], B, e["K"], e["codes"], e["alpha"], O, e["g"],
+            self.fgq.fgq_gemm_ws(e["q"], self.bits, sx, B, e["K"], e["codes"], e["alpha"], O, e["g"],
                                  prepared=e["prep"], out=e["y"].view(B, O), ws=e["wsfc"])
         else:
-            self.fgq.fgq_conv2d(e["q"], self.bits, e["sx"], (B, H, W, C), e["codes"], e["alpha"], O, R, S,
+            self.fgq.fgq_conv2d(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
                                 L["stride"], L["pad"], e["g"], prepared=e["prep"], y=e["y"])
 
     def forward(self, fused=False):
@@ -667,17 +678,17 @@ class ResNetChain:
             ds = self.layers.get(f"{p}.ds")
             self._quant(h, a)
             if ds is not None:
-                ds["q"], ds["sx"] = a["q"], a["sx"]  # the block input's codes (the stride is the conv's)
                 self._conv(ds)
             if fused:
                 self._conv_q(a, b)
-                self._conv_q(b, c)
+                self._conv_q(b, c, sx=b["sx_static"])
+                self._conv(c, sx=c["sx_static"])
             else:
                 self._conv(a)
                 self._quant(a["y"], b)
                 self._conv(b)
                 self._quant(b["y"], c)
-            self._conv(c)
+                self._conv(c)
             torch.add(c["y"], ds["y"] if ds is not None else h, out=out)
             out.relu_()
             h = out

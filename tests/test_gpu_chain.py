@@ -102,6 +102,6 @@ def test_fused_forward_matches_two_step_layers():
     for p in net.blocks:
         for i, j in ((1, 2), (2, 3)):
             e, nxt = net.layers[f"{p}.c{i}"], net.layers[f"{p}.c{j}"]
-            net._conv(e)  # the same layer, fp32 output
+            net._conv(e, sx=e["sx_static"] if i == 2 else None)  # the same layer, fp32 output
             q2, _ = fgq.fgq_quantize_act(e["y"], 8, scale_in=nxt["sx_static"])
             np.testing.assert_array_equal(host(nxt["q"]), host(q2), err_msg=f"{p}.c{j}")
