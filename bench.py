@@ -142,6 +142,28 @@ class Setup:
         return g
 
 
+def branch_graph(st, count, branches):
+    """One graph of steps 0..count-1 of the rotation dealt round-robin over
+    `branches` independent chains (step i on chain i % branches, so a set's
+    buffers are never used by two chains), forked from and joined back into
+    the capturing stream: a replay runs the chains concurrently, one batch's
+    quantization and tail overlapping another's convolution."""
+    torch = st.torch
+    g = torch.cuda.CUDAGraph()
+    side = [torch.cuda.Stream() for _ in range(branches)]
+    with torch.cuda.graph(g):
+        cap = torch.cuda.current_stream()
+        for s in side:
+            s.wait_stream(cap)
+        for r, s in enumerate(side):
+            with torch.cuda.stream(s):
+                for i in range(r, count, branches):
+                    st.step(i % len(st.sets))
+        for s in side:
+            cap.wait_stream(s)
+    return g
+
+
 def time_graphs(torch, graphs_and_reps):
     """Run each (graph, reps) pair in order between two events; wall and GPU ms."""
     torch.cuda.synchronize()
@@ -158,30 +180,50 @@ def time_graphs(torch, graphs_and_reps):
     return (t1 - t0) * 1e3, ev0.elapsed_time(ev1)
 
 
-def measure(torch, st, steps, warmup, conv_reps=20, trials=1):
-    """Times exactly `steps` steps (the reported figure), then, for
-    trials > 1, repeats the same timed region trials - 1 more times for a
-    median and spread; the component kernels are timed separately."""
+def measure(torch, st, steps, warmup, conv_reps=20, trials=1, streams=4):
+    """Times exactly `steps` steps (the reported figure): independent
+    batches (buffer sets) dealt round-robin over `streams` concurrent chains
+    of one graph, so one batch's quantization and tail overlap another's
+    convolution; then, for trials > 1, repeats the same timed region
+    trials - 1 more times for a median and spread.  The same steps on one
+    stream, and the component kernels alone, are timed separately."""
     nsets = len(st.sets)
-    # eager warm-up and a graph-replay correctness check against eager results
+    if nsets % streams:
+        raise ValueError("the buffer sets must divide evenly over the chains")
+    # eager warm-up and graph-replay correctness checks against eager results
     for i in range(nsets):
         st.step(i)
     torch.cuda.synchronize()
-    y_eager = st.sets[0][4].clone()
+    y_eager = [s[4].clone() for s in st.sets]
     full = st.graph(st.step, nsets)
     full.replay()
     full.replay()
     torch.cuda.synchronize()
-    if not torch.equal(st.sets[0][4], y_eager):
+    if not torch.equal(st.sets[0][4], y_eager[0]):
         raise RuntimeError("graph replay differs from eager execution")
+    full_b = branch_graph(st, nsets, streams)
+    for s in st.sets:
+        s[4].zero_()
+    full_b.replay()
+    torch.cuda.synchronize()
+    if not all(torch.equal(s[4], y) for s, y in zip(st.sets, y_eager)):
+        raise RuntimeError("replay of the concurrent chains differs from eager execution")
+    del y_eager
     rem = steps % nsets
     rem_graph = st.graph(st.step, rem) if rem else None
+    rem_b = branch_graph(st, rem, streams) if rem else None
     # warm-up replays (whole sets), then exactly `steps` timed steps
     for _ in range(max(1, -(-warmup // nsets))):
         full.replay()
+        full_b.replay()
+    for _ in range(2):
+        full_b.replay()
+    plan_b = [(full_b, steps // nsets)] + ([(rem_b, 1)] if rem_b else [])
+    wall_ms, gpu_ms = time_graphs(torch, plan_b)
+    trial_ms = [wall_ms] + [time_graphs(torch, plan_b)[0] for _ in range(trials - 1)]
+    # the same steps on one stream
     plan = [(full, steps // nsets)] + ([(rem_graph, 1)] if rem_graph else [])
-    wall_ms, gpu_ms = time_graphs(torch, plan)
-    trial_ms = [wall_ms] + [time_graphs(torch, plan)[0] for _ in range(trials - 1)]
+    one_ms = sorted(time_graphs(torch, plan)[0] for _ in range(max(1, min(trials, 3))))
     # the convolution alone, same stream, same rotation
     conv_g = st.graph(st.conv, nsets)
     conv_g.replay()
@@ -210,7 +252,8 @@ def measure(torch, st, steps, warmup, conv_reps=20, trials=1):
     _, dfp_ms = time_graphs(torch, [(dfp_g, conv_reps)])
     dfp_us = dfp_ms * 1e3 / (conv_reps * nsets)
     return dict(wall_ms=wall_ms, gpu_ms=gpu_ms, conv_us=conv_us, quant_us=quant_us, conv_fused_us=fused_us,
-                conv_dfp_us=dfp_us, trial_ms=trial_ms)
+                conv_dfp_us=dfp_us, trial_ms=trial_ms, streams=streams,
+                one_stream_ms=one_ms[len(one_ms) // 2])
 
 
 def host_cpu():
@@ -946,6 +989,9 @@ def main():
     ap.add_argument("--sets", type=int, default=96,
                     help="rotating buffer sets (~32 MB each; the 96 sets of 3.2 MB layer inputs "
                          "exceed the 256 MB memory-side cache)")
+    ap.add_argument("--streams", type=int, default=4,
+                    help="concurrent chains (streams forked inside one graph) the timed batches are "
+                         "dealt over (1: one after another); the buffer sets must divide evenly")
     ap.add_argument("--no-cpu", action="store_true", help="skip the CPU oracle baseline")
     ap.add_argument("--no-stacks", action="store_true", help="skip the ResNet stack measurements")
     ap.add_argument("--direct", action="store_true", help="time the direct per-group kernels")
@@ -1005,23 +1051,27 @@ def main():
 
     log(f"[bench] setting up G=4 ({args.sets} buffer sets)")
     st4 = Setup(torch, fgq, fi, LAYER, 4, bits, args.sets, folded=not args.direct)
-    r4 = measure(torch, st4, args.steps, args.warmup, trials=5)
+    r4 = measure(torch, st4, args.steps, args.warmup, trials=5, streams=args.streams)
     log(f"[bench] G=4: {r4}")
     ms_per_step = r4["wall_ms"] / args.steps
+    n_act = LAYER["B"] * LAYER["H"] * LAYER["W"] * LAYER["C"]
+    # a step's algorithmic bytes: fp32 input read and codes written by the
+    # quantization, then the convolution's own
+    step_bytes = 4 * n_act + n_act * bits // 8 + algorithmic_bytes(LAYER, 4, bits)
     del st4
     torch.cuda.empty_cache()
 
     log("[bench] setting up G=64")
     st64 = Setup(torch, fgq, fi, LAYER, 64, bits, args.sets, folded=not args.direct)
     steps64 = max(args.sets, args.steps // 4)
-    r64 = measure(torch, st64, steps64, args.sets)
+    r64 = measure(torch, st64, steps64, args.sets, streams=args.streams)
     log(f"[bench] G=64: {r64}")
     del st64
     torch.cuda.empty_cache()
 
     log("[bench] setting up the 1x1 layer, G=64")
     st11 = Setup(torch, fgq, fi, LAYER_1X1, 64, bits, args.sets, folded=not args.direct)
-    r11 = measure(torch, st11, steps64, args.sets)
+    r11 = measure(torch, st11, steps64, args.sets, streams=args.streams)
     log(f"[bench] 1x1 G=64: {r11}")
     del st11
     torch.cuda.empty_cache()
@@ -1047,18 +1097,25 @@ def main():
                    "B": LAYER["B"], "H": LAYER["H"], "W": LAYER["W"], "C": LAYER["C"], "O": LAYER["O"],
                    "R": 3, "S": 3, "G": 4, "bits": bits, "M": M, "K": K,
                    "kernel": "direct" if args.direct else "folded-scale int8 MFMA (G=4); per-group int8 MFMA + fp32 epilogue (G=64)",
-                   "step": "fgq_quantize_act + fgq_conv2d"},
+                   "step": "fgq_quantize_act + fgq_conv2d",
+                   "streams": args.streams},
         "roofline": roofline(LAYER, 4, bits, r4["conv_us"]),
         "step_detail": {"conv_us": round(r4["conv_us"], 3), "quantize_us": round(r4["quant_us"], 3),
                         "gpu_ms_per_step": round(r4["gpu_ms"] / args.steps, 5),
                         "trials_ms_per_step": [round(t / args.steps, 5) for t in r4["trial_ms"]],
                         "median_of_5_tops": round(ops / (sorted(r4["trial_ms"])[2] / args.steps * 1e-3) / 1e12, 2),
+                        "one_stream_ms_per_step": round(r4["one_stream_ms"] / args.steps, 5),
+                        "one_stream_tops": round(ops / (r4["one_stream_ms"] / args.steps * 1e-3) / 1e12, 2),
+                        "step_algorithmic_bytes": int(step_bytes),
+                        "step_hbm_gbs": round(step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
+                        "step_hbm_frac": round(step_bytes / (ms_per_step * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
                         "conv_only_tops": round(ops / (r4["conv_us"] * 1e-6) / 1e12, 1)},
         "fused": fused_entry(LAYER, 4, bits, r4, ops),
         "dfp": dfp_entry(LAYER, 4, bits, r4, ops),
         "g64": {"workload": "same layer, G=64", "steps": steps64,
                 "value": round(ops / (r64["wall_ms"] / steps64 * 1e-3) / 1e12, 2),
                 "ms_per_step": round(r64["wall_ms"] / steps64, 5),
+                "one_stream_tops": round(ops / (r64["one_stream_ms"] / steps64 * 1e-3) / 1e12, 2),
                 "conv_us": round(r64["conv_us"], 3),
                 "conv_only_tops": round(ops / (r64["conv_us"] * 1e-6) / 1e12, 1),
                 "roofline": roofline(LAYER, 64, bits, r64["conv_us"]),
@@ -1067,6 +1124,7 @@ def main():
         "g64_1x1": {"workload": "ResNet-50 1x1 conv 256->64, 56x56, batch 32, G=64", "steps": steps64,
                     "value": round(ops11 / (r11["wall_ms"] / steps64 * 1e-3) / 1e12, 2),
                     "ms_per_step": round(r11["wall_ms"] / steps64, 5),
+                    "one_stream_tops": round(ops11 / (r11["one_stream_ms"] / steps64 * 1e-3) / 1e12, 2),
                     "conv_us": round(r11["conv_us"], 3), "quantize_us": round(r11["quant_us"], 3),
                     "conv_only_tops": round(ops11 / (r11["conv_us"] * 1e-6) / 1e12, 1),
                     "roofline": roofline(LAYER_1X1, 64, bits, r11["conv_us"]),

@@ -439,6 +439,11 @@ fgq_status launch_cfg(const FoldArgs& a0, hipStream_t st) {
 // matrix instruction) and 128-row tiles (one workgroup per compute unit,
 // and register spills in the per-group kernel) were slower, and a tile
 // count balance of ceil(tiles / CUs) * kNB never prefers kNB = 4 over 2.
+// With weights expanded from codes at G = 4, 128-row waves fit without
+// spills (accumulators in the 192 accumulation registers) and halve the
+// expansion per matrix instruction, but a lone wave per SIMD leaves the
+// load and LDS latencies exposed: slower on every ResNet-50 layer
+// (1.0-1.55x).
 template <int kOut, bool kDfp, int kG, int kBits, int kNWO>
 fgq_status launch_nwo(const FoldArgs& a, hipStream_t st) {
   return launch_cfg<kOut, kDfp, kG, kBits, kNWO, 2>(a, st);
