@@ -742,27 +742,56 @@ class ResNetChain:
         return fc["y"]
 
 
-def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10):
+def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10, in_flight=3):
     """End-to-end time of ResNetChain's forward pass, captured in one HIP
-    graph: every layer's quantization, every FGQ layer and the torch glue."""
-    net = ResNetChain(torch, fgq, fi, depth, G, bits, batch)
-    net.calibrate()
-    res = {}
+    graph: every layer's quantization, every FGQ layer and the torch glue.
+    Also `in_flight` independent batches (one ResNetChain each, own buffers)
+    as concurrent chains of one graph, forked from and joined into the
+    capturing stream: the time per batch when batches overlap."""
+    nets = [ResNetChain(torch, fgq, fi, depth, G, bits, batch) for _ in range(in_flight)]
+    for net in nets:
+        net.calibrate()
+    net = nets[0]
+    res, conc = {}, {}
     for fused in (False, True):
-        net.forward(fused)
-        torch.cuda.synchronize()
-        ref = net.forward(fused).clone()
+        refs = []
+        for n in nets:
+            n.forward(fused)
+            torch.cuda.synchronize()
+            refs.append(n.forward(fused).clone())
         torch.cuda.synchronize()
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             net.forward(fused)
         g.replay()
         torch.cuda.synchronize()
-        if not torch.equal(net.layers["fc"]["y"], ref):
+        if not torch.equal(net.layers["fc"]["y"], refs[0]):
             raise RuntimeError("graph replay of the network differs from eager execution")
         _, ms = time_graphs(torch, [(g, reps)])
-        res[fused] = (ms * 1e3 / reps, bool(torch.isfinite(ref).all().item()))
+        res[fused] = (ms * 1e3 / reps, bool(torch.isfinite(refs[0]).all().item()))
         del g
+        if in_flight > 1:
+            gc = torch.cuda.CUDAGraph()
+            side = [torch.cuda.Stream() for _ in nets]
+            with torch.cuda.graph(gc):
+                cap = torch.cuda.current_stream()
+                for s in side:
+                    s.wait_stream(cap)
+                for s, n in zip(side, nets):
+                    with torch.cuda.stream(s):
+                        n.forward(fused)
+                for s in side:
+                    cap.wait_stream(s)
+            for n in nets:
+                n.layers["fc"]["y"].zero_()
+            gc.replay()
+            torch.cuda.synchronize()
+            if not all(torch.equal(n.layers["fc"]["y"], r) for n, r in zip(nets, refs)):
+                raise RuntimeError("concurrent replay of the networks differs from eager execution")
+            gc.replay()
+            _, ms = time_graphs(torch, [(gc, reps)])
+            conc[fused] = ms * 1e3 / (reps * in_flight)
+            del gc
     us, fus = res[False][0], res[True][0]
     out = {"workload": f"ResNet-{depth} forward pass, batch {batch}, 224x224, G={G}, u{bits}: every layer's "
                        "quantization, FGQ layer and the torch glue (max pooling, residual additions and their ReLU, "
@@ -772,7 +801,13 @@ def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10):
            "end_to_end_fused_us": round(fus, 1),
            "effective_tops_end_to_end_fused": round(net.ops / (fus * 1e-6) / 1e12, 1),
            "logits_finite": res[False][1] and res[True][1]}
-    del net
+    if in_flight > 1:
+        out["in_flight"] = {"batches": in_flight,
+                            "us_per_batch": round(conc[False], 1),
+                            "effective_tops": round(net.ops / (conc[False] * 1e-6) / 1e12, 1),
+                            "fused_us_per_batch": round(conc[True], 1),
+                            "effective_tops_fused": round(net.ops / (conc[True] * 1e-6) / 1e12, 1)}
+    del net, nets
     torch.cuda.empty_cache()
     return out
 
