@@ -4,7 +4,8 @@ eager results bit for bit.  Covers the dynamic-scale quantization (two
 passes), the folded and per-group convolutions, the row-walking folded
 kernel (a 1x1 layer with K = 64 over many row tiles), the fused 8-bit
 output, the fixed-point convolution, and the split-K GEMMs with their
-reduction (none of them may record a memset).
+reduction (none of them may record a memset); and independent batches as
+concurrent chains of one graph.
 """
 import numpy as np
 import pytest
@@ -99,3 +100,59 @@ def test_graph_replays_match_eager():
         torch.cuda.synchronize()
         for k, v in outs.items():
             assert torch.equal(v, eager[k]), f"eager after replay {rep}: {k} differs"
+
+
+@pytest.mark.parametrize("G,bits", [(4, 8), (64, 4)])
+def test_concurrent_chains_match_eager(G, bits):
+    """Independent batches as concurrent chains of one graph (the
+    benchmark's timed form): eight buffer sets dealt over four chains forked
+    from the capturing stream and joined back; every replay, with eager work
+    in between, reproduces each set's eager codes, scale and output."""
+    B, H, W, C, O, R, S = 4, 14, 14, 128, 128, 3, 3
+    K = R * S * C
+    w = fi.he_weights(O, C, R, S, "chains", G)
+    codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), G)
+    prep = fgq.fgq_prepare_weights(codes, alpha, O, K, G)
+    n = B * H * W * C
+    sets = []
+    for i in range(8):
+        x = torch.from_numpy(fi.relu_gauss((n,), "chains-x", G, i)).cuda()
+        sets.append(dict(x=x, q=torch.empty(n * bits // 8, dtype=torch.uint8, device="cuda"),
+                         sx=torch.empty(1, device="cuda"),
+                         ws=torch.empty(fgq.fgq_quantize_ws_bytes(n), dtype=torch.uint8, device="cuda"),
+                         y=torch.empty((B, H, W, O), device="cuda")))
+
+    def step(s):
+        fgq.fgq_quantize_act(s["x"], bits, q=s["q"], scale_out=s["sx"], ws=s["ws"])
+        fgq.fgq_conv2d(s["q"], bits, s["sx"], (B, H, W, C), codes, alpha, O, R, S, 1, 1, G, prepared=prep,
+                       y=s["y"])
+
+    for s in sets:
+        step(s)
+    torch.cuda.synchronize()
+    eager = [{k: s[k].clone() for k in ("q", "sx", "y")} for s in sets]
+    graph = torch.cuda.CUDAGraph()
+    side = [torch.cuda.Stream() for _ in range(4)]
+    with torch.cuda.graph(graph):
+        cap = torch.cuda.current_stream()
+        for st in side:
+            st.wait_stream(cap)
+        for r, st in enumerate(side):
+            with torch.cuda.stream(st):
+                for i in range(r, len(sets), len(side)):
+                    step(sets[i])
+        for st in side:
+            cap.wait_stream(st)
+    for rep in range(3):
+        for s in sets:
+            for k in ("q", "sx", "y"):
+                s[k].zero_()
+        torch.cuda.synchronize()
+        graph.replay()
+        torch.cuda.synchronize()
+        for i, (s, e) in enumerate(zip(sets, eager)):
+            for k in ("q", "sx", "y"):
+                assert torch.equal(s[k], e[k]), f"replay {rep}: set {i} {k} differs from the eager result"
+        step(sets[rep])  # eager work between replays
+        torch.cuda.synchronize()
+        assert torch.equal(sets[rep]["y"], eager[rep]["y"])
