@@ -12,6 +12,7 @@
 // each touch every bank once per pass.
 #pragma once
 
+#include <atomic>
 #include <type_traits>
 
 #include "fgq_internal.h"
@@ -305,16 +306,19 @@ inline bool igemm_shape_ok(const ConvGeom& g, const uint8_t* q, bool tiny_c = fa
 }
 
 // Compute units of the current device (cached per device; 256 if unknown).
+// Host threads may call this concurrently (calls on distinct streams are
+// thread-safe): the cache entries are atomics, and threads that race on the
+// first call store the same value.
 inline int device_cus() {
-  static int cached[64];
+  static std::atomic<int> cached[64];
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int n = 0;
+  int n = cached[dev].load(std::memory_order_relaxed);
+  if (n == 0) {
     if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n < 1) n = 256;
-    cached[dev] = n;
+    cached[dev].store(n, std::memory_order_relaxed);
   }
-  return cached[dev];
+  return n;
 }
 
 inline int c_mode(int64_t C) { return C % 16 == 0 ? (C >= kKT ? 0 : 1) : static_cast<int>(C); }
