@@ -602,8 +602,11 @@ class ResNetChain:
     the fully-connected layer through fgq_gemm_ws), and every layer's input
     is quantized by fgq_quantize_act with its own dynamic per-tensor scale.
     The glue between layers is plain torch on fp32 NHWC tensors: the
-    stem's 3x3 max pooling, the residual additions with their ReLU and the
-    global average pooling.  The ReLU after the stem and after the first two
+    stem's 3x3 max pooling and the global average pooling; each block's
+    shortcut addition and its ReLU are fused into the block's last
+    convolution (fgq_conv2d_residual writes max(conv + shortcut, 0) into the
+    block output), or with residual_fused=False run as a torch addition and
+    ReLU after it.  The ReLU after the stem and after the first two
     convolutions of a block is the quantizer's own clamp at zero (the codes
     and the scale of y and of ReLU(y) are the same), so those layers'
     outputs are quantized as they are.  The network input is pixel-like uint8 codes (128 + 32 z,
@@ -614,8 +617,9 @@ class ResNetChain:
     `self.layers`, and the stem and block outputs in `self.stem` and
     `self.blocks`, for checks."""
 
-    def __init__(self, torch, fgq, fi, depth, G, bits, batch, hw=224, tag="chain"):
+    def __init__(self, torch, fgq, fi, depth, G, bits, batch, hw=224, tag="chain", residual_fused=True):
         self.torch, self.fgq, self.bits = torch, fgq, bits
+        self.residual_fused = residual_fused
         self.convs = fi.resnet_convs(depth, batch, hw)
         self.layers = {}
         self.ops = 0.0
@@ -704,6 +708,15 @@ class ResNetChain:
             self.fgq.fgq_conv2d(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
                                 L["stride"], L["pad"], e["g"], prepared=e["prep"], y=e["y"])
 
+    def _conv_res(self, e, res, out, sx=None):
+        """Layer e with the block's shortcut addition and ReLU fused:
+        out = max(layer + res, 0)."""
+        L = e["L"]
+        sx = e["sx"] if sx is None else sx
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        self.fgq.fgq_conv2d_residual(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
+                                     L["stride"], L["pad"], e["g"], res, prepared=e["prep"], y=out)
+
     def forward(self, fused=False):
         """fused=False: every layer's input quantized with a dynamic scale.
         fused=True (after calibrate()): the first two convolutions of each
@@ -725,15 +738,20 @@ class ResNetChain:
             if fused:
                 self._conv_q(a, b)
                 self._conv_q(b, c, sx=b["sx_static"])
-                self._conv(c, sx=c["sx_static"])
+                sx_c = c["sx_static"]
             else:
                 self._conv(a)
                 self._quant(a["y"], b)
                 self._conv(b)
                 self._quant(b["y"], c)
-                self._conv(c)
-            torch.add(c["y"], ds["y"] if ds is not None else h, out=out)
-            out.relu_()
+                sx_c = None
+            shortcut = ds["y"] if ds is not None else h
+            if self.residual_fused:
+                self._conv_res(c, shortcut, out, sx=sx_c)
+            else:
+                self._conv(c, sx=sx_c)
+                torch.add(c["y"], shortcut, out=out)
+                out.relu_()
             h = out
         torch.mean(h, dim=(1, 2), out=self.pooled)
         fc = self.layers["fc"]
@@ -792,11 +810,23 @@ def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10, in_flight=3
             _, ms = time_graphs(torch, [(gc, reps)])
             conc[fused] = ms * 1e3 / (reps * in_flight)
             del gc
+    # the same pass with each block's shortcut addition and ReLU as torch ops
+    net.residual_fused = False
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        net.forward(False)
+    g.replay()
+    _, ms = time_graphs(torch, [(g, reps)])
+    torch_res_us = ms * 1e3 / reps
+    del g
+    net.residual_fused = True
     us, fus = res[False][0], res[True][0]
     out = {"workload": f"ResNet-{depth} forward pass, batch {batch}, 224x224, G={G}, u{bits}: every layer's "
-                       "quantization, FGQ layer and the torch glue (max pooling, residual additions and their ReLU, "
-                       "average pooling) in one graph; fused: the first two convolutions of each block write the "
-                       "next layer's codes at calibrated static scales",
+                       "quantization, FGQ layer (each block's last one with the block's shortcut addition and ReLU "
+                       "fused, fgq_conv2d_residual) and the torch glue (max pooling, average pooling) in one "
+                       "graph; fused: the first two convolutions of each block write the next layer's codes at "
+                       "calibrated static scales",
+           "end_to_end_torch_residual_us": round(torch_res_us, 1),
            "end_to_end_us": round(us, 1), "effective_tops_end_to_end": round(net.ops / (us * 1e-6) / 1e12, 1),
            "end_to_end_fused_us": round(fus, 1),
            "effective_tops_end_to_end_fused": round(net.ops / (fus * 1e-6) / 1e12, 1),

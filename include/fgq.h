@@ -347,6 +347,31 @@ fgq_status fgq_conv2d_q(const uint8_t* q, int32_t bits, const float* sx,
                         int32_t stride_h, int32_t stride_w, int32_t pad_h,
                         int32_t pad_w, int32_t G, int32_t out_bits,
                         const float* out_scale, uint8_t* q_out, void* stream);
+
+/*
+ * fgq_conv2d_residual -- the convolution with a residual block's shortcut
+ * addition and ReLU fused into its epilogue (the residual networks of the
+ * Sec. 4 experiments end each block with such an addition; it is not part of
+ * the FGQ layer itself).  Writes
+ *   y = max(yc + res, 0)   elementwise, the fp32 sum rounded once,
+ * where yc is the fp32 output fgq_conv2d computes with the same arguments
+ * (same kernels, same arithmetic; a NaN sum stays NaN), so the result equals
+ * fgq_conv2d followed by an fp32 addition and a ReLU, bit for bit, without
+ * the separate passes over the output.
+ *
+ * res [in]  fp32 [B][Ho][Wo][O] device tensor, the shortcut (the block input
+ *           or its projection); may be y itself (in place), must not
+ *           partially overlap it
+ * y   [out] fp32 [B][Ho][Wo][O]
+ * Other arguments and errors as fgq_conv2d; FGQ_ERR_NULL if res is NULL.
+ */
+fgq_status fgq_conv2d_residual(const uint8_t* q, int32_t bits, const float* sx,
+                               int64_t B, int64_t H, int64_t W, int64_t C,
+                               const uint8_t* codes, const float* alpha,
+                               const void* prepared, int64_t O, int32_t R,
+                               int32_t S, int32_t stride_h, int32_t stride_w,
+                               int32_t pad_h, int32_t pad_w, int32_t G,
+                               const float* res, float* y, void* stream);
 fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx,
                       int64_t M, int64_t K, const uint8_t* codes,
                       const float* alpha, const void* prepared, int64_t O,

@@ -57,6 +57,8 @@ _SIGS = {
     "fgq_prepare_weights": ([_P, _P, _I64, _I64, _I32, _P, _SZ, _P], _I32),
     "fgq_conv2d": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
                     _I32, _I32, _I32, _I32, _I32, _P, _P], _I32),
+    "fgq_conv2d_residual": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
+                             _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
     "fgq_gemm": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _P, _P], _I32),
     "fgq_conv2d_q": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
                       _I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
@@ -258,6 +260,27 @@ def fgq_conv2d(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, G, prepar
                           None if prepared is None else _dev(prepared, torch.uint8, "prepared"),
                           O, R, S, sh, sw, ph, pw, G, _dev(y, torch.float32, "y"), _stream())
     _check(rc, "fgq_conv2d")
+    return y
+
+
+def fgq_conv2d_residual(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, G, res, prepared=None, y=None):
+    """fgq_conv2d with a residual block's shortcut addition and ReLU fused:
+    y = max(conv + res, 0), res fp32 [B][Ho][Wo][O] (y may be res itself)."""
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv_out_hw(H, W, R, S, (sh, sw), (ph, pw))
+    if y is None:
+        y = torch.empty((B, Ho, Wo, O), dtype=torch.float32, device=q.device)
+    for t, name in ((res, "res"), (y, "y")):
+        if isinstance(t, torch.Tensor) and t.numel() != B * Ho * Wo * O:
+            raise ValueError(f"{name} must hold B*Ho*Wo*O = {B * Ho * Wo * O} values, got {t.numel()}")
+    rc = lib().fgq_conv2d_residual(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), B, H, W, C,
+                                   _dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                                   None if prepared is None else _dev(prepared, torch.uint8, "prepared"),
+                                   O, R, S, sh, sw, ph, pw, G, _dev(res, torch.float32, "res"),
+                                   _dev(y, torch.float32, "y"), _stream())
+    _check(rc, "fgq_conv2d_residual")
     return y
 
 

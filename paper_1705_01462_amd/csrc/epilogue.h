@@ -18,7 +18,10 @@
 // a 16-byte aligned output pointer); other shapes use the direct form.
 //
 // Output kinds (kOut): 0 = fp32 y; 8 = one code per byte; 4 = two codes per
-// byte, the even channel in the low nibble.  Codes follow qcode.h.
+// byte, the even channel in the low nibble; 2 = fp32 y = max(v + res, 0),
+// res an fp32 tensor of y's shape read at the same elements (a residual
+// block's shortcut addition and ReLU fused into its last layer).  Codes
+// follow qcode.h.
 #pragma once
 
 #include "qcode.h"
@@ -31,7 +34,7 @@ struct EpiTile {
   static constexpr int kNWM = 4 / kNWO;
   static constexpr int kTO = 32 * kNWO;   // tile channels
   static constexpr int kRows = kNWM * 32;  // tile rows per block pass
-  static constexpr int kRowBytes = kOut == 0 ? 4 * kTO : (kOut == 8 ? kTO : kTO / 2);
+  static constexpr int kRowBytes = (kOut == 0 || kOut == 2) ? 4 * kTO : (kOut == 8 ? kTO : kTO / 2);
   // 8 extra dwords per row: the two rows one write instruction touches
   // (4 apart) start 32 dwords apart modulo 64, so with 64 LDS banks their
   // 32-dword pieces do not share a bank.
@@ -39,15 +42,17 @@ struct EpiTile {
   static constexpr int kBytes = kRows * kPitch;
   static constexpr int kChunksPerRow = kRowBytes / 16;
   static constexpr int kChunks = kRows * kChunksPerRow;
-  static constexpr int kChanPerChunk = kOut == 0 ? 4 : (kOut == 8 ? 16 : 32);
+  static constexpr int kChanPerChunk = (kOut == 0 || kOut == 2) ? 4 : (kOut == 8 ? 16 : 32);
 };
 
-// Host side: whether the staged form applies to an output of O channels.
-inline bool epi_staged(int bits_out, int64_t O, const void* out) {
-  const bool aligned = reinterpret_cast<uintptr_t>(out) % 16 == 0;
-  const int64_t chunk = bits_out == 0 ? 4 : (bits_out == 8 ? 16 : 32);
+// Host side: whether the staged form applies to an output of O channels
+// (and, for kind 2, its residual).
+inline bool epi_staged(int bits_out, int64_t O, const void* out, const void* res = nullptr) {
+  const bool aligned = reinterpret_cast<uintptr_t>(out) % 16 == 0 && reinterpret_cast<uintptr_t>(res) % 16 == 0;
+  const int64_t chunk = (bits_out == 0 || bits_out == 2) ? 4 : (bits_out == 8 ? 16 : 32);
   return aligned && O % chunk == 0;
 }
+
 
 // The code of channel pair (o, o^1) as one byte, formed in the lane of the
 // even channel (lanes l and l^1 hold channels o and o^1).
@@ -60,6 +65,7 @@ struct OutPtrs {
   float* y;
   uint8_t* q;
   int M, O;
+  const float* res;  // kOut 2
 };
 
 // Direct form: each lane stores its own values.  `val(c, r)` is the fp32
@@ -78,6 +84,9 @@ __device__ inline void store_direct(const OutPtrs& out, const QScale& qs, int m_
       const float v = val(c, r);
       if constexpr (kOut == 0) {
         if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(v, out.y + e);
+      } else if constexpr (kOut == 2) {
+        if (check_store(kSiteStoreY, e, 1, n))
+          __builtin_nontemporal_store(add_relu(v, __builtin_nontemporal_load(out.res + e)), out.y + e);
       } else if constexpr (kOut == 8) {
         if (check_store(kSiteStoreY, e, 1, n))
           __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), out.q + e);
@@ -103,7 +112,7 @@ __device__ inline void store_staged(unsigned char* lds, const OutPtrs& out, cons
   const int lane = tid % 64;
   const int col = 32 * wo + lane % 32;  // the lane's channel within the tile
   unsigned char* base;
-  if constexpr (kOut == 0)
+  if constexpr (kOut == 0 || kOut == 2)
     base = reinterpret_cast<unsigned char*>(out.y);
   else
     base = out.q;
@@ -114,7 +123,7 @@ __device__ inline void store_staged(unsigned char* lds, const OutPtrs& out, cons
     for (int r = 0; r < 16; ++r) {
       const int lr = 32 * wm + 8 * (r / 4) + 4 * (lane / 32) + (r % 4);
       const float v = val(c, r);
-      if constexpr (kOut == 0) {
+      if constexpr (kOut == 0 || kOut == 2) {
         *reinterpret_cast<float*>(lds + lr * T::kPitch + 4 * col) = v;
       } else if constexpr (kOut == 8) {
         lds[lr * T::kPitch + col] = static_cast<unsigned char>(qcode<kRcp>(v, qs));
@@ -132,11 +141,19 @@ __device__ inline void store_staged(unsigned char* lds, const OutPtrs& out, cons
       const int m = m0 + (lr / 32) * kNB * 32 + 32 * c + lr % 32;
       const int ch = ot0 + cb * T::kChanPerChunk;
       if (m < out.M && ch < out.O) {
-        const u32x4 w = *reinterpret_cast<const u32x4*>(lds + lr * T::kPitch + 16 * cb);
-        const int64_t byte = (static_cast<int64_t>(m) * out.O + ch) * (kOut == 0 ? 4 : 1) / (kOut == 4 ? 2 : 1);
-        const int64_t nbytes = static_cast<int64_t>(out.M) * out.O * (kOut == 0 ? 4 : 1) / (kOut == 4 ? 2 : 1);
-        if (check_store(kSiteStoreY, byte, 16, nbytes))
+        u32x4 w = *reinterpret_cast<const u32x4*>(lds + lr * T::kPitch + 16 * cb);
+        constexpr int kEl = (kOut == 0 || kOut == 2) ? 4 : 1;
+        const int64_t byte = (static_cast<int64_t>(m) * out.O + ch) * kEl / (kOut == 4 ? 2 : 1);
+        const int64_t nbytes = static_cast<int64_t>(out.M) * out.O * kEl / (kOut == 4 ? 2 : 1);
+        if (check_store(kSiteStoreY, byte, 16, nbytes)) {
+          if constexpr (kOut == 2) {
+            const u32x4 rv = __builtin_nontemporal_load(
+                reinterpret_cast<const u32x4*>(reinterpret_cast<const unsigned char*>(out.res) + byte));
+#pragma unroll
+            for (int i = 0; i < 4; ++i) w[i] = __float_as_uint(add_relu(__uint_as_float(w[i]), __uint_as_float(rv[i])));
+          }
           __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(base + byte));
+        }
       }
     }
   }

@@ -213,7 +213,7 @@ __global__ __launch_bounds__(256) void exact_conv_kernel(
         const int64_t o = o0 + tx + 16 * j;  // lanes tx and tx^1 hold channels o and o^1
         if (o < g.O)
           emit_out<kOut, decltype(rcp)::value>(out.y, out.q, qs, m * g.O + o, g.M * g.O, static_cast<int>(o),
-                                               static_cast<float>(sx * acc[i][j]));
+                                               static_cast<float>(sx * acc[i][j]), out.res);
       }
     }
   });
@@ -268,6 +268,7 @@ fgq_status launch_exact_bits(const uint8_t* q, const float* sx, const uint8_t* c
                              const float* alpha, const ConvGeom& g, const LayerOut& y, hipStream_t st) {
   switch (y.bits) {
     case 0: return launch_exact_out<kBits, 0>(q, sx, codes, alpha, g, y, st);
+    case 2: return launch_exact_out<kBits, 2>(q, sx, codes, alpha, g, y, st);
     case 8: return launch_exact_out<kBits, 8>(q, sx, codes, alpha, g, y, st);
     default: return launch_exact_out<kBits, 4>(q, sx, codes, alpha, g, y, st);
   }

@@ -26,12 +26,15 @@ struct ConvGeom {
 // Where a layer's result goes: fp32 y (bits = 0), or the layer's output
 // fused with the next layer's activation quantization: unsigned `bits` codes
 // of every output value with the device scale *scale, NHWC like y (bits 4:
-// two channels per byte, the even channel in the low nibble; O even).
+// two channels per byte, the even channel in the low nibble; O even); or
+// (bits = 2) fp32 y = max(layer + res, 0) with res an fp32 tensor of y's
+// shape, a residual block's shortcut addition and ReLU.
 struct LayerOut {
   float* y;
   uint8_t* q;
   const float* scale;
   int32_t bits;
+  const float* res = nullptr;
 };
 
 inline hipStream_t as_stream(void* s) { return reinterpret_cast<hipStream_t>(s); }

@@ -27,13 +27,15 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.part = nullptr;
   a.splits = 1;
   a.steps_per_split = 1 << 30;
-  a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
+  a.res = out.res;
+  a.staged = ig::epi_staged(out.bits, g.O, (out.bits & ~2) ? static_cast<const void*>(out.q) : out.y, out.res);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
   set_codes_operand(a, g.G, base, L, 3);
   if (fold_rows_eligible(a)) return launch_fold_rows(a, g.bits, out.bits, st);
   switch (out.bits) {
     case 0: return launch_fold_out_f32(a, g.bits, st);
+    case 2: return launch_fold_out_res(a, g.bits, st);
     case 8: return launch_fold_out_q8(a, g.bits, st);
     default: return launch_fold_out_q4(a, g.bits, st);
   }

@@ -64,6 +64,7 @@ struct FoldArgs {
   float* y;
   uint8_t* qo;           // output codes (kOut 8 or 4)
   const float* oscale;   // their scale
+  const float* res = nullptr;  // residual added before the ReLU (kOut 2)
   const int32_t* fl;     // fixed-point scales: fractional length (prepared header)
   int32_t* part;         // split K (kOut 1): int32 sums [splits][planes][M][O]
   int32_t splits, steps_per_split;  // K steps [split*sps, min(nk, (split+1)*sps)) per workgroup
@@ -98,6 +99,7 @@ inline void set_codes_operand(FoldArgs& a, int32_t G, const char* base, const Pr
 fgq_status launch_fold_out_f32(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_out_q4(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_out_res(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_f32(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q4(const FoldArgs& a, int bits, hipStream_t st);
@@ -377,7 +379,7 @@ __global__ __launch_bounds__(kThreads, kNB <= 2 ? 2 : 1) void fold_conv_kernel(F
   } else {
     const float sx = *a.sx;
     // locals: a byte store may alias anything, including the argument block
-    const OutPtrs out{a.y, a.qo, a.x.M, a.x.O};
+    const OutPtrs out{a.y, a.qo, a.x.M, a.x.O, a.res};
     const bool staged = a.staged != 0;
     auto emit = [&](auto val) {
       with_out_scale<kOut>(a.oscale, [&](const QScale& qs, auto rcp) {

@@ -74,7 +74,7 @@ __global__ __launch_bounds__(kThreads, 2) void fold_rows_kernel(FoldArgs a) {
 
   const float c0 = o < a.x.O ? *a.sx * a.scale[o] : 0.0f;
   const float c1 = c0 * 255.0f, c2 = c0 * 65025.0f;
-  const OutPtrs out{a.y, a.qo, a.x.M, a.x.O};
+  const OutPtrs out{a.y, a.qo, a.x.M, a.x.O, a.res};
   const bool staged = a.staged != 0;
 
   int mt = blockIdx.x / a.x.n_otiles;

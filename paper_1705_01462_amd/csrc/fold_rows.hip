@@ -15,6 +15,7 @@ bool fold_rows_eligible(const FoldArgs& a) {
 fgq_status launch_fold_rows(const FoldArgs& a, int bits, int out_bits, hipStream_t st) {
   switch (out_bits) {
     case 0: return launch_rows<0>(a, bits, st);
+    case 2: return launch_rows<2>(a, bits, st);
     case 8: return launch_rows<8>(a, bits, st);
     default: return launch_rows<4>(a, bits, st);
   }

@@ -43,6 +43,7 @@ struct GroupArgs {
   float* y;
   uint8_t* qo;           // output codes (kOut 8 or 4)
   const float* oscale;   // their scale
+  const float* res = nullptr;  // residual added before the ReLU (kOut 2)
   int32_t staged;        // epilogue through LDS (epi_staged)
   int32_t nks, O32, codes_bytes, alpha_bytes;
 };
@@ -51,6 +52,7 @@ struct GroupArgs {
 fgq_status launch_group_out_f32(const GroupArgs& a, int bits, hipStream_t st);
 fgq_status launch_group_out_q8(const GroupArgs& a, int bits, hipStream_t st);
 fgq_status launch_group_out_q4(const GroupArgs& a, int bits, hipStream_t st);
+fgq_status launch_group_out_res(const GroupArgs& a, int bits, hipStream_t st);
 
 namespace {
 
@@ -184,7 +186,7 @@ __global__ __launch_bounds__(kThreads, 2) void group_conv_kernel(GroupArgs a) {
   const int o = o0 + lane % 32;
   const float sx = *a.sx;
   // locals: a byte store may alias anything, including the argument block
-  const OutPtrs out{a.y, a.qo, a.x.M, a.x.O};
+  const OutPtrs out{a.y, a.qo, a.x.M, a.x.O, a.res};
   const bool staged = a.staged != 0;
   with_out_scale<kOut>(a.oscale, [&](const QScale& qs, auto rcp) {
     constexpr bool kR = decltype(rcp)::value;

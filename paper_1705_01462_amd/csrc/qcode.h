@@ -66,16 +66,31 @@ __device__ inline void with_rcp(const QScale& c, F&& f) {
     f(std::false_type{});
 }
 
+// The fused shortcut addition and ReLU of output kind 2: max(v + r, 0), the
+// sum rounded once (a NaN sum stays NaN).  No contraction: v is often a
+// product, and an addition fused with it would round differently from the
+// layer's own fp32 output plus r.
+__device__ inline float add_relu(float v, float r) {
+#pragma clang fp contract(off)
+  const float s = v + r;
+  return s < 0.0f ? 0.0f : s;
+}
+
 // One output value of a layer, at element index e = m*O + o of n = M*O, by
-// output kind: kOut = 0 stores fp32 to y; kOut = 8 stores its code as one byte;
+// output kind: kOut = 0 stores fp32 to y; kOut = 2 stores max(v + res[e], 0)
+// to y (a residual block's shortcut addition and ReLU); kOut = 8 stores its
+// code as one byte;
 // kOut = 4 packs two codes per byte (the lanes holding channels o and o^1
 // must call together; the even one writes).  All stores are non-temporal:
 // the output is written once, and streaming it out leaves no dirty lines in
 // the per-XCD L2 caches for the end of the kernel to write back.
 template <int kOut, bool kRcp = true>
-__device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t e, int64_t n, int o, float v) {
+__device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t e, int64_t n, int o, float v,
+                                const float* res = nullptr) {
   if constexpr (kOut == 0) {
     if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(v, y + e);
+  } else if constexpr (kOut == 2) {
+    if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(add_relu(v, __builtin_nontemporal_load(res + e)), y + e);
   } else if constexpr (kOut == 8) {
     if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), q + e);
   } else {
@@ -93,7 +108,7 @@ __device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t 
 // used.
 template <int kOut, class F>
 __device__ inline void with_out_scale(const float* scale, F&& f) {
-  if constexpr (kOut == 0) {
+  if constexpr (kOut == 0 || kOut == 2) {
     f(QScale{}, std::true_type{});
   } else {
     const QScale qs = make_qscale(*scale, kOut);

@@ -76,6 +76,11 @@ def run_cases(fgq, torch):
         y = fgq.fgq_conv2d(q, bits, sx, shape, codes, alpha, O, R, S, st, pd, G, prepared=prep)
         res[tag + "_y"] = host(y)
         res[tag + "_ydirect"] = host(fgq.fgq_conv2d(q, bits, sx, shape, codes, alpha, O, R, S, st, pd, G))
+        shortcut = dev(fi.rng("check-res", *case).standard_normal(res[tag + "_y"].shape).astype(np.float32))
+        res[tag + "_res"] = host(fgq.fgq_conv2d_residual(q, bits, sx, shape, codes, alpha, O, R, S, st, pd, G,
+                                                         shortcut, prepared=prep))
+        res[tag + "_resdirect"] = host(fgq.fgq_conv2d_residual(q, bits, sx, shape, codes, alpha, O, R, S, st, pd,
+                                                               G, shortcut))
         yh = res[tag + "_y"]
         for ob in (8, 4):
             if ob == 4 and O % 2:

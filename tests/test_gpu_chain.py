@@ -1,15 +1,19 @@
 """GPU: a whole ResNet forward pass on the library, checked layer by layer.
 
 ResNetChain (bench.py) runs every convolution and the fully-connected layer
-as FGQ layers with their inputs quantized by fgq_quantize_act, and the glue
-between them (max pooling, residual additions and their ReLU, average
-pooling) in torch; the other ReLUs are the quantizer's clamp at zero.  Chained layers cannot be compared with an independently chained
-oracle (a one-ulp difference flips a rounding tie and the chains diverge
-legitimately), so each layer is checked on the codes the GPU fed it: its
-output against the oracle's layer on those codes (1e-5 of the summand
-magnitude, bit-exact where the direct kernel ran), every quantization
-against the oracle's quantization of the fp32 tensor it read, and the glue
-against numpy on the GPU's own tensors.
+as FGQ layers with their inputs quantized by fgq_quantize_act, each block's
+shortcut addition and ReLU fused into its last convolution
+(fgq_conv2d_residual; or, unfused, as torch ops after it), and the other
+glue (max pooling, average pooling) in torch; the other ReLUs are the
+quantizer's clamp at zero.  Chained layers cannot be compared with an
+independently chained oracle (a one-ulp difference flips a rounding tie and
+the chains diverge legitimately), so each layer is checked on the codes the
+GPU fed it: its output against the oracle's layer on those codes (1e-5 of
+the summand magnitude, bit-exact where the direct kernel ran; a block's
+output against the oracle's last layer plus the shortcut and ReLU, within
+that plus the addition's rounding), every quantization against the
+oracle's quantization of the fp32 tensor it read, and the glue against
+numpy on the GPU's own tensors.
 """
 import numpy as np
 import pytest
@@ -45,9 +49,11 @@ def maxpool3s2(a):
     return out
 
 
-@pytest.mark.parametrize("depth,G,bits,hw", [(50, 4, 8, 64), (101, 64, 4, 32)])
-def test_chained_forward_layer_by_layer(depth, G, bits, hw):
-    net = bench.ResNetChain(torch, fgq, fi, depth, G, bits, batch=2, hw=hw, tag="chain-test")
+@pytest.mark.parametrize("depth,G,bits,hw,residual_fused", [(50, 4, 8, 64, True), (101, 64, 4, 32, True),
+                                                             (50, 4, 8, 64, False)])
+def test_chained_forward_layer_by_layer(depth, G, bits, hw, residual_fused):
+    net = bench.ResNetChain(torch, fgq, fi, depth, G, bits, batch=2, hw=hw, tag="chain-test",
+                            residual_fused=residual_fused)
     logits = host(net.forward())
     assert np.isfinite(logits).all()
     print(f"[chain] ResNet-{depth} G={G} u{bits} {hw}x{hw}: {len(net.layers)} layers", flush=True)
@@ -57,6 +63,7 @@ def test_chained_forward_layer_by_layer(depth, G, bits, hw):
         assert host(e["sx"])[0] == np.float32(s_ref), name
         np.testing.assert_array_equal(host(e["q"]), q_ref, err_msg=name)
 
+    refs = {}
     for L in net.convs:
         name = L["name"]
         e = net.layers[name]
@@ -67,10 +74,14 @@ def test_chained_forward_layer_by_layer(depth, G, bits, hw):
         t, a, _ = oracle.ternarize(w, e["g"])
         q = host(e["q"])
         sx = host(e["sx"])[0]
-        y = host(e["y"]).reshape(-1, O)
-        rows = np.arange(y.shape[0], dtype=np.int64)
+        Ho, Wo = fgq.conv_out_hw(H, W, R, S, (L["stride"],) * 2, (L["pad"],) * 2)
+        rows = np.arange(B * Ho * Wo, dtype=np.int64)
         y_ref, mag = oracle.conv2d_rows(q, bits, sx, (B, H, W, C), oracle.pack_codes(t), a, O, R, S,
                                         (L["stride"],) * 2, (L["pad"],) * 2, e["g"], rows)
+        refs[name] = (y_ref, mag, e["prep"] is None)
+        if residual_fused and name.endswith(".c3"):
+            continue  # its output is the block's, checked below
+        y = host(e["y"]).reshape(-1, O)
         err = np.abs(y.astype(np.float64) - y_ref)
         assert np.all(err <= TOL * mag), (name, float((err / np.maximum(mag, 1e-300)).max()))
         if e["prep"] is None:
@@ -86,7 +97,18 @@ def test_chained_forward_layer_by_layer(depth, G, bits, hw):
         check_quant(c1["y"], c2, p + ".c2")
         check_quant(c2["y"], c3, p + ".c3")
         idn = host(ds["y"]) if ds is not None else host(h)
-        np.testing.assert_array_equal(host(out), np.maximum(host(c3["y"]) + idn, np.float32(0)), err_msg=p)
+        if residual_fused:
+            y_ref, mag, direct = refs[p + ".c3"]
+            idn2 = idn.reshape(y_ref.shape)
+            s = (y_ref + idn2).astype(np.float32)
+            want = np.where(s < 0, np.float32(0), s)
+            got = host(out).reshape(y_ref.shape)
+            bound = TOL * mag + np.abs(y_ref.astype(np.float64) + idn2) * 2.0 ** -23
+            if direct:
+                np.testing.assert_array_equal(got, want, err_msg=p)
+            assert np.all(np.abs(got.astype(np.float64) - want) <= bound), p
+        else:
+            np.testing.assert_array_equal(host(out), np.maximum(host(c3["y"]) + idn, np.float32(0)), err_msg=p)
         h = out
     np.testing.assert_allclose(host(net.pooled), host(h).mean(axis=(1, 2)), rtol=1e-6, atol=0)
     check_quant(net.pooled, net.layers["fc"], "fc")
