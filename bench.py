@@ -717,26 +717,42 @@ class ResNetChain:
         self.fgq.fgq_conv2d_residual(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
                                      L["stride"], L["pad"], e["g"], res, prepared=e["prep"], y=out)
 
+    def _conv_res_q(self, e, res, out, nxt, sx=None):
+        """Layer e with the block's shortcut addition and ReLU fused, writing
+        out and also its codes as nxt's input at nxt's static scale."""
+        L = e["L"]
+        sx = e["sx"] if sx is None else sx
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        self.fgq.fgq_conv2d_residual_q(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
+                                       L["stride"], L["pad"], e["g"], res, self.bits, nxt["sx_static"],
+                                       prepared=e["prep"], y=out, q_out=nxt["q"])
+
     def forward(self, fused=False):
         """fused=False: every layer's input quantized with a dynamic scale.
         fused=True (after calibrate()): the first two convolutions of each
         block write the next layer's codes at its static scale
-        (fgq_conv2d_q), so only the block inputs and the head are quantized
-        separately."""
+        (fgq_conv2d_q), and with residual_fused the last one also writes the
+        next block's input codes at that block's static scale
+        (fgq_conv2d_residual_q), so only the stem's output and the head are
+        quantized separately."""
         torch, F = self.torch, self.torch.nn.functional
         c1 = self.layers["conv1"]
         self._conv(c1)
         pooled = F.max_pool2d(c1["y"].permute(0, 3, 1, 2), 3, 2, 1)
         self.stem.copy_(pooled.permute(0, 2, 3, 1))
         h = self.stem
-        for p, out in self.blocks.items():
-            a, b, c = (self.layers[f"{p}.c{i}"] for i in (1, 2, 3))
+        names = list(self.blocks)
+        coded = False  # the block input's codes already written (static scale)
+        for bi, (p, out) in enumerate(self.blocks.items()):
+            a, b, c = (self.layers[f"{p}.c{j}"] for j in (1, 2, 3))
             ds = self.layers.get(f"{p}.ds")
-            self._quant(h, a)
+            if not coded:
+                self._quant(h, a)
+            sx_a = a["sx_static"] if coded else None
             if ds is not None:
-                self._conv(ds)
+                self._conv(ds, sx=sx_a)
             if fused:
-                self._conv_q(a, b)
+                self._conv_q(a, b, sx=sx_a)
                 self._conv_q(b, c, sx=b["sx_static"])
                 sx_c = c["sx_static"]
             else:
@@ -746,7 +762,12 @@ class ResNetChain:
                 self._quant(b["y"], c)
                 sx_c = None
             shortcut = ds["y"] if ds is not None else h
-            if self.residual_fused:
+            nxt = self.layers[f"{names[bi + 1]}.c1"] if bi + 1 < len(names) else None
+            coded = False
+            if self.residual_fused and fused and nxt is not None:
+                self._conv_res_q(c, shortcut, out, nxt, sx=sx_c)
+                coded = True
+            elif self.residual_fused:
                 self._conv_res(c, shortcut, out, sx=sx_c)
             else:
                 self._conv(c, sx=sx_c)

@@ -372,6 +372,25 @@ fgq_status fgq_conv2d_residual(const uint8_t* q, int32_t bits, const float* sx,
                                int32_t S, int32_t stride_h, int32_t stride_w,
                                int32_t pad_h, int32_t pad_w, int32_t G,
                                const float* res, float* y, void* stream);
+
+/*
+ * fgq_conv2d_residual_q -- fgq_conv2d_residual that also writes the codes of
+ * its output, the next block's input (Sec. 4: activations are quantized
+ * before each convolution), at a given scale:
+ *   y     = max(yc + res, 0)                             as fgq_conv2d_residual
+ *   q_out = fgq_quantize_act(y, out_bits, scale_in = out_scale)
+ * both bit for bit, from one epilogue.  Arguments as fgq_conv2d_residual,
+ * plus out_bits / out_scale / q_out as fgq_conv2d_q (out_bits 4 needs O even).
+ */
+fgq_status fgq_conv2d_residual_q(const uint8_t* q, int32_t bits, const float* sx,
+                                 int64_t B, int64_t H, int64_t W, int64_t C,
+                                 const uint8_t* codes, const float* alpha,
+                                 const void* prepared, int64_t O, int32_t R,
+                                 int32_t S, int32_t stride_h, int32_t stride_w,
+                                 int32_t pad_h, int32_t pad_w, int32_t G,
+                                 const float* res, float* y, int32_t out_bits,
+                                 const float* out_scale, uint8_t* q_out,
+                                 void* stream);
 fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx,
                       int64_t M, int64_t K, const uint8_t* codes,
                       const float* alpha, const void* prepared, int64_t O,

@@ -59,6 +59,8 @@ _SIGS = {
                     _I32, _I32, _I32, _I32, _I32, _P, _P], _I32),
     "fgq_conv2d_residual": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
                              _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
+    "fgq_conv2d_residual_q": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
+                               _I32, _I32, _I32, _I32, _I32, _P, _P, _I32, _P, _P, _P], _I32),
     "fgq_gemm": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _P, _P], _I32),
     "fgq_conv2d_q": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
                       _I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
@@ -282,6 +284,33 @@ def fgq_conv2d_residual(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, 
                                    _dev(y, torch.float32, "y"), _stream())
     _check(rc, "fgq_conv2d_residual")
     return y
+
+
+def fgq_conv2d_residual_q(q, bits, sx, shape, codes, alpha, O, R, S, stride, pad, G, res, out_bits, out_scale,
+                          prepared=None, y=None, q_out=None):
+    """fgq_conv2d_residual that also writes the codes of its output at the
+    device scale out_scale (fp32[1]): returns (y, q_out)."""
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv_out_hw(H, W, R, S, (sh, sw), (ph, pw))
+    n = B * Ho * Wo * O
+    if y is None:
+        y = torch.empty((B, Ho, Wo, O), dtype=torch.float32, device=q.device)
+    if q_out is None:
+        q_out = torch.empty((B, Ho, Wo, O * out_bits // 8), dtype=torch.uint8, device=q.device)
+    for t, name, want in ((res, "res", n), (y, "y", n), (q_out, "q_out", n * out_bits // 8)):
+        if isinstance(t, torch.Tensor) and t.numel() != want:
+            raise ValueError(f"{name} must hold {want} values, got {t.numel()}")
+    rc = lib().fgq_conv2d_residual_q(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), B, H, W, C,
+                                     _dev(codes, torch.uint8, "codes"), _dev(alpha, torch.float32, "alpha"),
+                                     None if prepared is None else _dev(prepared, torch.uint8, "prepared"),
+                                     O, R, S, sh, sw, ph, pw, G, _dev(res, torch.float32, "res"),
+                                     _dev(y, torch.float32, "y"), out_bits,
+                                     _dev(out_scale, torch.float32, "out_scale"), _dev(q_out, torch.uint8, "q_out"),
+                                     _stream())
+    _check(rc, "fgq_conv2d_residual_q")
+    return y, q_out
 
 
 def fgq_gemm(q, bits, sx, M, K, codes, alpha, O, G, prepared=None, y=None):

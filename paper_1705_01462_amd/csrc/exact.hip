@@ -269,6 +269,8 @@ fgq_status launch_exact_bits(const uint8_t* q, const float* sx, const uint8_t* c
   switch (y.bits) {
     case 0: return launch_exact_out<kBits, 0>(q, sx, codes, alpha, g, y, st);
     case 2: return launch_exact_out<kBits, 2>(q, sx, codes, alpha, g, y, st);
+    case 2 | 8: return launch_exact_out<kBits, 2 | 8>(q, sx, codes, alpha, g, y, st);
+    case 2 | 4: return launch_exact_out<kBits, 2 | 4>(q, sx, codes, alpha, g, y, st);
     case 8: return launch_exact_out<kBits, 8>(q, sx, codes, alpha, g, y, st);
     default: return launch_exact_out<kBits, 4>(q, sx, codes, alpha, g, y, st);
   }

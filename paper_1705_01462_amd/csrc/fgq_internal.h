@@ -28,7 +28,8 @@ struct ConvGeom {
 // of every output value with the device scale *scale, NHWC like y (bits 4:
 // two channels per byte, the even channel in the low nibble; O even); or
 // (bits = 2) fp32 y = max(layer + res, 0) with res an fp32 tensor of y's
-// shape, a residual block's shortcut addition and ReLU.
+// shape, a residual block's shortcut addition and ReLU; or (bits = 2 | 8,
+// 2 | 4) that y and also its codes in q.
 struct LayerOut {
   float* y;
   uint8_t* q;

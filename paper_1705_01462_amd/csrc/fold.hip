@@ -28,7 +28,7 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   a.splits = 1;
   a.steps_per_split = 1 << 30;
   a.res = out.res;
-  a.staged = ig::epi_staged(out.bits, g.O, (out.bits & ~2) ? static_cast<const void*>(out.q) : out.y, out.res);
+  a.staged = ig::epi_staged(out.bits, g.O, out.y, out.q, out.res);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(3 * L.O32 * L.Kp);
   set_codes_operand(a, g.G, base, L, 3);
@@ -36,6 +36,8 @@ fgq_status launch_fold_conv(const uint8_t* q, const float* sx, const void* prepa
   switch (out.bits) {
     case 0: return launch_fold_out_f32(a, g.bits, st);
     case 2: return launch_fold_out_res(a, g.bits, st);
+    case 2 | 8: return launch_fold_out_res_q8(a, g.bits, st);
+    case 2 | 4: return launch_fold_out_res_q4(a, g.bits, st);
     case 8: return launch_fold_out_q8(a, g.bits, st);
     default: return launch_fold_out_q4(a, g.bits, st);
   }

@@ -27,7 +27,7 @@ fgq_status launch_fold_dfp_conv(const uint8_t* q, const float* sx, const void* p
   a.part = nullptr;
   a.splits = 1;
   a.steps_per_split = 1 << 30;
-  a.staged = ig::epi_staged(out.bits, g.O, out.bits ? static_cast<const void*>(out.q) : out.y);
+  a.staged = ig::epi_staged(out.bits, g.O, out.y, out.q);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(L.O32 * L.Kp);
   a.xg = 0;  // the one-plane kernel reads the plane (see launch_out)

@@ -100,6 +100,8 @@ fgq_status launch_fold_out_f32(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_out_q4(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_out_res(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_out_res_q8(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_out_res_q4(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_f32(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q4(const FoldArgs& a, int bits, hipStream_t st);

@@ -1,0 +1,10 @@
+// fold_res_q8.hip -- the folded-scale layer kernels whose fp32 output takes a
+// residual block's shortcut addition and ReLU and that also write its
+// 8-bit codes (the next block's input).
+#include "fold_kernel.h"
+
+namespace fgq {
+
+fgq_status launch_fold_out_res_q8(const FoldArgs& a, int bits, hipStream_t st) { return launch_out<2 | 8>(a, bits, st); }
+
+}  // namespace fgq

@@ -16,6 +16,8 @@ fgq_status launch_fold_rows(const FoldArgs& a, int bits, int out_bits, hipStream
   switch (out_bits) {
     case 0: return launch_rows<0>(a, bits, st);
     case 2: return launch_rows<2>(a, bits, st);
+    case 2 | 8: return launch_rows<2 | 8>(a, bits, st);
+    case 2 | 4: return launch_rows<2 | 4>(a, bits, st);
     case 8: return launch_rows<8>(a, bits, st);
     default: return launch_rows<4>(a, bits, st);
   }

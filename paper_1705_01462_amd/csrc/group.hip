@@ -23,7 +23,7 @@ fgq_status launch_group_conv(const uint8_t* q, const float* sx, const void* prep
   a.qo = out.q;
   a.oscale = out.scale;
   a.res = out.res;
-  a.staged = ig::epi_staged(out.bits, g.O, (out.bits & ~2) ? static_cast<const void*>(out.q) : out.y, out.res);
+  a.staged = ig::epi_staged(out.bits, g.O, out.y, out.q, out.res);
   a.nks = static_cast<int32_t>(L.nks);
   a.O32 = static_cast<int32_t>(L.O32);
   a.codes_bytes = static_cast<int32_t>(L.O32 * L.Kp / 4);
@@ -31,6 +31,8 @@ fgq_status launch_group_conv(const uint8_t* q, const float* sx, const void* prep
   switch (out.bits) {
     case 0: return launch_group_out_f32(a, g.bits, st);
     case 2: return launch_group_out_res(a, g.bits, st);
+    case 2 | 8: return launch_group_out_res_q8(a, g.bits, st);
+    case 2 | 4: return launch_group_out_res_q4(a, g.bits, st);
     case 8: return launch_group_out_q8(a, g.bits, st);
     default: return launch_group_out_q4(a, g.bits, st);
   }

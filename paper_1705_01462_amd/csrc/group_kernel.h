@@ -53,6 +53,8 @@ fgq_status launch_group_out_f32(const GroupArgs& a, int bits, hipStream_t st);
 fgq_status launch_group_out_q8(const GroupArgs& a, int bits, hipStream_t st);
 fgq_status launch_group_out_q4(const GroupArgs& a, int bits, hipStream_t st);
 fgq_status launch_group_out_res(const GroupArgs& a, int bits, hipStream_t st);
+fgq_status launch_group_out_res_q8(const GroupArgs& a, int bits, hipStream_t st);
+fgq_status launch_group_out_res_q4(const GroupArgs& a, int bits, hipStream_t st);
 
 namespace {
 

@@ -66,6 +66,14 @@ __device__ inline void with_rcp(const QScale& c, F&& f) {
     f(std::false_type{});
 }
 
+// Output kinds of the layer kernels, as bit sets: 0 = fp32 output; 8 or 4 =
+// codes (8 or 4 bits) of the output instead; 2 = fp32 output with a
+// residual added before a ReLU; 2 | 8, 2 | 4 = that output and also its
+// codes.  (Kind 1, split-K partial sums, never reaches an epilogue.)
+constexpr bool out_res(int kind) { return kind != 1 && (kind & 2) != 0; }
+constexpr bool out_f32(int kind) { return kind == 0 || out_res(kind); }
+constexpr int out_code_bits(int kind) { return kind == 1 ? 0 : (kind & 12); }
+
 // The fused shortcut addition and ReLU of output kind 2: max(v + r, 0), the
 // sum rounded once (a NaN sum stays NaN).  No contraction: v is often a
 // product, and an addition fused with it would round differently from the
@@ -77,24 +85,26 @@ __device__ inline float add_relu(float v, float r) {
 }
 
 // One output value of a layer, at element index e = m*O + o of n = M*O, by
-// output kind: kOut = 0 stores fp32 to y; kOut = 2 stores max(v + res[e], 0)
-// to y (a residual block's shortcut addition and ReLU); kOut = 8 stores its
-// code as one byte;
-// kOut = 4 packs two codes per byte (the lanes holding channels o and o^1
-// must call together; the even one writes).  All stores are non-temporal:
-// the output is written once, and streaming it out leaves no dirty lines in
-// the per-XCD L2 caches for the end of the kernel to write back.
+// output kind: the residual and ReLU first where the kind has them
+// (v = max(v + res[e], 0)), then v stored as fp32 to y where it has an
+// fp32 output, and its code to q where it has codes: one byte (8 bits), or
+// two codes per byte (4 bits; the lanes holding channels o and o^1 must
+// call together and the even one writes).  All stores are non-temporal: the
+// output is written once, and streaming it out leaves no dirty lines in the
+// per-XCD L2 caches for the end of the kernel to write back.
 template <int kOut, bool kRcp = true>
 __device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t e, int64_t n, int o, float v,
                                 const float* res = nullptr) {
-  if constexpr (kOut == 0) {
+  constexpr int kCode = out_code_bits(kOut);
+  if constexpr (out_res(kOut)) {
+    if (check_store(kSiteStoreY, e, 1, n)) v = add_relu(v, __builtin_nontemporal_load(res + e));
+  }
+  if constexpr (out_f32(kOut)) {
     if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(v, y + e);
-  } else if constexpr (kOut == 2) {
-    if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(add_relu(v, __builtin_nontemporal_load(res + e)), y + e);
-  } else if constexpr (kOut == 8) {
+  }
+  if constexpr (kCode == 8) {
     if (check_store(kSiteStoreY, e, 1, n)) __builtin_nontemporal_store(static_cast<uint8_t>(qcode<kRcp>(v, qs)), q + e);
-  } else {
-    static_assert(kOut == 4, "output kind");
+  } else if constexpr (kCode == 4) {
     const unsigned c = qcode<kRcp>(v, qs);
     const unsigned other = static_cast<unsigned>(__builtin_amdgcn_mov_dpp(static_cast<int>(c), 0xB1, 0xF, 0xF, false));
     if ((o & 1) == 0 && check_store(kSiteStoreY, e >> 1, 1, (n + 1) / 2))
@@ -108,10 +118,10 @@ __device__ inline void emit_out(float* y, uint8_t* q, const QScale& qs, int64_t 
 // used.
 template <int kOut, class F>
 __device__ inline void with_out_scale(const float* scale, F&& f) {
-  if constexpr (kOut == 0 || kOut == 2) {
+  if constexpr (out_code_bits(kOut) == 0) {
     f(QScale{}, std::true_type{});
   } else {
-    const QScale qs = make_qscale(*scale, kOut);
+    const QScale qs = make_qscale(*scale, out_code_bits(kOut));
     with_rcp(qs, [&](auto rcp) { f(qs, rcp); });
   }
 }

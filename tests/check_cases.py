@@ -81,6 +81,13 @@ def run_cases(fgq, torch):
                                                          shortcut, prepared=prep))
         res[tag + "_resdirect"] = host(fgq.fgq_conv2d_residual(q, bits, sx, shape, codes, alpha, O, R, S, st, pd,
                                                                G, shortcut))
+        rsc = dev(np.array([np.float32(0.8 * max(float(res[tag + "_res"].max()), 1e-3) / 255.0)], np.float32))
+        yq, qq = fgq.fgq_conv2d_residual_q(q, bits, sx, shape, codes, alpha, O, R, S, st, pd, G, shortcut, 8, rsc,
+                                           prepared=prep)
+        res[tag + "_resq8"], res[tag + "_resq8y"] = host(qq), host(yq)
+        if O % 2 == 0:
+            res[tag + "_resq4d"] = host(fgq.fgq_conv2d_residual_q(q, bits, sx, shape, codes, alpha, O, R, S, st,
+                                                                  pd, G, shortcut, 4, rsc)[1])
         yh = res[tag + "_y"]
         for ob in (8, 4):
             if ob == 4 and O % 2:

@@ -116,14 +116,24 @@ def test_chained_forward_layer_by_layer(depth, G, bits, hw, residual_fused):
 
 def test_fused_forward_matches_two_step_layers():
     """The fused form (fgq_conv2d_q writing the next layer's codes at the
-    calibrated static scale) gives the codes of the layer followed by a
-    separate quantization at that scale, for every fused layer."""
+    calibrated static scale, fgq_conv2d_residual_q writing the next block's
+    input codes) gives the codes of the layer followed by a separate
+    quantization at that scale, for every fused layer."""
     net = bench.ResNetChain(torch, fgq, fi, 50, 4, 8, batch=2, hw=64, tag="chain-test")
     net.calibrate()
     assert np.isfinite(host(net.forward(fused=True))).all()
-    for p in net.blocks:
+    names = list(net.blocks)
+    for k, p in enumerate(names):
+        if k > 0:
+            # the block input's codes, written by the previous block's last
+            # convolution at this block's static scale
+            a = net.layers[f"{p}.c1"]
+            q2, _ = fgq.fgq_quantize_act(net.blocks[names[k - 1]].reshape(-1), 8, scale_in=a["sx_static"])
+            np.testing.assert_array_equal(host(a["q"]), host(q2), err_msg=f"{p}.c1")
+    for k, p in enumerate(names):
         for i, j in ((1, 2), (2, 3)):
             e, nxt = net.layers[f"{p}.c{i}"], net.layers[f"{p}.c{j}"]
-            net._conv(e, sx=e["sx_static"] if i == 2 else None)  # the same layer, fp32 output
+            sx = e["sx_static"] if (i == 2 or k > 0) else None
+            net._conv(e, sx=sx)  # the same layer, fp32 output
             q2, _ = fgq.fgq_quantize_act(e["y"], 8, scale_in=nxt["sx_static"])
             np.testing.assert_array_equal(host(nxt["q"]), host(q2), err_msg=f"{p}.c{j}")

@@ -6,7 +6,10 @@ prepared buffer, C % 4 != 0), staged (O % 4 == 0) and direct (O % 4 != 0)
 stores.
 
 Bars: bit-identical to fgq_conv2d followed by an fp32 addition and a ReLU
-(same kernels and arithmetic); the same in place (y is the residual);
+(same kernels and arithmetic); the same in place (y is the residual); with
+the output's 8- or 4-bit codes written by the same epilogue
+(fgq_conv2d_residual_q), the same fp32 output and codes bit-identical to
+fgq_quantize_act of it at the same scale;
 against the oracle's layer on sampled rows plus the same addition and ReLU,
 within the layer tolerance (1e-5 of the summand magnitude) plus the
 addition's rounding.
@@ -74,6 +77,18 @@ def test_residual_epilogue(case, prepared_path):
     # in place: the residual buffer receives the result
     fgq.fgq_conv2d_residual(q, bits, sx, shape, codes, alpha, O, R, S, st, pd, G, rd, prepared=prep, y=rd)
     np.testing.assert_array_equal(host(rd).reshape(-1, O), got)
+    # the output's codes from the same epilogue (the next block's input)
+    sc = dev(np.array([np.float32(0.8 * float(got.max()) / 255.0)], np.float32))
+    for ob in (8, 4):
+        if ob == 4 and O % 2:
+            continue
+        rd2 = dev(res)
+        scb = sc if ob == 8 else dev(np.array([np.float32(0.8 * float(got.max()) / 15.0)], np.float32))
+        y2, q2 = fgq.fgq_conv2d_residual_q(q, bits, sx, shape, codes, alpha, O, R, S, st, pd, G, rd2, ob, scb,
+                                           prepared=prep)
+        np.testing.assert_array_equal(host(y2).reshape(-1, O), got)
+        qref, _ = fgq.fgq_quantize_act(y2.reshape(-1), ob, scale_in=scb)
+        np.testing.assert_array_equal(host(q2).ravel(), host(qref))
     # the residual tensor must match the output's size
     with pytest.raises(ValueError):
         fgq.fgq_conv2d_residual(q, bits, sx, shape, codes, alpha, O, R, S, st, pd, G, rd.reshape(-1)[:-1],
