@@ -609,7 +609,10 @@ class ResNetChain:
     ReLU after it.  The ReLU after the stem and after the first two
     convolutions of a block is the quantizer's own clamp at zero (the codes
     and the scale of y and of ReLU(y) are the same), so those layers'
-    outputs are quantized as they are.  The network input is pixel-like uint8 codes (128 + 32 z,
+    outputs are quantized as they are.  With dfp=True the layers follow the
+    paper's pipeline: group scales as an 8-bit fixed point (fgq_conv2d_dfp
+    and its residual form, fgq_gemm_dfp_ws) and the first layer at 8-bit
+    weights (fgq_conv2d_w8).  The network input is pixel-like uint8 codes (128 + 32 z,
     clamped, scale 1/255; a zero fourth channel), the weights He-initialised
     and ternarized per layer (conv1 in groups of 4).  Every buffer is
     allocated up front, so forward() can be captured in a HIP graph; after
@@ -617,9 +620,14 @@ class ResNetChain:
     `self.layers`, and the stem and block outputs in `self.stem` and
     `self.blocks`, for checks."""
 
-    def __init__(self, torch, fgq, fi, depth, G, bits, batch, hw=224, tag="chain", residual_fused=True):
+    def __init__(self, torch, fgq, fi, depth, G, bits, batch, hw=224, tag="chain", residual_fused=True,
+                 dfp=False):
         self.torch, self.fgq, self.bits = torch, fgq, bits
         self.residual_fused = residual_fused
+        # dfp: the paper's pipeline -- group scales as an 8-bit fixed point
+        # (fgq_conv2d_dfp, fgq_gemm_dfp_ws) and the first layer at 8-bit
+        # weights (fgq_conv2d_w8)
+        self.dfp = dfp
         self.convs = fi.resnet_convs(depth, batch, hw)
         self.layers = {}
         self.ops = 0.0
@@ -634,13 +642,17 @@ class ResNetChain:
             Ho, Wo = fi.conv_out(H, W, R, S, L["stride"], L["pad"])
             n = B * H * W * C
             e = dict(L=L, g=g, K=K, codes=codes, alpha=alpha,
-                     prep=fgq.fgq_prepare_weights(codes, alpha, O, K, g, fallback=True),
+                     prep=None if dfp else fgq.fgq_prepare_weights(codes, alpha, O, K, g, fallback=True),
                      q=torch.empty(n * bits // 8, dtype=torch.uint8, device="cuda"),
                      sx=torch.empty(1, dtype=torch.float32, device="cuda"),
                      ws=torch.empty(max(fgq.fgq_quantize_ws_bytes(n), 4), dtype=torch.uint8, device="cuda"),
                      y=torch.empty((B, Ho, Wo, O), dtype=torch.float32, device="cuda"))
+            if dfp:
+                e["prep_dfp"] = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, g, 8)
+                if L["name"] == "conv1":
+                    e["prep_w8"] = fgq.fgq_prepare_weights_w8(torch.from_numpy(w).cuda())
             if L["name"] == "fc":
-                e["wsfc"] = torch.empty(max(fgq.fgq_gemm_ws_bytes(B, K, O, g, False), 4), dtype=torch.uint8,
+                e["wsfc"] = torch.empty(max(fgq.fgq_gemm_ws_bytes(B, K, O, g, dfp), 4), dtype=torch.uint8,
                                         device="cuda")
             self.layers[L["name"]] = e
             self.ops += 2.0 * B * Ho * Wo * O * R * S * (3 if L["name"] == "conv1" else C)
@@ -691,6 +703,10 @@ class ResNetChain:
         L = e["L"]
         sx = e["sx"] if sx is None else sx
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        if self.dfp:
+            self.fgq.fgq_conv2d_dfp(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["prep_dfp"], O, R, S,
+                                    L["stride"], L["pad"], e["g"], self.bits, nxt["sx_static"], out=nxt["q"])
+            return
         self.fgq.fgq_conv2d_q(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
                               L["stride"], L["pad"], e["g"], self.bits, nxt["sx_static"], prepared=e["prep"],
                               q_out=nxt["q"])
@@ -701,6 +717,17 @@ class ResNetChain:
         L = e["L"]
         sx = e["sx"] if sx is None else sx
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        if self.dfp:
+            if L["name"] == "fc":
+                self.fgq.fgq_gemm_dfp_ws(e["q"], self.bits, sx, B, e["K"], e["codes"], e["prep_dfp"], O, e["g"],
+                                         out=e["y"].view(B, O), ws=e["wsfc"])
+            elif L["name"] == "conv1":
+                self.fgq.fgq_conv2d_w8(e["q"], self.bits, sx, (B, H, W, C), e["prep_w8"], O, R, S, L["stride"],
+                                       L["pad"], out=e["y"])
+            else:
+                self.fgq.fgq_conv2d_dfp(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["prep_dfp"], O, R, S,
+                                        L["stride"], L["pad"], e["g"], out=e["y"])
+            return
         if L["name"] == "fc":
             self.fgq.fgq_gemm_ws(e["q"], self.bits, sx, B, e["K"], e["codes"], e["alpha"], O, e["g"],
                                  prepared=e["prep"], out=e["y"].view(B, O), ws=e["wsfc"])
@@ -714,6 +741,10 @@ class ResNetChain:
         L = e["L"]
         sx = e["sx"] if sx is None else sx
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        if self.dfp:
+            self.fgq.fgq_conv2d_dfp_residual(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["prep_dfp"], O, R,
+                                             S, L["stride"], L["pad"], e["g"], res, y=out)
+            return
         self.fgq.fgq_conv2d_residual(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
                                      L["stride"], L["pad"], e["g"], res, prepared=e["prep"], y=out)
 
@@ -723,6 +754,11 @@ class ResNetChain:
         L = e["L"]
         sx = e["sx"] if sx is None else sx
         B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        if self.dfp:
+            self.fgq.fgq_conv2d_dfp_residual(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["prep_dfp"], O, R,
+                                             S, L["stride"], L["pad"], e["g"], res, self.bits, nxt["sx_static"],
+                                             y=out, q_out=nxt["q"])
+            return
         self.fgq.fgq_conv2d_residual_q(e["q"], self.bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S,
                                        L["stride"], L["pad"], e["g"], res, self.bits, nxt["sx_static"],
                                        prepared=e["prep"], y=out, q_out=nxt["q"])
@@ -781,15 +817,10 @@ class ResNetChain:
         return fc["y"]
 
 
-def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10, in_flight=3):
-    """End-to-end time of ResNetChain's forward pass, captured in one HIP
-    graph: every layer's quantization, every FGQ layer and the torch glue.
-    Also `in_flight` independent batches (one ResNetChain each, own buffers)
-    as concurrent chains of one graph, forked from and joined into the
-    capturing stream: the time per batch when batches overlap."""
-    nets = [ResNetChain(torch, fgq, fi, depth, G, bits, batch) for _ in range(in_flight)]
-    for net in nets:
-        net.calibrate()
+def _time_nets(torch, nets, reps):
+    """One network's forward pass (dynamic scales, then the fused form with
+    static scales) captured in one graph, and the networks' passes as
+    concurrent chains of one graph; each checked against eager logits."""
     net = nets[0]
     res, conc = {}, {}
     for fused in (False, True):
@@ -809,7 +840,7 @@ def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10, in_flight=3
         _, ms = time_graphs(torch, [(g, reps)])
         res[fused] = (ms * 1e3 / reps, bool(torch.isfinite(refs[0]).all().item()))
         del g
-        if in_flight > 1:
+        if len(nets) > 1:
             gc = torch.cuda.CUDAGraph()
             side = [torch.cuda.Stream() for _ in nets]
             with torch.cuda.graph(gc):
@@ -829,36 +860,58 @@ def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10, in_flight=3
                 raise RuntimeError("concurrent replay of the networks differs from eager execution")
             gc.replay()
             _, ms = time_graphs(torch, [(gc, reps)])
-            conc[fused] = ms * 1e3 / (reps * in_flight)
+            conc[fused] = ms * 1e3 / (reps * len(nets))
             del gc
+    out = {"end_to_end_us": round(res[False][0], 1),
+           "effective_tops_end_to_end": round(net.ops / (res[False][0] * 1e-6) / 1e12, 1),
+           "end_to_end_fused_us": round(res[True][0], 1),
+           "effective_tops_end_to_end_fused": round(net.ops / (res[True][0] * 1e-6) / 1e12, 1),
+           "logits_finite": res[False][1] and res[True][1]}
+    if len(nets) > 1:
+        out["in_flight"] = {"batches": len(nets),
+                            "us_per_batch": round(conc[False], 1),
+                            "effective_tops": round(net.ops / (conc[False] * 1e-6) / 1e12, 1),
+                            "fused_us_per_batch": round(conc[True], 1),
+                            "effective_tops_fused": round(net.ops / (conc[True] * 1e-6) / 1e12, 1)}
+    return out
+
+
+def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10, in_flight=3):
+    """End-to-end time of ResNetChain's forward pass, captured in one HIP
+    graph: every layer's quantization, every FGQ layer and the torch glue.
+    Also `in_flight` independent batches (one ResNetChain each, own buffers)
+    as concurrent chains of one graph, forked from and joined into the
+    capturing stream: the time per batch when batches overlap.  The same
+    for the paper's pipeline (8-bit fixed-point group scales, the first
+    layer at 8-bit weights: `paper_pipeline`)."""
+    nets = [ResNetChain(torch, fgq, fi, depth, G, bits, batch) for _ in range(in_flight)]
+    for net in nets:
+        net.calibrate()
+    out = {"workload": f"ResNet-{depth} forward pass, batch {batch}, 224x224, G={G}, u{bits}: every layer's "
+                       "quantization, FGQ layer (each block's last one with the block's shortcut addition and ReLU "
+                       "fused, fgq_conv2d_residual) and the torch glue (max pooling, average pooling) in one "
+                       "graph; fused: the first two convolutions of each block write the next layer's codes and "
+                       "the last one the next block's input codes, at calibrated static scales"}
+    out.update(_time_nets(torch, nets, reps))
     # the same pass with each block's shortcut addition and ReLU as torch ops
+    net = nets[0]
     net.residual_fused = False
     g = torch.cuda.CUDAGraph()
     with torch.cuda.graph(g):
         net.forward(False)
     g.replay()
     _, ms = time_graphs(torch, [(g, reps)])
-    torch_res_us = ms * 1e3 / reps
-    del g
-    net.residual_fused = True
-    us, fus = res[False][0], res[True][0]
-    out = {"workload": f"ResNet-{depth} forward pass, batch {batch}, 224x224, G={G}, u{bits}: every layer's "
-                       "quantization, FGQ layer (each block's last one with the block's shortcut addition and ReLU "
-                       "fused, fgq_conv2d_residual) and the torch glue (max pooling, average pooling) in one "
-                       "graph; fused: the first two convolutions of each block write the next layer's codes at "
-                       "calibrated static scales",
-           "end_to_end_torch_residual_us": round(torch_res_us, 1),
-           "end_to_end_us": round(us, 1), "effective_tops_end_to_end": round(net.ops / (us * 1e-6) / 1e12, 1),
-           "end_to_end_fused_us": round(fus, 1),
-           "effective_tops_end_to_end_fused": round(net.ops / (fus * 1e-6) / 1e12, 1),
-           "logits_finite": res[False][1] and res[True][1]}
-    if in_flight > 1:
-        out["in_flight"] = {"batches": in_flight,
-                            "us_per_batch": round(conc[False], 1),
-                            "effective_tops": round(net.ops / (conc[False] * 1e-6) / 1e12, 1),
-                            "fused_us_per_batch": round(conc[True], 1),
-                            "effective_tops_fused": round(net.ops / (conc[True] * 1e-6) / 1e12, 1)}
-    del net, nets
+    out["end_to_end_torch_residual_us"] = round(ms * 1e3 / reps, 1)
+    del g, net, nets
+    torch.cuda.empty_cache()
+    nets = [ResNetChain(torch, fgq, fi, depth, G, bits, batch, dfp=True) for _ in range(in_flight)]
+    for net in nets:
+        net.calibrate()
+    out["paper_pipeline"] = {"layers": "group scales as an 8-bit fixed point (fgq_conv2d_dfp, "
+                                       "fgq_conv2d_dfp_residual, fgq_gemm_dfp_ws), the first layer at 8-bit "
+                                       "weights (fgq_conv2d_w8)"}
+    out["paper_pipeline"].update(_time_nets(torch, nets, reps))
+    del nets
     torch.cuda.empty_cache()
     return out
 

@@ -454,6 +454,26 @@ fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx,
                         void* stream);
 
 /*
+ * fgq_conv2d_dfp_residual -- fgq_conv2d_dfp with a residual block's shortcut
+ * addition and ReLU in its epilogue, as fgq_conv2d_residual does for
+ * fgq_conv2d: y = max(yd + res, 0) for the fp32 output yd of fgq_conv2d_dfp
+ * (the sum rounded once), bit for bit.  out_bits 0: y only; 8 or 4: also
+ * q_out = fgq_quantize_act(y, out_bits, scale_in = out_scale) (4 needs O
+ * even), the next block's input.  res: fp32 [B][Ho][Wo][O], may be y
+ * itself, must not partially overlap it.  Other arguments as
+ * fgq_conv2d_dfp; out_scale and q_out are ignored when out_bits is 0.
+ */
+fgq_status fgq_conv2d_dfp_residual(const uint8_t* q, int32_t bits, const float* sx,
+                                   int64_t B, int64_t H, int64_t W, int64_t C,
+                                   const uint8_t* codes, const void* prepared,
+                                   int64_t O, int32_t R, int32_t S,
+                                   int32_t stride_h, int32_t stride_w,
+                                   int32_t pad_h, int32_t pad_w, int32_t G,
+                                   const float* res, float* y, int32_t out_bits,
+                                   const float* out_scale, uint8_t* q_out,
+                                   void* stream);
+
+/*
  * GEMMs with split K, for fully-connected layers at small batch (few rows,
  * long K: the rows and channels alone would occupy few compute units).
  *

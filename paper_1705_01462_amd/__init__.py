@@ -61,6 +61,8 @@ _SIGS = {
                              _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
     "fgq_conv2d_residual_q": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
                                _I32, _I32, _I32, _I32, _I32, _P, _P, _I32, _P, _P, _P], _I32),
+    "fgq_conv2d_dfp_residual": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _I64, _I32, _I32,
+                                 _I32, _I32, _I32, _I32, _I32, _P, _P, _I32, _P, _P, _P], _I32),
     "fgq_gemm": ([_P, _I32, _P, _I64, _I64, _P, _P, _P, _I64, _I32, _P, _P], _I32),
     "fgq_conv2d_q": ([_P, _I32, _P, _I64, _I64, _I64, _I64, _P, _P, _P, _I64, _I32, _I32,
                       _I32, _I32, _I32, _I32, _I32, _I32, _P, _P, _P], _I32),
@@ -451,6 +453,34 @@ def fgq_gemm_ws(q, bits, sx, M, K, codes, alpha, O, G, prepared=None, out_bits=0
                            ws.numel() if ws is not None else 0, _stream())
     _check(rc, "fgq_gemm_ws")
     return out
+
+
+def fgq_conv2d_dfp_residual(q, bits, sx, shape, codes, prepared, O, R, S, stride, pad, G, res, out_bits=0,
+                            out_scale=None, y=None, q_out=None):
+    """fgq_conv2d_dfp with a residual block's shortcut addition and ReLU
+    fused: y = max(layer + res, 0); with out_bits 8 or 4 also the codes of y
+    at out_scale.  Returns y, or (y, q_out) when out_bits is not 0."""
+    B, H, W, C = shape
+    sh, sw = _pair(stride)
+    ph, pw = _pair(pad)
+    Ho, Wo = conv_out_hw(H, W, R, S, (sh, sw), (ph, pw))
+    n = B * Ho * Wo * O
+    if y is None:
+        y = torch.empty((B, Ho, Wo, O), dtype=torch.float32, device=q.device)
+    if out_bits and q_out is None:
+        q_out = torch.empty((B, Ho, Wo, O * out_bits // 8), dtype=torch.uint8, device=q.device)
+    checks = [(res, "res", n), (y, "y", n)] + ([(q_out, "q_out", n * out_bits // 8)] if out_bits else [])
+    for t, name, want in checks:
+        if isinstance(t, torch.Tensor) and t.numel() != want:
+            raise ValueError(f"{name} must hold {want} values, got {t.numel()}")
+    rc = lib().fgq_conv2d_dfp_residual(_dev(q, torch.uint8, "q"), bits, _dev(sx, torch.float32, "sx"), B, H, W, C,
+                                       _dev(codes, torch.uint8, "codes"), _dev(prepared, torch.uint8, "prepared"),
+                                       O, R, S, sh, sw, ph, pw, G, _dev(res, torch.float32, "res"),
+                                       _dev(y, torch.float32, "y"), out_bits,
+                                       None if not out_bits else _dev(out_scale, torch.float32, "out_scale"),
+                                       None if not out_bits else _dev(q_out, torch.uint8, "q_out"), _stream())
+    _check(rc, "fgq_conv2d_dfp_residual")
+    return (y, q_out) if out_bits else y
 
 
 def fgq_gemm_dfp_ws(q, bits, sx, M, K, codes, prepared, O, G, out_bits=0, out_scale=None, out=None, ws=None):

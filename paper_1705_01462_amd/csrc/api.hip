@@ -459,6 +459,25 @@ fgq_status fgq_conv2d_dfp(const uint8_t* q, int32_t bits, const float* sx, int64
   return run_layer_dfp(q, sx, codes, prepared, g, lo, stream);
 }
 
+fgq_status fgq_conv2d_dfp_residual(const uint8_t* q, int32_t bits, const float* sx, int64_t B, int64_t H,
+                                   int64_t W, int64_t C, const uint8_t* codes, const void* prepared,
+                                   int64_t O, int32_t R, int32_t S, int32_t stride_h, int32_t stride_w,
+                                   int32_t pad_h, int32_t pad_w, int32_t G, const float* res, float* y,
+                                   int32_t out_bits, const float* out_scale, uint8_t* q_out, void* stream) {
+  if (!q || !sx || !codes || !prepared || !res || !y) return FGQ_ERR_NULL;
+  if (out_bits != 0 && (!out_scale || !q_out)) return FGQ_ERR_NULL;
+  ConvGeom g;
+  fgq_status err;
+  if (!conv_geom(B, H, W, C, O, R, S, stride_h, stride_w, pad_h, pad_w, G, bits, &g, &err))
+    return err;
+  if (out_bits != 0 && out_bits != 8 && out_bits != 4) return FGQ_ERR_BITS;
+  if (out_bits == 4 && O % 2 != 0) return FGQ_ERR_BITS;
+  if (reinterpret_cast<uintptr_t>(prepared) % 256 != 0) return FGQ_ERR_WORKSPACE;
+  LayerOut lo{y, out_bits ? q_out : nullptr, out_bits ? out_scale : nullptr, 2 | out_bits};
+  lo.res = res;
+  return run_layer_dfp(q, sx, codes, prepared, g, lo, stream);
+}
+
 fgq_status fgq_gemm_dfp(const uint8_t* q, int32_t bits, const float* sx, int64_t M, int64_t K,
                         const uint8_t* codes, const void* prepared, int64_t O, int32_t G,
                         int32_t out_bits, const float* out_scale, void* out, void* stream) {

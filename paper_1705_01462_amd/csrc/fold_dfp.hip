@@ -27,12 +27,16 @@ fgq_status launch_fold_dfp_conv(const uint8_t* q, const float* sx, const void* p
   a.part = nullptr;
   a.splits = 1;
   a.steps_per_split = 1 << 30;
-  a.staged = ig::epi_staged(out.bits, g.O, out.y, out.q);
+  a.res = out.res;
+  a.staged = ig::epi_staged(out.bits, g.O, out.y, out.q, out.res);
   a.nks = static_cast<int32_t>(L.nks);
   a.planes_bytes = static_cast<int32_t>(L.O32 * L.Kp);
   a.xg = 0;  // the one-plane kernel reads the plane (see launch_out)
   switch (out.bits) {
     case 0: return launch_fold_dfp_out_f32(a, g.bits, st);
+    case 2: return launch_fold_dfp_out_res(a, g.bits, st);
+    case 2 | 8: return launch_fold_dfp_out_res_q8(a, g.bits, st);
+    case 2 | 4: return launch_fold_dfp_out_res_q4(a, g.bits, st);
     case 8: return launch_fold_dfp_out_q8(a, g.bits, st);
     default: return launch_fold_dfp_out_q4(a, g.bits, st);
   }

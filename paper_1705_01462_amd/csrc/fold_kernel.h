@@ -105,6 +105,9 @@ fgq_status launch_fold_out_res_q4(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_f32(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q8(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_out_q4(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_dfp_out_res(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_dfp_out_res_q8(const FoldArgs& a, int bits, hipStream_t st);
+fgq_status launch_fold_dfp_out_res_q4(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_part(const FoldArgs& a, int bits, hipStream_t st);
 fgq_status launch_fold_dfp_part(const FoldArgs& a, int bits, hipStream_t st);
 // Short reductions (K <= 128) over many row tiles, fp32 group scales: the

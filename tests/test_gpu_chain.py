@@ -137,3 +137,80 @@ def test_fused_forward_matches_two_step_layers():
             net._conv(e, sx=sx)  # the same layer, fp32 output
             q2, _ = fgq.fgq_quantize_act(e["y"], 8, scale_in=nxt["sx_static"])
             np.testing.assert_array_equal(host(nxt["q"]), host(q2), err_msg=f"{p}.c{j}")
+
+
+@pytest.mark.parametrize("depth,G,bits,hw", [(50, 4, 8, 64), (101, 64, 4, 32)])
+def test_paper_pipeline_forward_layer_by_layer(depth, G, bits, hw):
+    """The paper's pipeline (group scales as an 8-bit fixed point, the first
+    layer at 8-bit weights): every layer bit-exact against the oracle's
+    fixed-point layer on the codes the GPU fed it, each block output
+    against the oracle's last layer plus the shortcut and ReLU, every
+    quantization bit-exact; the fused form's codes equal the two-step ones."""
+    net = bench.ResNetChain(torch, fgq, fi, depth, G, bits, batch=2, hw=hw, tag="chain-test", dfp=True)
+    logits = host(net.forward())
+    assert np.isfinite(logits).all()
+
+    def check_quant(src, e, name):
+        q_ref, s_ref = oracle.quantize_act(host(src), bits)
+        assert host(e["sx"])[0] == np.float32(s_ref), name
+        np.testing.assert_array_equal(host(e["q"]), q_ref, err_msg=name)
+
+    refs = {}
+    for L in net.convs:
+        name = L["name"]
+        e = net.layers[name]
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        w = fi.he_weights(O, C, R, S, "chain-test", depth, name)
+        if name == "conv1":
+            w[:, 3:] = 0.0
+        q, sx = host(e["q"]), host(e["sx"])[0]
+        st, pd = (L["stride"],) * 2, (L["pad"],) * 2
+        if name == "conv1":
+            W8, fl = oracle.w8_quantize(w)
+            y_ref = oracle.conv2d_w8(q, bits, sx, (B, H, W, C), W8, fl, O, R, S, st, pd)
+        else:
+            t, a, _ = oracle.ternarize(w, e["g"])
+            A, fl = oracle.dfp_alpha(a, 8)
+            if name == "fc":
+                y_ref = oracle.gemm_dfp(q, bits, sx, B, C, oracle.pack_codes(t), A, fl, O, e["g"])
+            else:
+                y_ref = oracle.conv2d_dfp(q, bits, sx, (B, H, W, C), oracle.pack_codes(t), A, fl, O, R, S, st, pd,
+                                          e["g"])
+        y_ref = y_ref.reshape(-1, O).astype(np.float32)
+        refs[name] = y_ref
+        if name.endswith(".c3"):
+            continue  # its output is the block's, checked below
+        np.testing.assert_array_equal(host(e["y"]).reshape(-1, O).view(np.uint32), y_ref.view(np.uint32),
+                                      err_msg=name)
+
+    np.testing.assert_array_equal(host(net.stem), maxpool3s2(host(net.layers["conv1"]["y"])))
+    h = net.stem
+    for p, out in net.blocks.items():
+        c1, c2, c3 = (net.layers[f"{p}.c{i}"] for i in (1, 2, 3))
+        ds = net.layers.get(f"{p}.ds")
+        check_quant(h, c1, p + ".c1")
+        check_quant(c1["y"], c2, p + ".c2")
+        check_quant(c2["y"], c3, p + ".c3")
+        idn = (host(ds["y"]) if ds is not None else host(h)).reshape(refs[p + ".c3"].shape)
+        s = (refs[p + ".c3"] + idn).astype(np.float32)
+        want = np.where(s < 0, np.float32(0), s)
+        np.testing.assert_array_equal(host(out).reshape(want.shape).view(np.uint32), want.view(np.uint32),
+                                      err_msg=p)
+        h = out
+    check_quant(net.pooled, net.layers["fc"], "fc")
+
+    # the fused form: every fused layer's codes equal the layer then a separate quantization
+    net.calibrate()
+    assert np.isfinite(host(net.forward(fused=True))).all()
+    names = list(net.blocks)
+    for k, p in enumerate(names):
+        if k > 0:
+            a = net.layers[f"{p}.c1"]
+            q2, _ = fgq.fgq_quantize_act(net.blocks[names[k - 1]].reshape(-1), bits, scale_in=a["sx_static"])
+            np.testing.assert_array_equal(host(a["q"]), host(q2), err_msg=f"{p}.c1")
+    for k, p in enumerate(names):
+        for i, j in ((1, 2), (2, 3)):
+            e, nxt = net.layers[f"{p}.c{i}"], net.layers[f"{p}.c{j}"]
+            net._conv(e, sx=e["sx_static"] if (i == 2 or k > 0) else None)
+            q2, _ = fgq.fgq_quantize_act(e["y"], bits, scale_in=nxt["sx_static"])
+            np.testing.assert_array_equal(host(nxt["q"]), host(q2), err_msg=f"{p}.c{j}")

@@ -209,3 +209,30 @@ def test_conv2d_w8_unsupported_and_bad_weights():
     with pytest.raises(fgq.FgqError) as e:
         fgq.fgq_prepare_weights_w8(dev(w))
     assert e.value.code == 5
+
+
+@pytest.mark.parametrize("out_bits", [0, 8, 4])
+@pytest.mark.parametrize("case", [LAYER_CASES[0], LAYER_CASES[2], LAYER_CASES[4], LAYER_CASES[5],
+                                  LAYER_CASES[7]])
+def test_conv2d_dfp_residual_bit_exact(case, out_bits):
+    """The shortcut addition and ReLU in the epilogue (and the output's codes
+    from it): the oracle's layer plus an fp32 addition and a ReLU, and the
+    oracle's quantization of that, bit for bit."""
+    B, H, W, C, O, R, S, st, pd, G, bits, ab = case
+    if out_bits == 4 and O % 2:
+        pytest.skip("4-bit output needs even O")
+    codes, q, sx, prep, ref, shape = dfp_layer(*case, tag=case)
+    y_ref = oracle.conv2d_dfp(ref["q"], bits, ref["s"], shape, ref["codes"], ref["A"], ref["fl"], O, R, S,
+                              (st, st), (pd, pd), G).reshape(-1, O)
+    res = fi.rng("gpu-dfp-residual", case).standard_normal(y_ref.shape).astype(np.float32)
+    s = (y_ref + res).astype(np.float32)
+    want = np.where(s < 0, np.float32(0), s)
+    Ho, Wo = fgq.conv_out_hw(H, W, R, S, (st, st), (pd, pd))
+    rd = dev(res.reshape(B, Ho, Wo, O))
+    s_out = np.float32(0.8 * float(want.max()) / (2 ** out_bits - 1)) if out_bits else None
+    sc = dev(np.array([s_out], np.float32)) if out_bits else None
+    got = fgq.fgq_conv2d_dfp_residual(q, bits, sx, shape, codes, prep, O, R, S, st, pd, G, rd, out_bits, sc)
+    y = got[0] if out_bits else got
+    np.testing.assert_array_equal(host(y).reshape(-1, O).view(np.uint32), want.view(np.uint32))
+    if out_bits:
+        np.testing.assert_array_equal(host(got[1]).ravel(), oracle.quantize_act(want.ravel(), out_bits, s_out)[0])
