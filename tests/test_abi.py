@@ -224,3 +224,26 @@ def test_layer_validation():
 @no_device
 def test_no_device_reports_hip_error():
     assert fgq.lib().fgq_device_count() == 0
+
+
+@no_device
+def test_residual_validation():
+    L = fgq.lib()
+    geo = (P, 8, P, 2, 8, 8, 16, P, P, None, 16, 3, 3, 1, 1, 1, 1, 4)
+    assert L.fgq_conv2d_residual(*geo, None, P, None) == 1              # FGQ_ERR_NULL: res
+    assert L.fgq_conv2d_residual(*geo, P, None, None) == 1              # FGQ_ERR_NULL: y
+    assert L.fgq_conv2d_residual(P, 8, P, 2, 8, 8, 15, P, P, None, 16, 3, 3, 1, 1, 1, 1, 4,
+                                 P, P, None) == 3                       # FGQ_ERR_GROUP: C % G
+    rq = lambda O, ob, sc, qo: L.fgq_conv2d_residual_q(P, 8, P, 2, 8, 8, 16, P, P, None, O, 3, 3, 1, 1, 1, 1,
+                                                       4, P, P, ob, sc, qo, None)
+    assert rq(16, 7, P, P) == 4                                         # out_bits
+    assert rq(15, 4, P, P) == 4                                         # 4-bit output needs even O
+    assert rq(16, 8, None, P) == 1                                      # scale for codes
+    assert rq(16, 8, P, None) == 1                                      # q_out
+    dr = lambda ob, sc, qo, prep: L.fgq_conv2d_dfp_residual(P, 8, P, 2, 8, 8, 16, P, prep, 16, 3, 3, 1, 1, 1, 1,
+                                                            4, P, P, ob, sc, qo, None)
+    assert dr(0, None, None, None) == 1                                 # prepared required
+    assert dr(8, None, P, P) == 1                                       # scale for codes
+    assert dr(8, P, None, P) == 1                                       # q_out for codes
+    assert dr(6, P, P, P) == 4                                          # out_bits
+    assert dr(0, None, None, ctypes.c_void_p(0x1001)) == 8              # prepared alignment
