@@ -60,16 +60,7 @@ def _compile(src, verbose, check=False):
     return obj
 
 
-def build(verbose=False, jobs=None, check=False):
-    """Compile libfgq.so; with check=True the checking build
-    libfgq_check.so (-DFGQ_CHECK: bounds-checked loads and stores, see
-    csrc/bufcheck.h), from the same sources into its own object folder."""
-    os.makedirs(BUILD_CHECK if check else BUILD, exist_ok=True)
-    # the kernel-heavy sources first, so the parallel compile ends together
-    srcs = sorted(sources(), key=lambda s: not os.path.basename(s).startswith(("fold", "group")))
-    jobs = jobs or min(len(srcs), 8)
-    with cf.ThreadPoolExecutor(jobs) as ex:
-        objs = list(ex.map(lambda s: _compile(s, verbose, check), srcs))
+def _link(objs, check, verbose):
     out = LIB_CHECK if check else LIB
     tmp = out + ".tmp"
     cmd = ["hipcc", f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
@@ -80,5 +71,37 @@ def build(verbose=False, jobs=None, check=False):
     return out
 
 
+def build_all(verbose=False, jobs=None):
+    """Both libraries (libfgq.so and the checking build libfgq_check.so)
+    from one pool of compile jobs, the kernel-heavy sources of the slower
+    checking build first, so that the cores stay busy to the end."""
+    os.makedirs(BUILD, exist_ok=True)
+    os.makedirs(BUILD_CHECK, exist_ok=True)
+    heavy = lambda s: os.path.basename(s).startswith(("fold", "group"))
+    srcs = sources()
+    order = ([(s, True) for s in srcs if heavy(s)] + [(s, False) for s in srcs if heavy(s)] +
+             [(s, True) for s in srcs if not heavy(s)] + [(s, False) for s in srcs if not heavy(s)])
+    jobs = jobs or min(len(order), os.cpu_count() or 8)
+    with cf.ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(lambda sc: (sc[1], _compile(sc[0], verbose, sc[1])), order))
+    return [_link(sorted(o for c, o in objs if c == check), check, verbose) for check in (False, True)]
+
+
+def build(verbose=False, jobs=None, check=False):
+    """Compile libfgq.so; with check=True the checking build
+    libfgq_check.so (-DFGQ_CHECK: bounds-checked loads and stores, see
+    csrc/bufcheck.h), from the same sources into its own object folder."""
+    os.makedirs(BUILD_CHECK if check else BUILD, exist_ok=True)
+    # the kernel-heavy sources first, so the parallel compile ends together
+    srcs = sorted(sources(), key=lambda s: not os.path.basename(s).startswith(("fold", "group")))
+    jobs = jobs or min(len(srcs), 8)
+    with cf.ThreadPoolExecutor(jobs) as ex:
+        objs = list(ex.map(lambda s: _compile(s, verbose, check), srcs))
+    return _link(objs, check, verbose)
+
+
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv, check="--check" in sys.argv))
+    if "--all" in sys.argv:
+        print(build_all(verbose="-v" in sys.argv))
+    else:
+        print(build(verbose="-v" in sys.argv, check="--check" in sys.argv))
