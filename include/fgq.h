@@ -347,6 +347,11 @@ fgq_status fgq_conv2d_q(const uint8_t* q, int32_t bits, const float* sx,
                         int32_t stride_h, int32_t stride_w, int32_t pad_h,
                         int32_t pad_w, int32_t G, int32_t out_bits,
                         const float* out_scale, uint8_t* q_out, void* stream);
+fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx,
+                      int64_t M, int64_t K, const uint8_t* codes,
+                      const float* alpha, const void* prepared, int64_t O,
+                      int32_t G, int32_t out_bits, const float* out_scale,
+                      uint8_t* q_out, void* stream);
 
 /*
  * fgq_conv2d_residual -- the convolution with a residual block's shortcut
@@ -391,11 +396,6 @@ fgq_status fgq_conv2d_residual_q(const uint8_t* q, int32_t bits, const float* sx
                                  const float* res, float* y, int32_t out_bits,
                                  const float* out_scale, uint8_t* q_out,
                                  void* stream);
-fgq_status fgq_gemm_q(const uint8_t* q, int32_t bits, const float* sx,
-                      int64_t M, int64_t K, const uint8_t* codes,
-                      const float* alpha, const void* prepared, int64_t O,
-                      int32_t G, int32_t out_bits, const float* out_scale,
-                      uint8_t* q_out, void* stream);
 
 /*
  * Fixed-point group scales (Sec. 4: the scaling factors are quantized to an
