@@ -685,6 +685,7 @@ class ResNetChain:
                 ds["q"], ds["sx"], ds["ws"] = c1["q"], c1["sx"], c1["ws"]
         last = self.blocks[list(self.blocks)[-1]]
         self.pooled = torch.empty((last.shape[0], last.shape[3]), dtype=torch.float32, device="cuda")
+        self.logits = self.layers["fc"]["y"]
 
     def calibrate(self):
         """Static input scales for the fused form: each layer's scale from one
@@ -835,7 +836,7 @@ def _time_nets(torch, nets, reps):
             net.forward(fused)
         g.replay()
         torch.cuda.synchronize()
-        if not torch.equal(net.layers["fc"]["y"], refs[0]):
+        if not torch.equal(net.logits, refs[0]):
             raise RuntimeError("graph replay of the network differs from eager execution")
         _, ms = time_graphs(torch, [(g, reps)])
         res[fused] = (ms * 1e3 / reps, bool(torch.isfinite(refs[0]).all().item()))
@@ -853,10 +854,10 @@ def _time_nets(torch, nets, reps):
                 for s in side:
                     cap.wait_stream(s)
             for n in nets:
-                n.layers["fc"]["y"].zero_()
+                n.logits.zero_()
             gc.replay()
             torch.cuda.synchronize()
-            if not all(torch.equal(n.layers["fc"]["y"], r) for n, r in zip(nets, refs)):
+            if not all(torch.equal(n.logits, r) for n, r in zip(nets, refs)):
                 raise RuntimeError("concurrent replay of the networks differs from eager execution")
             gc.replay()
             _, ms = time_graphs(torch, [(gc, reps)])
@@ -913,6 +914,166 @@ def chain_measure(torch, fgq, fi, depth, G, bits, batch=64, reps=10, in_flight=3
     out["paper_pipeline"].update(_time_nets(torch, nets, reps))
     del nets
     torch.cuda.empty_cache()
+    return out
+
+
+class AlexNetChain:
+    """A whole AlexNet forward pass on the library (single tower, 227x227
+    pixel-like uint8 input with a zero fourth channel, batch `batch`):
+    conv1 -> 3x3/2 max pooling -> conv2 -> pooling -> conv3 -> conv4 ->
+    conv5 -> pooling -> fc6 -> fc7 -> fc8, every convolution and
+    fully-connected layer an FGQ layer (fgq_conv2d, fgq_gemm_ws) with its
+    input quantized by fgq_quantize_act; the ReLUs are the quantizer's clamp
+    at zero (a max pooling of y and of ReLU(y) gives the same codes), and
+    the pooling is torch on fp32 NHWC.  Fused form (after calibrate()):
+    conv3 -> conv4 -> conv5 and fc6 -> fc7 -> fc8 write the next layer's
+    codes at calibrated static scales.  dfp=True: the paper's pipeline, the
+    first layer at 8-bit weights (fgq_conv2d_w8) and the others with 8-bit
+    fixed-point group scales (fgq_conv2d_dfp, fgq_gemm_dfp_ws).  Every
+    buffer is allocated up front, so forward() can be captured in a graph;
+    each layer's input codes, scale and fp32 output stay in `self.layers`,
+    the pooled tensors in `self.pooled`.  The weights are those the per-layer
+    AlexNet measurement draws (the same tag); a layer whose scales fail the
+    folded layout's accuracy guard runs on the exact direct kernel and is
+    listed in `self.direct_layers`."""
+
+    def __init__(self, torch, fgq, fi, G, bits, batch, tag="alexnet-bench", dfp=False):
+        self.torch, self.fgq, self.bits, self.dfp = torch, fgq, bits, dfp
+        self.convs = fi.alexnet_layers(batch)
+        self.layers, self.ops = {}, 0.0
+        for L in self.convs:
+            B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+            g = G if C % G == 0 else 4
+            w = fi.he_weights(O, C, R, S, tag, L["name"])
+            if L["name"] == "conv1":
+                w[:, 3:] = 0.0
+            codes, alpha, _ = fgq.fgq_ternarize(torch.from_numpy(w).cuda(), g)
+            K = R * S * C
+            Ho, Wo = fi.conv_out(H, W, R, S, L["stride"], L["pad"])
+            n = B * H * W * C
+            e = dict(L=L, g=g, K=K, codes=codes, alpha=alpha, fc=H == 1 and W == 1,
+                     q=torch.empty(n * bits // 8, dtype=torch.uint8, device="cuda"),
+                     sx=torch.empty(1, dtype=torch.float32, device="cuda"),
+                     ws=torch.empty(max(fgq.fgq_quantize_ws_bytes(n), 4), dtype=torch.uint8, device="cuda"),
+                     y=torch.empty((B, Ho, Wo, O), dtype=torch.float32, device="cuda"))
+            if dfp:
+                e["prep"] = fgq.fgq_prepare_weights_dfp(codes, alpha, O, K, g, 8)
+                if L["name"] == "conv1":
+                    e["prep_w8"] = fgq.fgq_prepare_weights_w8(torch.from_numpy(w).cuda())
+            else:
+                e["prep"] = fgq.fgq_prepare_weights(codes, alpha, O, K, g, fallback=True)
+            if e["fc"]:
+                e["wsfc"] = torch.empty(max(fgq.fgq_gemm_ws_bytes(B, K, O, g, dfp), 4), dtype=torch.uint8,
+                                        device="cuda")
+            self.layers[L["name"]] = e
+            self.ops += 2.0 * B * Ho * Wo * O * R * S * (3 if L["name"] == "conv1" else C)
+        self.direct_layers = [n for n, e in self.layers.items() if e["prep"] is None]
+        L0 = self.convs[0]
+        z = fi.rng("alexnet-chain-input", batch).standard_normal((L0["B"], L0["H"], L0["W"], 4))
+        x0 = np.clip(np.rint(128.0 + 32.0 * z), 0, 255).astype(np.uint8)
+        x0[..., 3] = 0
+        if bits == 4:
+            x0 = x0 >> 4
+            x0 = (x0[..., 0::2] | (x0[..., 1::2] << 4)).astype(np.uint8)
+        c1 = self.layers["conv1"]
+        c1["q"].copy_(torch.from_numpy(x0.reshape(-1)))
+        c1["sx"].fill_(1.0 / (255.0 if bits == 8 else 15.0))
+        self.pooled = {}
+        for a, b in (("conv1", "conv2"), ("conv2", "conv3"), ("conv5", "fc6")):
+            y = self.layers[a]["y"]
+            Hp = (y.shape[1] - 3) // 2 + 1
+            self.pooled[a] = torch.empty((y.shape[0], Hp, Hp, y.shape[3]), dtype=torch.float32, device="cuda")
+        self.logits = self.layers["fc8"]["y"]
+
+    def calibrate(self):
+        """Static input scales for the fused form, from one dynamic pass."""
+        self.forward()
+        for e in self.layers.values():
+            e["sx_static"] = e["sx"].clone()
+
+    def _quant(self, src, e):
+        self.fgq.fgq_quantize_act(src, self.bits, q=e["q"], scale_out=e["sx"], ws=e["ws"])
+
+    def _layer(self, e, sx=None, nxt=None):
+        """Layer e at input scale sx (default: its own); with nxt, writing
+        nxt's input codes at nxt's static scale instead of fp32."""
+        f, L, bits = self.fgq, e["L"], self.bits
+        sx = e["sx"] if sx is None else sx
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        ob, osc = (bits, nxt["sx_static"]) if nxt is not None else (0, None)
+        if e["fc"]:
+            out = nxt["q"] if nxt is not None else e["y"].view(B, O)
+            if self.dfp:
+                f.fgq_gemm_dfp_ws(e["q"], bits, sx, B, e["K"], e["codes"], e["prep"], O, e["g"], ob, osc, out=out,
+                                  ws=e["wsfc"])
+            else:
+                f.fgq_gemm_ws(e["q"], bits, sx, B, e["K"], e["codes"], e["alpha"], O, e["g"], prepared=e["prep"],
+                              out_bits=ob, out_scale=osc, out=out, ws=e["wsfc"])
+        elif self.dfp and L["name"] == "conv1":
+            f.fgq_conv2d_w8(e["q"], bits, sx, (B, H, W, C), e["prep_w8"], O, R, S, L["stride"], L["pad"],
+                            out=e["y"])
+        elif self.dfp:
+            f.fgq_conv2d_dfp(e["q"], bits, sx, (B, H, W, C), e["codes"], e["prep"], O, R, S, L["stride"], L["pad"],
+                             e["g"], ob, osc, out=nxt["q"] if nxt is not None else e["y"])
+        elif nxt is not None:
+            f.fgq_conv2d_q(e["q"], bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S, L["stride"], L["pad"],
+                           e["g"], bits, osc, prepared=e["prep"], q_out=nxt["q"])
+        else:
+            f.fgq_conv2d(e["q"], bits, sx, (B, H, W, C), e["codes"], e["alpha"], O, R, S, L["stride"], L["pad"],
+                         e["g"], prepared=e["prep"], y=e["y"])
+
+    def _pool(self, name):
+        F = self.torch.nn.functional
+        p = F.max_pool2d(self.layers[name]["y"].permute(0, 3, 1, 2), 3, 2)
+        self.pooled[name].copy_(p.permute(0, 2, 3, 1))
+        return self.pooled[name]
+
+    def forward(self, fused=False):
+        """fused=False: every layer's input quantized with a dynamic scale;
+        fused=True (after calibrate()): conv3 -> conv5 and fc6 -> fc8 write
+        the next layer's codes at its static scale, and the layers after a
+        pooling quantize their input with a dynamic scale."""
+        Ls = self.layers
+        self._layer(Ls["conv1"])
+        self._quant(self._pool("conv1"), Ls["conv2"])
+        self._layer(Ls["conv2"])
+        self._quant(self._pool("conv2"), Ls["conv3"])
+        chain = (("conv3", "conv4"), ("conv4", "conv5"))
+        for i, (a, b) in enumerate(chain):
+            sx = Ls[a]["sx_static"] if (fused and i > 0) else None
+            if fused:
+                self._layer(Ls[a], sx=sx, nxt=Ls[b])
+            else:
+                self._layer(Ls[a])
+                self._quant(Ls[a]["y"], Ls[b])
+        self._layer(Ls["conv5"], sx=Ls["conv5"]["sx_static"] if fused else None)
+        self._quant(self._pool("conv5").reshape(Ls["fc6"]["L"]["B"], -1), Ls["fc6"])
+        for i, (a, b) in enumerate((("fc6", "fc7"), ("fc7", "fc8"))):
+            sx = Ls[a]["sx_static"] if (fused and i > 0) else None
+            if fused:
+                self._layer(Ls[a], sx=sx, nxt=Ls[b])
+            else:
+                self._layer(Ls[a])
+                self._quant(Ls[a]["y"], Ls[b])
+        self._layer(Ls["fc8"], sx=Ls["fc8"]["sx_static"] if fused else None)
+        return self.logits
+
+
+def alexnet_chain_measure(torch, fgq, fi, batch=64, G=4, bits=8, reps=10, in_flight=3):
+    """End-to-end AlexNet forward passes (AlexNetChain), with fp32 group
+    scales and as the paper's pipeline, one batch and `in_flight` batches
+    at a time (as chain_measure)."""
+    out = {"workload": f"AlexNet forward pass, batch {batch}, 227x227, G={G}, u{bits}: every layer's "
+                       "quantization and FGQ layer and the torch max pooling in one graph; fused: conv3-conv5 "
+                       "and fc6-fc8 write the next layer's codes at calibrated static scales"}
+    for key, dfp in (("fp32_scales", False), ("paper_pipeline", True)):
+        nets = [AlexNetChain(torch, fgq, fi, G, bits, batch, dfp=dfp) for _ in range(in_flight)]
+        for n in nets:
+            n.calibrate()
+        out[key] = _time_nets(torch, nets, reps)
+        out[key]["direct_kernel_layers"] = nets[0].direct_layers
+        del nets
+        torch.cuda.empty_cache()
     return out
 
 
@@ -1293,6 +1454,7 @@ def main():
     if not args.no_stacks:
         log("[bench] AlexNet-shaped layers, batch 64, G=4, u8")
         out["alexnet_b64_g4_u8"] = alexnet_measure(torch, fgq, fi)
+        out["alexnet_b64_g4_u8"]["end_to_end"] = alexnet_chain_measure(torch, fgq, fi)
         log(f"[bench] AlexNet: sum {out['alexnet_b64_g4_u8']['sum_us']} us, "
             f"paper pipeline {out['alexnet_b64_g4_u8']['sum_paper_pipeline_us']} us")
     if not args.no_cpu:

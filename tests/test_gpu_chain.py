@@ -214,3 +214,70 @@ def test_paper_pipeline_forward_layer_by_layer(depth, G, bits, hw):
             net._conv(e, sx=e["sx_static"] if (i == 2 or k > 0) else None)
             q2, _ = fgq.fgq_quantize_act(e["y"], bits, scale_in=nxt["sx_static"])
             np.testing.assert_array_equal(host(nxt["q"]), host(q2), err_msg=f"{p}.c{j}")
+
+
+def maxpool3s2_valid(a):
+    """3x3 max pooling, stride 2, no padding, of an NHWC array."""
+    B, H, W, C = a.shape
+    Ho, Wo = (H - 3) // 2 + 1, (W - 3) // 2 + 1
+    out = np.full((B, Ho, Wo, C), -np.inf, np.float32)
+    for r in range(3):
+        for s in range(3):
+            out = np.maximum(out, a[:, r:r + 2 * Ho:2, s:s + 2 * Wo:2])
+    return out
+
+
+@pytest.mark.parametrize("dfp", [False, True], ids=["fp32-scales", "paper-pipeline"])
+def test_alexnet_forward_layer_by_layer(dfp):
+    """AlexNet on the library, every layer checked on the codes the GPU fed
+    it: against the oracle's layer (1e-5 of the summand magnitude with fp32
+    group scales; bit-exact with fixed-point scales and the 8-bit-weight
+    first layer), every quantization bit-exact, the pooling against numpy;
+    the fused form's codes equal the layer then a separate quantization."""
+    bits, G = 8, 4
+    net = bench.AlexNetChain(torch, fgq, fi, G, bits, 2, tag="alexnet-test", dfp=dfp)
+    assert np.isfinite(host(net.forward())).all()
+    for L in net.convs:
+        name = L["name"]
+        e = net.layers[name]
+        B, H, W, C, O, R, S = (L[k] for k in ("B", "H", "W", "C", "O", "R", "S"))
+        w = fi.he_weights(O, C, R, S, "alexnet-test", name)
+        if name == "conv1":
+            w[:, 3:] = 0.0
+        q, sx = host(e["q"]), host(e["sx"])[0]
+        st, pd = (L["stride"],) * 2, (L["pad"],) * 2
+        y = host(e["y"]).reshape(-1, O)
+        t, a, _ = oracle.ternarize(w, e["g"])
+        if dfp:
+            if name == "conv1":
+                W8, fl = oracle.w8_quantize(w)
+                y_ref = oracle.conv2d_w8(q, bits, sx, (B, H, W, C), W8, fl, O, R, S, st, pd)
+            else:
+                A, fl = oracle.dfp_alpha(a, 8)
+                y_ref = oracle.conv2d_dfp(q, bits, sx, (B, H, W, C), oracle.pack_codes(t), A, fl, O, R, S, st, pd,
+                                          e["g"])
+            np.testing.assert_array_equal(y.view(np.uint32), y_ref.reshape(-1, O).astype(np.float32).view(np.uint32),
+                                          err_msg=name)
+        else:
+            rows = np.arange(y.shape[0], dtype=np.int64)
+            y_ref, mag = oracle.conv2d_rows(q, bits, sx, (B, H, W, C), oracle.pack_codes(t), a, O, R, S, st, pd,
+                                            e["g"], rows)
+            assert np.all(np.abs(y.astype(np.float64) - y_ref) <= TOL * mag), name
+    # pooling and the quantization of every layer input
+    Ls = net.layers
+    for a, b in (("conv1", "conv2"), ("conv2", "conv3"), ("conv5", "fc6")):
+        np.testing.assert_array_equal(host(net.pooled[a]), maxpool3s2_valid(host(Ls[a]["y"])), err_msg=a)
+        q_ref, s_ref = oracle.quantize_act(host(net.pooled[a]), bits)
+        np.testing.assert_array_equal(host(Ls[b]["q"]), q_ref, err_msg=b)
+    for a, b in (("conv3", "conv4"), ("conv4", "conv5"), ("fc6", "fc7"), ("fc7", "fc8")):
+        q_ref, s_ref = oracle.quantize_act(host(Ls[a]["y"]), bits)
+        assert host(Ls[b]["sx"])[0] == np.float32(s_ref), b
+        np.testing.assert_array_equal(host(Ls[b]["q"]), q_ref, err_msg=b)
+    # the fused form
+    net.calibrate()
+    assert np.isfinite(host(net.forward(fused=True))).all()
+    for i, (a, b) in enumerate((("conv3", "conv4"), ("conv4", "conv5"), ("fc6", "fc7"), ("fc7", "fc8"))):
+        e = Ls[a]
+        net._layer(e, sx=e["sx_static"] if i in (1, 3) else None)  # the same layer, fp32 output
+        q2, _ = fgq.fgq_quantize_act(e["y"], bits, scale_in=Ls[b]["sx_static"])
+        np.testing.assert_array_equal(host(Ls[b]["q"]), host(q2), err_msg=b)
